@@ -1,0 +1,173 @@
+"""CPU oracle for the FoldQuantVLA runtime quantized projection.
+
+TEST INFRASTRUCTURE.  Only tests/, the smoke check and the benchmark's
+cpu_baseline leg may import this package.  It shares no code with the GPU
+library and never imports it; it takes plain numpy arrays / CPU tensors.
+
+Parts:
+  * fq_oracle.c (via ctypes): the fp32 contract of the runtime prologue
+    (blockwise FWHT butterfly, per-token absmax, quantize; Sec. III-C, eq. (5)),
+    canonical INT4 packing, the brute-force int64 contraction and the double
+    rescale (eq. (8)).
+  * definitions.py: float64 definitions written out with explicit matrices
+    (Sylvester H_b, block rotation R, eq. (2) fold, eq. (5), eq. (8)).
+  * exact.py: exact rational arithmetic of eq. (5) for tiny inputs.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import numpy as np
+
+from . import build as _build
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(_build.LIB) or os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC):
+            _build.build()
+        lib = ctypes.CDLL(_build.LIB)
+        i64, i32, f32 = ctypes.c_int64, ctypes.c_int, ctypes.c_float
+        vp = ctypes.c_void_p
+        lib.fqo_fwht_quant_bf16.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp, vp, vp]
+        lib.fqo_fwht_quant_f32.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp, vp, vp]
+        lib.fqo_pack_int4.argtypes = [vp, i64, i64, vp]
+        lib.fqo_gemm_i64.argtypes = [vp, vp, i64, i64, i64, vp]
+        lib.fqo_dequant.argtypes = [vp, vp, vp, vp, i64, i64, vp]
+        lib.fqo_fwht_block_f32.argtypes = [vp, i64]
+        lib.fqo_fwht_block_f32.restype = None
+        lib.fqo_inv_sqrt_b.argtypes = [i64]
+        lib.fqo_inv_sqrt_b.restype = f32
+        lib.fqo_max_threads.restype = i32
+        lib.fqo_set_threads.argtypes = [i32]
+        lib.fqo_set_threads.restype = None
+        for name in ("fqo_fwht_quant_bf16", "fqo_fwht_quant_f32", "fqo_pack_int4", "fqo_gemm_i64",
+                     "fqo_dequant"):
+            getattr(lib, name).restype = i32
+        _LIB = lib
+    return _LIB
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise ValueError(f"oracle {what}: bad arguments")
+
+
+def max_threads() -> int:
+    return int(_lib().fqo_max_threads())
+
+
+def set_threads(n: int) -> None:
+    _lib().fqo_set_threads(int(n))
+
+
+def inv_sqrt_b(b: int) -> np.float32:
+    """c_b, the float nearest to 1/sqrt(b)."""
+    return np.float32(_lib().fqo_inv_sqrt_b(int(b)))
+
+
+def fwht_block(v: np.ndarray) -> np.ndarray:
+    """fp32 butterfly FWHT of one block (length = power of two), unnormalized."""
+    out = np.ascontiguousarray(v, dtype=np.float32).copy()
+    _lib().fqo_fwht_block_f32(_ptr(out), out.size)
+    return out
+
+
+def bf16_bits(x) -> np.ndarray:
+    """uint16 bit patterns of a bf16 torch tensor (no conversion)."""
+    import torch
+    assert x.dtype == torch.bfloat16
+    return x.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def fwht_quant(x, b: int, bits: int, clip_ratio: float = 1.0,
+               chan_mult: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Runtime prologue on tokens (Alg. 1 runtime; eq. (5)).
+
+    x: bf16 torch tensor [M, K] or uint16 bit array, or float32 array [M, K].
+    chan_mult: optional fp32 [K] multiplier applied before the rotation.
+    Returns (codes int8 [M, K] unpacked, delta float32 [M]).
+    """
+    lib = _lib()
+    if not isinstance(x, np.ndarray):
+        x = bf16_bits(x)
+    M, K = x.shape
+    codes = np.zeros((M, K), dtype=np.int8)
+    delta = np.zeros(M, dtype=np.float32)
+    scratch = np.zeros(max(1, max_threads()) * max(K, 1), dtype=np.float32)
+    cm = None if chan_mult is None else np.ascontiguousarray(chan_mult, dtype=np.float32)
+    if x.dtype == np.uint16:
+        xx = np.ascontiguousarray(x)
+        rc = lib.fqo_fwht_quant_bf16(_ptr(xx), K, _ptr(cm), M, K, b, bits, clip_ratio,
+                                     _ptr(codes), _ptr(delta), _ptr(scratch))
+    elif x.dtype == np.float32:
+        xx = np.ascontiguousarray(x)
+        rc = lib.fqo_fwht_quant_f32(_ptr(xx), K, _ptr(cm), M, K, b, bits, clip_ratio,
+                                    _ptr(codes), _ptr(delta), _ptr(scratch))
+    else:
+        raise TypeError(f"unsupported dtype {x.dtype}")
+    _check(rc, "fwht_quant")
+    return codes, delta
+
+
+def quantize_weights(w: np.ndarray, b: int, bits: int,
+                     col_scale: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Offline fold + round-to-nearest (Alg. 1 offline; eq. (2) with T = R S^-1).
+
+    Row j of the folded weight W S R^T is R (s . w_j); it is rounded with the same
+    per-row rule as a token at r = 1.  Returns (codes int8 [N, K], s_w float32 [N]).
+    """
+    return fwht_quant(np.ascontiguousarray(w, dtype=np.float32), b, bits, 1.0, col_scale)
+
+
+def pack_int4(codes: np.ndarray) -> np.ndarray:
+    """Canonical nibble packing: channel 2i -> low nibble of byte i."""
+    codes = np.ascontiguousarray(codes, dtype=np.int8)
+    M, K = codes.shape
+    out = np.zeros((M, K // 2), dtype=np.uint8)
+    _check(_lib().fqo_pack_int4(_ptr(codes), M, K, _ptr(out)), "pack_int4")
+    return out
+
+
+def gemm(qa: np.ndarray, qw: np.ndarray) -> np.ndarray:
+    """acc[t, j] = sum_c qa[t, c] qw[j, c] in int64 (eq. (8) accumulator)."""
+    qa = np.ascontiguousarray(qa, dtype=np.int8)
+    qw = np.ascontiguousarray(qw, dtype=np.int8)
+    M, K = qa.shape
+    N, K2 = qw.shape
+    assert K == K2
+    acc = np.zeros((M, N), dtype=np.int64)
+    _check(_lib().fqo_gemm_i64(_ptr(qa), _ptr(qw), M, N, K, _ptr(acc)), "gemm")
+    return acc
+
+
+def dequant(acc: np.ndarray, delta: np.ndarray, s_w: np.ndarray,
+            bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """y[t, j] = s_w[j] delta[t] acc[t, j] + bias[j] in double (eq. (8))."""
+    acc = np.ascontiguousarray(acc, dtype=np.int64)
+    M, N = acc.shape
+    y = np.zeros((M, N), dtype=np.float64)
+    d = np.ascontiguousarray(delta, dtype=np.float32)
+    s = np.ascontiguousarray(s_w, dtype=np.float32)
+    bb = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    _check(_lib().fqo_dequant(_ptr(acc), _ptr(d), _ptr(s), _ptr(bb), M, N, _ptr(y)), "dequant")
+    return y
+
+
+def linear(x, w_codes: np.ndarray, s_w: np.ndarray, b: int, bits: int,
+           clip_ratio: float = 1.0, smooth_inv: Optional[np.ndarray] = None,
+           bias: Optional[np.ndarray] = None):
+    """Whole runtime path of Alg. 1 for one consumer: returns (codes, delta, acc, y)."""
+    codes, delta = fwht_quant(x, b, bits, clip_ratio, smooth_inv)
+    acc = gemm(codes, w_codes)
+    y = dequant(acc, delta, s_w, bias)
+    return codes, delta, acc, y

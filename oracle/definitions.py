@@ -1,0 +1,83 @@
+"""Float64 definitions written out with explicit matrices (test infrastructure).
+
+Each function is the paper's formula evaluated directly, with no fast transform
+and no reordering, so it can be checked against the paper by eye:
+  * sylvester(b): H_b[i, j] = (-1)^popcount(i & j), the Sylvester +-1 matrix in
+    natural order (Sec. III-C).
+  * block_rotation(K, b): R = I_{K/b} (x) H_b / sqrt(b) (Sec. III-C).
+  * fold_weight(W, s, b): W~ = W S R^T, the fold-before consumer weight
+    (Sec. III-C, T = R S^-1 in eq. (3); eq. (2) with identity output transform).
+  * transform_tokens(X, s_inv, b): z_t = R S^-1 x_t.
+  * quantize_eq5(Z, bits, r): eq. (5) in float64 with the zero-token rule.
+  * integer_output(qw, s_w, qa, delta, bias): eq. (8).
+"""
+from __future__ import annotations
+
+from typing import Optional, Tuple
+
+import numpy as np
+
+
+def sylvester(b: int) -> np.ndarray:
+    """H_b with entries (-1)^popcount(i & j); b a power of two."""
+    assert b >= 1 and b & (b - 1) == 0
+    i = np.arange(b)[:, None]
+    j = np.arange(b)[None, :]
+    bits_and = i & j
+    parity = np.zeros_like(bits_and)
+    v = bits_and.copy()
+    while v.any():
+        parity ^= v & 1
+        v >>= 1
+    return np.where(parity == 1, -1.0, 1.0)
+
+
+def block_rotation(K: int, b: int) -> np.ndarray:
+    """R = I_{K/b} (x) H_b / sqrt(b), float64 [K, K]."""
+    assert K % b == 0
+    return np.kron(np.eye(K // b), sylvester(b) / np.sqrt(b))
+
+
+def transform_tokens(X: np.ndarray, b: int, s_inv: Optional[np.ndarray] = None) -> np.ndarray:
+    """z_t = R S^-1 x_t for every row x_t of X (float64 [M, K])."""
+    X = np.asarray(X, dtype=np.float64)
+    if s_inv is not None:
+        X = X * np.asarray(s_inv, dtype=np.float64)[None, :]
+    R = block_rotation(X.shape[1], b)
+    return X @ R.T
+
+
+def fold_weight(W: np.ndarray, b: int, s: Optional[np.ndarray] = None) -> np.ndarray:
+    """W~ = W S R^T (float64 [N, K])."""
+    W = np.asarray(W, dtype=np.float64)
+    if s is not None:
+        W = W * np.asarray(s, dtype=np.float64)[None, :]
+    R = block_rotation(W.shape[1], b)
+    return W @ R.T
+
+
+def quantize_eq5(Z: np.ndarray, bits: int, r: float = 1.0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Eq. (5) per row: delta = r ||z||_inf / q, codes = clip(round(z / delta), -q, q).
+
+    Returns (codes int64 [M, K], delta float64 [M], ratio float64 [M, K] = z / delta)
+    so callers can see how close each element sits to a rounding tie.
+    A zero row gives codes 0 and delta 0.
+    """
+    Z = np.asarray(Z, dtype=np.float64)
+    q = 2 ** (bits - 1) - 1
+    amax = np.abs(Z).max(axis=1) if Z.shape[1] else np.zeros(Z.shape[0])
+    delta = r * amax / q
+    safe = np.where(delta > 0, delta, 1.0)
+    ratio = np.where(delta[:, None] > 0, Z / safe[:, None], 0.0)
+    codes = np.clip(np.rint(ratio), -q, q).astype(np.int64)
+    return codes, delta, ratio
+
+
+def integer_output(qw: np.ndarray, s_w: np.ndarray, qa: np.ndarray, delta: np.ndarray,
+                   bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """Eq. (8): y[t, j] = s_w[j] delta[t] sum_c qw[j, c] qa[t, c] + b_j (float64 [M, N])."""
+    acc = np.asarray(qa, dtype=np.int64) @ np.asarray(qw, dtype=np.int64).T
+    y = acc.astype(np.float64) * np.asarray(s_w, np.float64)[None, :] * np.asarray(delta, np.float64)[:, None]
+    if bias is not None:
+        y = y + np.asarray(bias, np.float64)[None, :]
+    return y

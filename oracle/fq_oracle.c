@@ -1,0 +1,193 @@
+/*
+ * Plain CPU oracle for the FoldQuantVLA runtime quantized projection.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this file; only the tests, the smoke check and the benchmark's CPU
+ * baseline do.  It shares no code, header or constant with the GPU path.
+ *
+ * It follows the paper step by step, with no blocking or fusion:
+ *   - Sec. III-C: block Hadamard rotation R = I (x) H_b / sqrt(b), H_b the
+ *     Sylvester +-1 matrix, applied as a fast Walsh-Hadamard transform.
+ *   - Eq. (5), Sec. III-E: dynamic per-token symmetric quantization,
+ *     delta_t = r * ||z_t||_inf / q, q = 2^(bits-1) - 1, codes clip(round(z/delta)),
+ *     and the zero-token rule (z_t = 0 gives codes 0 and delta 0; Alg. 1 runtime).
+ *   - Eq. (8), Sec. III-F: integer output y_jt = s_j * delta_t * sum_c qW_jc qA_ct + b_j.
+ *
+ * Floating-point contract (the paper fixes no precision or summation order for
+ * these steps; the readings are listed in the design notes):
+ *   * the transform runs in fp32 as an in-place butterfly with stages
+ *     h = 1, 2, 4, ..., b/2, each pair (a, c) -> (a + c, a - c), on the
+ *     UNNORMALIZED Sylvester matrix; the 1/sqrt(b) factor is carried by delta
+ *     (by Prop. 2 this leaves the codes unchanged in exact arithmetic);
+ *   * the per-token division z/delta is one fp32 reciprocal per token,
+ *     inv = q / (r*A), followed by one fp32 multiply per element;
+ *   * round() is round-half-to-even;
+ *   * delta = ((r*A) * c_b) / q in fp32, c_b = the float nearest 1/sqrt(b).
+ * Build with -ffp-contract=off so no multiply-add is fused.
+ *
+ * The integer contraction is a brute-force int64 triple loop (eq. (8) is the
+ * definition), and the dequantization is done in double.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+static int omp_thread_slot(void) { return omp_get_thread_num(); }
+int fqo_max_threads(void) { return omp_get_max_threads(); }
+void fqo_set_threads(int n) { if (n > 0) omp_set_num_threads(n); }
+#else
+static int omp_thread_slot(void) { return 0; }
+int fqo_max_threads(void) { return 1; }
+void fqo_set_threads(int n) { (void)n; }
+#endif
+
+#define FQO_OK 0
+#define FQO_BAD_ARG 1
+
+static float bf16_bits_to_float(uint16_t h) {
+    uint32_t u = ((uint32_t)h) << 16; /* bf16 is the top half of an fp32 */
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return f;
+}
+
+static int is_pow2(int64_t b) { return b >= 1 && (b & (b - 1)) == 0; }
+
+/* c_b: the float nearest to 1/sqrt(b) (Sec. III-C normalization of H_b). */
+float fqo_inv_sqrt_b(int64_t b) {
+    return (float)(1.0 / sqrt((double)b));
+}
+
+/* Unnormalized Sylvester FWHT of one block of length b, in place, fp32.
+ * Stage h pairs index j with j + h inside every 2h-aligned group. */
+void fqo_fwht_block_f32(float *v, int64_t b) {
+    for (int64_t h = 1; h < b; h *= 2) {
+        for (int64_t i = 0; i < b; i += 2 * h) {
+            for (int64_t j = i; j < i + h; ++j) {
+                float a = v[j];
+                float c = v[j + h];
+                v[j] = a + c;
+                v[j + h] = a - c;
+            }
+        }
+    }
+}
+
+/* Eq. (5) on one transformed token u[0..K) (unnormalized coordinates). */
+static void quantize_token(const float *u, int64_t K, int bits, float r, float cb,
+                           int8_t *code, float *delta) {
+    const int q = (1 << (bits - 1)) - 1;
+    float A = 0.0f;
+    for (int64_t c = 0; c < K; ++c) {
+        float m = fabsf(u[c]);
+        if (m > A) A = m;
+    }
+    if (A == 0.0f) { /* zero-token rule */
+        for (int64_t c = 0; c < K; ++c) code[c] = 0;
+        *delta = 0.0f;
+        return;
+    }
+    const float rA = r * A;
+    const float inv = (float)q / rA;
+    for (int64_t c = 0; c < K; ++c) {
+        float t = u[c] * inv;
+        float k = rintf(t); /* round half to even (default rounding mode) */
+        if (k > (float)q) k = (float)q;
+        if (k < (float)-q) k = (float)-q;
+        code[c] = (int8_t)k;
+    }
+    *delta = (rA * cb) / (float)q;
+}
+
+static int check_args(int64_t M, int64_t K, int64_t b, int bits, float r, int64_t ld) {
+    if (M < 0 || K < 1 || !is_pow2(b) || K % b != 0) return FQO_BAD_ARG;
+    if (bits != 4 && bits != 8) return FQO_BAD_ARG;
+    if (!(r > 0.0f && r <= 1.0f)) return FQO_BAD_ARG;
+    if (ld < K) return FQO_BAD_ARG;
+    return FQO_OK;
+}
+
+/* One row: optional per-channel multiplier, blockwise FWHT, quantize. */
+static void transform_quantize_row(float *v, const float *chan_mult, int64_t K, int64_t b,
+                                   int bits, float r, float cb, int8_t *code, float *delta) {
+    if (chan_mult)
+        for (int64_t c = 0; c < K; ++c) v[c] = v[c] * chan_mult[c];
+    for (int64_t k0 = 0; k0 < K; k0 += b) fqo_fwht_block_f32(v + k0, b);
+    quantize_token(v, K, bits, r, cb, code, delta);
+}
+
+/* Activation prologue (Alg. 1 runtime, first two steps) on bf16 tokens.
+ * x: [M, ldx] bf16 bit patterns; chan_mult: [K] or NULL (fold-before S^-1);
+ * codes: [M, K] int8 (unpacked); delta: [M]; scratch: [nthreads * K] floats. */
+int fqo_fwht_quant_bf16(const uint16_t *x, int64_t ldx, const float *chan_mult, int64_t M,
+                        int64_t K, int64_t b, int bits, float r, int8_t *codes, float *delta,
+                        float *scratch) {
+    if (check_args(M, K, b, bits, r, ldx)) return FQO_BAD_ARG;
+    const float cb = fqo_inv_sqrt_b(b);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < M; ++t) {
+        float *v = scratch + (int64_t)omp_thread_slot() * K;
+        for (int64_t c = 0; c < K; ++c) v[c] = bf16_bits_to_float(x[t * ldx + c]);
+        transform_quantize_row(v, chan_mult, K, b, bits, r, cb, codes + t * K, delta + t);
+    }
+    return FQO_OK;
+}
+
+/* Same on fp32 rows.  With r = 1 and chan_mult = s (fold-before S), this is the
+ * offline weight rounding: row j of W S R^T equals R (s . w_j) because H_b is
+ * symmetric, and RTN with a per-output-channel scale (Sec. III-E/F, Alg. 1
+ * offline) rounds it with the same per-row rule. */
+int fqo_fwht_quant_f32(const float *x, int64_t ldx, const float *chan_mult, int64_t M, int64_t K,
+                       int64_t b, int bits, float r, int8_t *codes, float *delta, float *scratch) {
+    if (check_args(M, K, b, bits, r, ldx)) return FQO_BAD_ARG;
+    const float cb = fqo_inv_sqrt_b(b);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < M; ++t) {
+        float *v = scratch + (int64_t)omp_thread_slot() * K;
+        memcpy(v, x + t * ldx, (size_t)K * sizeof(float));
+        transform_quantize_row(v, chan_mult, K, b, bits, r, cb, codes + t * K, delta + t);
+    }
+    return FQO_OK;
+}
+
+/* Canonical signed-INT4 nibble packing: byte i of a row holds channel 2i in the
+ * low nibble and channel 2i+1 in the high nibble, two's complement. */
+int fqo_pack_int4(const int8_t *codes, int64_t M, int64_t K, uint8_t *out) {
+    if (M < 0 || K < 0 || K % 2) return FQO_BAD_ARG;
+    for (int64_t t = 0; t < M; ++t)
+        for (int64_t i = 0; i < K / 2; ++i) {
+            uint8_t lo = (uint8_t)codes[t * K + 2 * i] & 0x0F;
+            uint8_t hi = (uint8_t)codes[t * K + 2 * i + 1] & 0x0F;
+            out[t * (K / 2) + i] = (uint8_t)(lo | (hi << 4));
+        }
+    return FQO_OK;
+}
+
+/* Eq. (8) accumulator: acc[t, j] = sum_c qA[t, c] * qW[j, c], brute force in int64. */
+int fqo_gemm_i64(const int8_t *qa, const int8_t *qw, int64_t M, int64_t N, int64_t K,
+                 int64_t *acc) {
+    if (M < 0 || N < 0 || K < 0) return FQO_BAD_ARG;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < M; ++t)
+        for (int64_t j = 0; j < N; ++j) {
+            int64_t s = 0;
+            for (int64_t c = 0; c < K; ++c) s += (int64_t)qa[t * K + c] * (int64_t)qw[j * K + c];
+            acc[t * N + j] = s;
+        }
+    return FQO_OK;
+}
+
+/* Eq. (8) rescale: y[t, j] = s_w[j] * delta[t] * acc[t, j] + bias[j], in double. */
+int fqo_dequant(const int64_t *acc, const float *delta, const float *s_w, const float *bias,
+                int64_t M, int64_t N, double *y) {
+    if (M < 0 || N < 0) return FQO_BAD_ARG;
+    for (int64_t t = 0; t < M; ++t)
+        for (int64_t j = 0; j < N; ++j) {
+            double v = (double)s_w[j] * (double)delta[t] * (double)acc[t * N + j];
+            if (bias) v += (double)bias[j];
+            y[t * N + j] = v;
+        }
+    return FQO_OK;
+}

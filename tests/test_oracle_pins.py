@@ -1,0 +1,315 @@
+"""Pins for the CPU oracle against what the paper and the mathematics fix.
+
+None of these compares the oracle with itself: each check uses a library
+routine, an exact rational computation, a closed form or an invariant that a
+plausible mistake in the oracle (a dropped term, a wrong sign or index, a
+transposed operand, a wrong rounding rule) would break.
+"""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.linalg
+import torch
+
+import oracle
+from oracle import definitions as D
+from oracle import exact
+from paper_2609_24433_amd import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "worked_examples.json")
+BLOCKS = [1, 2, 4, 8, 16, 32, 64, 128, 256]
+
+
+# --- Sec. III-C: Sylvester Hadamard and the block rotation -------------------------------------
+
+@pytest.mark.parametrize("b", BLOCKS)
+def test_sylvester_matches_library_and_is_orthogonal(b):
+    H = D.sylvester(b)
+    np.testing.assert_array_equal(H, scipy.linalg.hadamard(b).astype(np.float64))
+    np.testing.assert_array_equal(H @ H.T, b * np.eye(b))  # H H^T = b I, exact in float64
+    np.testing.assert_array_equal(H, H.T)
+
+
+def test_block_rotation_is_orthonormal_block_diagonal():
+    R = D.block_rotation(256, 64)
+    np.testing.assert_allclose(R @ R.T, np.eye(256), atol=1e-12)
+    assert np.count_nonzero(R[:64, 64:]) == 0 and np.count_nonzero(R[64:128, :64]) == 0
+
+
+@pytest.mark.parametrize("b", BLOCKS)
+def test_butterfly_matches_explicit_matrix(b):
+    rng = np.random.default_rng(b)
+    for _ in range(4):
+        v = rng.standard_normal(b).astype(np.float32)
+        got = oracle.fwht_block(v).astype(np.float64)
+        want = D.sylvester(b) @ v.astype(np.float64)
+        scale = np.abs(v).sum()
+        assert np.max(np.abs(got - want)) <= 1e-6 * scale * np.log2(max(b, 2))
+
+
+@pytest.mark.parametrize("b", BLOCKS)
+def test_butterfly_bit_exact_on_integers(b):
+    # all partial sums stay far below 2^24, so the fp32 butterfly must be exact
+    rng = np.random.default_rng(100 + b)
+    v = rng.integers(-1000, 1001, size=b).astype(np.float32)
+    got = oracle.fwht_block(v)
+    want = D.sylvester(b) @ v.astype(np.float64)
+    np.testing.assert_array_equal(got.astype(np.float64), want)
+
+
+@pytest.mark.parametrize("b", [2, 16, 128, 256])
+def test_butterfly_preserves_squared_norm(b):
+    v = np.random.default_rng(7).standard_normal(b).astype(np.float32)
+    u = oracle.fwht_block(v).astype(np.float64)
+    assert abs((u @ u) - b * float(v.astype(np.float64) @ v.astype(np.float64))) <= 1e-5 * b * (v @ v)
+
+
+def test_inv_sqrt_b_is_nearest_float():
+    for b in BLOCKS:
+        c = oracle.inv_sqrt_b(b)
+        exact_sq = Fraction(1, b)
+        # c is the nearest float to 1/sqrt(b): its neighbours bracket it farther away
+        lo = np.nextafter(c, np.float32(0))
+        hi = np.nextafter(c, np.float32(1))
+        dist = lambda f: abs(Fraction(float(f)) ** 2 - exact_sq)  # monotone in |f - 1/sqrt(b)| near it
+        assert dist(c) <= dist(lo) and dist(c) <= dist(hi)
+    assert oracle.inv_sqrt_b(64) == np.float32(0.125)
+    assert oracle.inv_sqrt_b(256) == np.float32(0.0625)
+
+
+# --- eq. (5): worked examples in exact rational arithmetic ---------------------------------------
+
+def _golden_cases():
+    with open(GOLDEN) as f:
+        return json.load(f)["cases"]
+
+
+@pytest.mark.parametrize("case", _golden_cases(), ids=lambda c: c["pins"][:40])
+def test_worked_examples(case):
+    x = np.array([case["x"]], dtype=np.float32)
+    r = case["r"][0] / case["r"][1]
+    codes, delta = oracle.fwht_quant(x, case["b"], case["bits"], r)
+    assert codes[0].tolist() == case["codes"], case["pins"]
+    rAq = Fraction(*case["rA_over_q"])
+    # delta = (r A / q) / sqrt(b), rounded in fp32 a few times: within 3 ulp
+    want = float(rAq) / np.sqrt(case["b"])
+    if want == 0:
+        assert delta[0] == 0
+    else:
+        assert abs(float(delta[0]) - want) <= 3 * np.spacing(np.float32(want))
+
+
+def test_golden_fixture_is_reproducible_from_exact_arithmetic():
+    for case in _golden_cases():
+        codes, rAq, _ = exact.quantize_token(case["x"], case["b"], case["bits"],
+                                             Fraction(*case["r"]))
+        assert codes == case["codes"]
+        assert rAq == Fraction(*case["rA_over_q"])
+
+
+def test_exact_ties_round_half_to_even_random():
+    # A = 14 after the transform with q = 7 makes inv = 1/2 exact, so every odd
+    # u gives an exact tie that the fp32 contract must resolve to the even code.
+    rng = np.random.default_rng(3)
+    for _ in range(20):
+        v = rng.integers(-13, 14, size=8).astype(np.float32)
+        v[rng.integers(0, 8)] = 14.0 * rng.choice([-1, 1])
+        codes, delta = oracle.fwht_quant(v[None, :], 1, 4)
+        ref, _, _ = exact.quantize_token(v.tolist(), 1, 4)
+        assert codes[0].tolist() == ref
+
+
+@pytest.mark.parametrize("b", [1, 2, 8, 32, 64, 128])
+@pytest.mark.parametrize("bits", [4, 8])
+def test_codes_match_exact_rational_away_from_ties(b, bits):
+    rng = np.random.default_rng(b * 10 + bits)
+    K = max(b, 16)
+    for _ in range(6):
+        x = (rng.standard_normal(K) * 4).astype(np.float32)
+        codes, delta = oracle.fwht_quant(x[None, :], b, bits)
+        ref, rAq, ratios = exact.quantize_token(x.tolist(), b, bits)
+        for c, rc, t in zip(codes[0].tolist(), ref, ratios):
+            frac = abs(float(t) - np.floor(float(t)) - 0.5)
+            if frac > 1e-5:
+                assert c == rc
+        want = float(rAq) / np.sqrt(b)
+        assert abs(float(delta[0]) - want) <= 3 * np.spacing(np.float32(want))
+
+
+# --- eq. (5) against its float64 definition on synthetic token rows ------------------------------
+
+@pytest.mark.parametrize("b", [1, 16, 64, 128, 256])
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("r", [1.0, 0.8])
+def test_quant_matches_float64_definition(b, bits, r):
+    x = synth.activations(24, 1024, seed=11, outlier_frac=0.01, outlier_scale=30.0)
+    codes, delta = oracle.fwht_quant(x, b, bits, r)
+    Z = D.transform_tokens(x.float().numpy(), b)
+    ref, dref, ratio = D.quantize_eq5(Z, bits, r)
+    np.testing.assert_allclose(delta, dref, rtol=1e-6)
+    near_tie = np.abs(np.abs(ratio - np.floor(ratio)) - 0.5) < 1e-4
+    mism = (codes != ref) & ~near_tie
+    assert not mism.any()
+    assert np.all(np.abs(codes.astype(np.int64) - ref) <= 1)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_quant_range_error_bound_and_full_scale(bits):
+    q = 2 ** (bits - 1) - 1
+    x = synth.activations(32, 2048, seed=5, outlier_frac=0.005, outlier_scale=50.0)
+    codes, delta = oracle.fwht_quant(x, 128, bits)
+    assert codes.min() >= -q and codes.max() <= q
+    assert np.all(np.abs(codes).max(axis=1) == q)  # r = 1: the absmax element maps to +-q
+    Z = D.transform_tokens(x.float().numpy(), 128)
+    err = np.abs(Z - delta[:, None].astype(np.float64) * codes)
+    assert np.all(err <= delta[:, None] * 0.5 * (1 + 1e-5))
+
+
+def test_clip_ratio_saturates():
+    x = synth.activations(8, 512, seed=9, outlier_frac=0.01, outlier_scale=30.0)
+    codes, delta = oracle.fwht_quant(x, 64, 4, 0.5)
+    Z = D.transform_tokens(x.float().numpy(), 64)
+    ref, dref, ratio = D.quantize_eq5(Z, 4, 0.5)
+    assert np.all((np.abs(ratio) > 7.5) <= (np.abs(codes) == 7))
+    np.testing.assert_array_equal(np.abs(codes) == 7, np.abs(ref) == 7)
+
+
+def test_zero_token_rule():
+    x = synth.activations(6, 256, seed=1)
+    x[2].zero_()
+    x[5].zero_()
+    codes, delta = oracle.fwht_quant(x, 32, 4)
+    assert delta[2] == 0 and delta[5] == 0
+    assert not codes[2].any() and not codes[5].any()
+    assert np.all(delta[[0, 1, 3, 4]] > 0)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_positive_homogeneity_bit_exact(bits):
+    # Prop. 2: scaling a token by lambda > 0 scales delta by lambda and keeps the codes.
+    x = synth.activations(16, 1024, seed=21, outlier_frac=0.01, outlier_scale=30.0)
+    c0, d0 = oracle.fwht_quant(x, 128, bits)
+    for k in (-6, -1, 3, 9):
+        xs = (x.float() * 2.0 ** k).to(torch.bfloat16)  # exact: power-of-two scaling
+        c1, d1 = oracle.fwht_quant(xs, 128, bits)
+        np.testing.assert_array_equal(c1, c0)
+        np.testing.assert_array_equal(d1, d0 * np.float32(2.0 ** k))
+
+
+def test_b1_is_textbook_per_token_rtn():
+    x = synth.activations(16, 256, seed=4, dist="student_t3")
+    xf = x.float().numpy()
+    codes, delta = oracle.fwht_quant(x, 1, 4)
+    A = np.abs(xf).max(axis=1)
+    np.testing.assert_array_equal(delta, (A / np.float32(7)).astype(np.float32))
+    ratio = xf.astype(np.float64) / delta[:, None].astype(np.float64)
+    want = np.clip(np.rint(ratio), -7, 7)
+    ok = np.abs(np.abs(ratio - np.floor(ratio)) - 0.5) > 1e-4
+    np.testing.assert_array_equal(codes[ok], want[ok])
+
+
+def test_fold_before_multiplier():
+    x = synth.activations(8, 512, seed=31, outlier_frac=0.01, outlier_scale=30.0)
+    s_inv = synth.channel_vector(512, seed=32, low=0.25, high=4.0)
+    codes, delta = oracle.fwht_quant(x, 64, 4, 1.0, s_inv)
+    # the multiplier is rounded to fp32 once per element before the rotation
+    xm = (x.float().numpy() * s_inv).astype(np.float32)
+    Z = D.transform_tokens(xm, 64)
+    ref, dref, ratio = D.quantize_eq5(Z, 4)
+    ok = np.abs(np.abs(ratio - np.floor(ratio)) - 0.5) > 1e-4
+    np.testing.assert_array_equal(codes[ok], ref[ok])
+    np.testing.assert_allclose(delta, dref, rtol=1e-6)
+
+
+# --- eq. (2) / Sec. III-C fold, and the offline weight rounding ---------------------------------
+
+@pytest.mark.parametrize("b", [1, 8, 64, 128])
+def test_fold_identity_float64(b):
+    W = synth.weights(48, 256, seed=40).astype(np.float64)
+    X = synth.activations(10, 256, seed=41, outlier_frac=0.02, outlier_scale=30.0).double().numpy()
+    s = synth.channel_vector(256, seed=42, low=0.5, high=2.0).astype(np.float64)
+    Wt = D.fold_weight(W, b, s)
+    Z = D.transform_tokens(X, b, 1.0 / s)
+    np.testing.assert_allclose(Z @ Wt.T, X @ W.T, rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_weight_rounding_reconstructs_folded_weight(bits):
+    W = synth.weights(64, 512, seed=50)
+    gamma = synth.channel_vector(512, seed=51, low=0.5, high=1.5)
+    codes, s_w = oracle.quantize_weights(W, 128, bits, gamma)
+    Wt = D.fold_weight(W * gamma, 128)  # gamma pre-multiplied in fp32, as the contract does
+    err = np.abs(Wt - s_w[:, None].astype(np.float64) * codes)
+    assert np.all(err <= s_w[:, None] * 0.5 * (1 + 1e-5))
+    q = 2 ** (bits - 1) - 1
+    assert np.all(np.abs(codes).max(axis=1) == q)
+    np.testing.assert_allclose(s_w, np.abs(Wt).max(axis=1) / q, rtol=1e-6)
+
+
+def test_zero_weight_row():
+    W = synth.weights(4, 128, seed=60)
+    W[1] = 0
+    codes, s_w = oracle.quantize_weights(W, 64, 4)
+    assert s_w[1] == 0 and not codes[1].any()
+
+
+# --- eq. (8): integer contraction and rescale ---------------------------------------------------
+
+def test_gemm_matches_numpy_int64():
+    qa = synth.random_codes(37, 320, 8, seed=70)
+    qw = synth.random_codes(52, 320, 8, seed=71)
+    np.testing.assert_array_equal(oracle.gemm(qa, qw), qa.astype(np.int64) @ qw.astype(np.int64).T)
+
+
+def test_gemm_one_hot_and_operand_order():
+    qa = np.zeros((3, 64), np.int8)
+    qw = np.zeros((5, 64), np.int8)
+    qa[1, 10] = 3
+    qw[4, 10] = -7
+    qw[2, 11] = 5
+    acc = oracle.gemm(qa, qw)
+    want = np.zeros((3, 5), np.int64)
+    want[1, 4] = -21
+    np.testing.assert_array_equal(acc, want)
+
+
+def test_dequant_matches_eq8_and_zero_token_gives_bias():
+    qa = synth.random_codes(6, 128, 4, seed=80)
+    qa[3] = 0
+    qw = synth.random_codes(32, 128, 4, seed=81)
+    delta = synth.random_scales(6, seed=82)
+    delta[3] = 0
+    s_w = synth.random_scales(32, seed=83)
+    bias = synth.random_scales(32, seed=84, low=-1, high=1)
+    y = oracle.dequant(oracle.gemm(qa, qw), delta, s_w, bias)
+    np.testing.assert_allclose(y, D.integer_output(qw, s_w, qa, delta, bias), rtol=1e-13)
+    np.testing.assert_array_equal(y[3], bias.astype(np.float64))
+
+
+def test_pack_int4_canonical_nibbles():
+    codes = np.array([[1, -1, -7, 7, 0, -8 + 1, 3, -2]], dtype=np.int8)
+    packed = oracle.pack_int4(codes)
+    assert packed[0].tolist() == [0xF1, 0x79, 0x90, 0xE3]
+    # decode by hand: sign-extend each nibble
+    lo = (packed.astype(np.int16) & 0xF)
+    hi = (packed.astype(np.int16) >> 4)
+    lo = np.where(lo > 7, lo - 16, lo)
+    hi = np.where(hi > 7, hi - 16, hi)
+    np.testing.assert_array_equal(np.stack([lo, hi], -1).reshape(1, -1), codes)
+
+
+# --- the whole path: sanity of accuracy against the unquantized projection ---------------------
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_quantized_projection_tracks_float_projection(bits):
+    # accuracy versus W x is not pinned by the paper; this is a loose sanity bound
+    x = synth.activations(16, 1024, seed=90, outlier_frac=0.01, outlier_scale=30.0)
+    W = synth.weights(128, 1024, seed=91)
+    wc, s_w = oracle.quantize_weights(W, 64, bits)
+    _, _, _, y = oracle.linear(x, wc, s_w, 64, bits)
+    ref = x.double().numpy() @ W.astype(np.float64).T
+    cos = (y * ref).sum() / np.linalg.norm(y) / np.linalg.norm(ref)
+    assert cos > (0.97 if bits == 4 else 0.9995)
