@@ -1,0 +1,138 @@
+/*
+ * fq.h -- C ABI of the FoldQuantVLA runtime quantized projection on AMD MI355X (gfx950).
+ *
+ * The projection (Sec. III-E/F, Alg. 1 runtime) computes, for tokens x_t:
+ *   z_t   = R S^-1 x_t,  R = I_{K/b} (x) H_b / sqrt(b)   (block Hadamard, Sec. III-C)
+ *   qA_t, delta_t = per-token symmetric quantization of z_t       (eq. (5))
+ *   c_jt  = sum_c qW_jc qA_ct   (integer accumulation, INT32)     (eq. (8))
+ *   y_jt  = s_j delta_t c_jt + b_j                                 (eq. (8))
+ * against weights folded and rounded offline: W~ = W S R^T rounded per output
+ * channel to signed INT4 / INT8 codes qW with scales s (Alg. 1 offline).
+ *
+ * Conventions shared by every entry point:
+ *   - Every buffer argument is a DEVICE pointer owned by the caller, except where a
+ *     comment says otherwise.  The library never allocates or frees memory; scratch
+ *     space comes from a caller-provided workspace.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls enqueue work and
+ *     return without synchronizing.  Device-side faults surface at the caller's next
+ *     synchronization, as usual in HIP.
+ *   - Arguments are validated before anything is enqueued; a failed check returns a
+ *     status and enqueues nothing.  fq_last_error() (thread-local) then describes it.
+ *   - M = 0 (or N = 0) is a valid no-op.
+ *   - Layouts are row-major.  `ld*` arguments are row strides in elements.
+ *   - Shape limits: K % 128 == 0, 128 <= K <= 32768, N % 16 == 0, b a power of two
+ *     with 1 <= b <= 256 and K % b == 0, bits in {4, 8}, 0 < clip_ratio <= 1.
+ *   - Alignment: every pointer 16-byte aligned; ldx and ldy multiples of 8.
+ *
+ * Numerical contract of the prologue (so that codes are reproducible bit for bit):
+ *   the transform is an fp32 butterfly on the UNNORMALIZED Sylvester matrix with
+ *   stages h = 1, 2, ..., b/2, pairs (a, c) -> (a + c, a - c); A_t = max_c |u_tc|
+ *   over the whole row; inv = q / (r * A_t) (one correctly rounded fp32 division);
+ *   code = clamp(rne(u * inv), -q, q); delta_t = ((r * A_t) * c_b) / q with c_b
+ *   the float nearest 1/sqrt(b); a zero row gives codes 0 and delta 0.  No fused
+ *   multiply-adds.
+ */
+#ifndef FQ_H_
+#define FQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FQ_OK = 0,
+  FQ_ERR_NULL = 1,        /* a required pointer is NULL */
+  FQ_ERR_SHAPE = 2,       /* negative or inconsistent sizes, ld too small */
+  FQ_ERR_UNSUPPORTED = 3, /* sizes outside the supported range, bad b / bits / clip ratio */
+  FQ_ERR_ALIGN = 4,       /* pointer or leading dimension misaligned */
+  FQ_ERR_WORKSPACE = 5,   /* workspace missing or smaller than required */
+  FQ_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed */
+} fq_status;
+
+/* Runtime prologue, Alg. 1 runtime steps 1-2 (Sec. III-C transform, eq. (5)).
+ *   x_bf16     [M, ldx] bf16 tokens (only the first K columns are read).
+ *   smooth_inv [K] fp32 fold-before multiplier S^-1 (Sec. III-C), or NULL for S = I;
+ *              multiplied into x once, in fp32, before the rotation.
+ *   b          Hadamard block size; bits: 4 or 8 (q = 7 or 127); clip_ratio: r in eq. (5).
+ *   a_codes    output codes, canonical layout: bits = 8 -> int8 [M, K];
+ *              bits = 4 -> uint8 [M, K/2], byte i of a row = channel 2i in the low
+ *              nibble, channel 2i+1 in the high nibble (two's complement).
+ *   delta      output fp32 [M] per-token scales (0 for a zero token). */
+fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
+                        int64_t K, int b, int bits, float clip_ratio, void *a_codes, float *delta,
+                        void *stream);
+
+/* Offline weight fold and round-to-nearest, Alg. 1 offline (eq. (2), Sec. III-C/F).
+ *   w          [N, ldw] fp32 weights of one consumer (row j = output channel j).
+ *   col_scale  [K] fp32 S (fold-before smoothing, times a folded norm gain, eq. (4)),
+ *              or NULL; multiplied into each row once, in fp32, before the rotation.
+ *   Row j of W S R^T is R (s . w_j) because H_b is symmetric, so each row is rounded
+ *   with the prologue's contract at r = 1: w_codes int8 [N, K] in [-q, q] and
+ *   w_scale fp32 [N] (the per-output-channel s_j). */
+fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scale, int64_t N,
+                              int64_t K, int b, int bits, int8_t *w_codes, float *w_scale,
+                              void *stream);
+
+/* Bytes of the packed, kernel-native weight layout for an [N, K] matrix. */
+size_t fq_packed_weight_bytes(int64_t N, int64_t K, int bits);
+
+/* Pack int8 codes [N, K] (values in [-q, q]) into the kernel-native layout that the
+ * GEMM entry points read (Sec. III-F: packed signed-INT4 / INT8 weight codes).
+ * The layout is opaque; fq_unpack_weights inverts it exactly. */
+fq_status fq_pack_weights(const int8_t *w_codes, int64_t N, int64_t K, int bits, void *w_packed,
+                          void *stream);
+fq_status fq_unpack_weights(const void *w_packed, int64_t N, int64_t K, int bits, int8_t *w_codes,
+                            void *stream);
+
+/* Workspace bytes fq_gemm_w4a4 / fq_gemm_w8a8 need for this shape (may be 0). */
+size_t fq_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
+
+/* Integer GEMM with the eq. (8) rescale epilogue (Alg. 1 runtime, consumer loop).
+ *   a_codes   canonical activation codes as written by fq_fwht_quant
+ *             (w4a4: uint8 [M, K/2] nibbles; w8a8: int8 [M, K]).
+ *   delta     fp32 [M]; w_packed: from fq_pack_weights with the same bits;
+ *   w_scale   fp32 [N]; bias: fp32 [N] or NULL.
+ *   y_bf16    [M, ldy] bf16 output: y = bf16_rne(fp32(acc) * (w_scale[j] * delta[t]) + bias[j]).
+ *   acc_out   int32 [M, N] raw accumulators, or NULL (for verification).
+ *   ws        workspace of at least fq_gemm_workspace_bytes(M, N, K, bits) bytes (0 when
+ *             the shape needs no split of K; ws may then be NULL).  When non-empty, its
+ *             first 64 KiB hold split-K arrival counters: they must be zero before the
+ *             first call (zero-fill a new workspace once) and every call leaves them
+ *             zero, so one workspace serves calls of any shape.  Calls that share a
+ *             workspace race unless they are ordered, e.g. on one stream.
+ * Accumulation is exact: |acc| <= K q^2 < 2^31 for K <= 32768 at INT4 and
+ * K <= 32768 at INT8 (127^2 * 32768 < 2^31 holds up to K = 133152). */
+fq_status fq_gemm_w4a4(const void *a_codes, const float *delta, const void *w_packed,
+                       const float *w_scale, const float *bias, void *y_bf16, int64_t ldy,
+                       int32_t *acc_out, int64_t M, int64_t N, int64_t K, void *ws,
+                       size_t ws_bytes, void *stream);
+fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_packed,
+                       const float *w_scale, const float *bias, void *y_bf16, int64_t ldy,
+                       int32_t *acc_out, int64_t M, int64_t N, int64_t K, void *ws,
+                       size_t ws_bytes, void *stream);
+
+/* Workspace bytes fq_linear needs: 64 KiB of split-K counters first (same zero-fill
+ * contract as the GEMM workspace), then the activation codes, scales and partial sums. */
+size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
+
+/* The whole runtime projection for one consumer (Alg. 1 runtime; eqs. (5), (8)):
+ * prologue on x, integer GEMM against w_packed, rescale + bias, bf16 out.
+ * Same arguments and contracts as fq_fwht_quant followed by fq_gemm_w{4a4,8a8}; the
+ * intermediate codes live in `ws` in a kernel-native layout. */
+fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
+                    int64_t K, int64_t N, int b, int bits, float clip_ratio, const void *w_packed,
+                    const float *w_scale, const float *bias, void *y_bf16, int64_t ldy, void *ws,
+                    size_t ws_bytes, void *stream);
+
+/* Static description of a status code, and the thread-local message of the last failure. */
+const char *fq_status_string(fq_status s);
+const char *fq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FQ_H_ */

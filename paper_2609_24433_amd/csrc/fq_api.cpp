@@ -1,0 +1,294 @@
+// C ABI of libfq: argument validation, workspace layout and dispatch to the gfx950 kernels.
+// Every check runs before anything is enqueued, so a failing call has no device effect.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/fq.h"
+#include "fq_launch.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+fq_status fail(fq_status s, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+fq_status ok() {
+  g_err[0] = '\0';
+  return FQ_OK;
+}
+
+fq_status hip_fail(hipError_t e, const char *where) {
+  return fail(FQ_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool is_pow2(int64_t v) { return v >= 1 && (v & (v - 1)) == 0; }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+constexpr int64_t kMaxK = 32768;
+
+// float nearest to 1/sqrt(b), b = 2^k: 2^(-k/2) for even k, 2^(-(k-1)/2) / sqrt(2) for odd k
+float inv_sqrt_pow2(int b) {
+  int k = 0;
+  while ((1 << k) < b) ++k;
+  const float rsqrt2 = 0x1.6a09e6p-1f;  // nearest float to 1/sqrt(2)
+  return (k & 1) ? std::ldexp(rsqrt2, -(k - 1) / 2) : std::ldexp(1.0f, -k / 2);
+}
+
+fq_status check_k(int64_t K) {
+  if (K < 128 || K > kMaxK) return fail(FQ_ERR_UNSUPPORTED, "K=%lld outside [128, %lld]", (long long)K, (long long)kMaxK);
+  if (K % 128) return fail(FQ_ERR_UNSUPPORTED, "K=%lld is not a multiple of 128", (long long)K);
+  return FQ_OK;
+}
+
+fq_status check_bits(int bits) {
+  if (bits != 4 && bits != 8) return fail(FQ_ERR_UNSUPPORTED, "bits=%d (must be 4 or 8)", bits);
+  return FQ_OK;
+}
+
+fq_status check_block(int b, int64_t K) {
+  if (!is_pow2(b) || b > 256) return fail(FQ_ERR_UNSUPPORTED, "b=%d is not a power of two in [1, 256]", b);
+  if (K % b) return fail(FQ_ERR_SHAPE, "K=%lld is not a multiple of b=%d", (long long)K, b);
+  return FQ_OK;
+}
+
+// Shape/argument checks of the prologue; `ld_mult` is the element multiple that keeps
+// rows 16-byte aligned (8 for bf16, 4 for fp32).
+fq_status check_prologue_shape(int64_t ldx, int ld_mult, int64_t M, int64_t K, int b, int bits,
+                               float r) {
+  if (M < 0) return fail(FQ_ERR_SHAPE, "M=%lld < 0", (long long)M);
+  fq_status s;
+  if ((s = check_k(K)) != FQ_OK) return s;
+  if ((s = check_bits(bits)) != FQ_OK) return s;
+  if ((s = check_block(b, K)) != FQ_OK) return s;
+  if (!(r > 0.0f && r <= 1.0f)) return fail(FQ_ERR_UNSUPPORTED, "clip_ratio=%g outside (0, 1]", (double)r);
+  if (ldx < K) return fail(FQ_ERR_SHAPE, "leading dimension %lld < K=%lld", (long long)ldx, (long long)K);
+  if (ldx % ld_mult) return fail(FQ_ERR_ALIGN, "leading dimension %lld is not a multiple of %d", (long long)ldx, ld_mult);
+  return FQ_OK;
+}
+
+fq_status check_prologue(const void *x, int64_t ldx, int ld_mult, const float *smooth, int64_t M,
+                         int64_t K, int b, int bits, float r, const void *codes, const float *delta) {
+  fq_status s = check_prologue_shape(ldx, ld_mult, M, K, b, bits, r);
+  if (s != FQ_OK || M == 0) return s;
+  if (!x || !codes || !delta) return fail(FQ_ERR_NULL, "input, codes and scales must be non-NULL");
+  if (!aligned16(x) || !aligned16(codes) || !aligned16(delta) || (smooth && !aligned16(smooth)))
+    return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  return FQ_OK;
+}
+
+fq_status check_gemm(const void *a, const float *delta, const void *w, const float *w_scale,
+                     const float *bias, const void *y, int64_t ldy, const int32_t *acc_out,
+                     int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || N < 0) return fail(FQ_ERR_SHAPE, "M=%lld, N=%lld must be >= 0", (long long)M, (long long)N);
+  fq_status s;
+  if ((s = check_k(K)) != FQ_OK) return s;
+  if (N % 16) return fail(FQ_ERR_UNSUPPORTED, "N=%lld is not a multiple of 16", (long long)N);
+  if (N > (1ll << 24) || M > (1ll << 24)) return fail(FQ_ERR_UNSUPPORTED, "M or N too large");
+  if (ldy < N) return fail(FQ_ERR_SHAPE, "ldy=%lld < N=%lld", (long long)ldy, (long long)N);
+  if (ldy % 8) return fail(FQ_ERR_ALIGN, "ldy=%lld is not a multiple of 8", (long long)ldy);
+  if (M == 0 || N == 0) return FQ_OK;
+  if (!a || !delta || !w || !w_scale || !y) return fail(FQ_ERR_NULL, "a, delta, w, w_scale and y must be non-NULL");
+  if (!aligned16(a) || !aligned16(delta) || !aligned16(w) || !aligned16(w_scale) || !aligned16(y) ||
+      (bias && !aligned16(bias)) || (acc_out && !aligned16(acc_out)))
+    return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  return FQ_OK;
+}
+
+// `gap`: bytes between the counter region and the partial sums (fq_linear keeps its codes
+// and scales there); the GEMM's own entry points use gap = 0.
+fq_status gemm_common(const void *a_codes, int a_fmt, int64_t lda, const float *delta,
+                      const void *w_packed, const float *w_scale, const float *bias, void *y,
+                      int64_t ldy, int32_t *acc_out, int64_t M, int64_t N, int64_t K, int bits,
+                      void *ws, size_t ws_bytes, hipStream_t stream, size_t gap = 0) {
+  const fq::GemmPlan pl = fq::plan_gemm(M, N, K, bits);
+  const size_t need = fq::gemm_plan_workspace(pl) + (pl.splits > 1 ? gap : 0);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (need > 0 && !aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  fq::GemmArgs g;
+  g.a = static_cast<const uint8_t *>(a_codes);
+  g.lda = lda;
+  g.a_fmt = a_fmt;
+  g.delta = delta;
+  g.w = static_cast<const uint8_t *>(w_packed);
+  g.w_scale = w_scale;
+  g.bias = bias;
+  g.y = static_cast<uint16_t *>(y);
+  g.ldy = ldy;
+  g.acc_out = acc_out;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.bits = bits;
+  hipError_t e = fq::launch_gemm(g, pl, ws, gap, stream);
+  if (e != hipSuccess) return hip_fail(e, "gemm launch");
+  return ok();
+}
+
+fq_status gemm_entry(int bits, const void *a_codes, const float *delta, const void *w_packed,
+                     const float *w_scale, const float *bias, void *y, int64_t ldy, int32_t *acc_out,
+                     int64_t M, int64_t N, int64_t K, void *ws, size_t ws_bytes, void *stream) {
+  fq_status s = check_gemm(a_codes, delta, w_packed, w_scale, bias, y, ldy, acc_out, M, N, K);
+  if (s != FQ_OK) return s;
+  if (M == 0 || N == 0) return ok();
+  const int a_fmt = bits == 4 ? fq::kANibble : fq::kAInt8;
+  const int64_t lda = bits == 4 ? K / 2 : K;
+  return gemm_common(a_codes, a_fmt, lda, delta, w_packed, w_scale, bias, y, ldy, acc_out, M, N, K,
+                     bits, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *fq_status_string(fq_status s) {
+  switch (s) {
+    case FQ_OK: return "ok";
+    case FQ_ERR_NULL: return "null pointer";
+    case FQ_ERR_SHAPE: return "bad shape";
+    case FQ_ERR_UNSUPPORTED: return "unsupported argument";
+    case FQ_ERR_ALIGN: return "misaligned pointer or leading dimension";
+    case FQ_ERR_WORKSPACE: return "workspace too small";
+    case FQ_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char *fq_last_error(void) { return g_err; }
+
+fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
+                        int64_t K, int b, int bits, float clip_ratio, void *a_codes, float *delta,
+                        void *stream) {
+  fq_status s = check_prologue(x_bf16, ldx, 8, smooth_inv, M, K, b, bits, clip_ratio, a_codes, delta);
+  if (s != FQ_OK) return s;
+  if (M == 0) return ok();
+  const int fmt = bits == 4 ? fq::kOutNibble : fq::kOutInt8;
+  const int64_t ldc = bits == 4 ? K / 2 : K;
+  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, M, (int)K, b, bits, clip_ratio,
+                                       inv_sqrt_pow2(b), static_cast<uint8_t *>(a_codes), ldc, delta,
+                                       fmt, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
+  return ok();
+}
+
+fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scale, int64_t N,
+                              int64_t K, int b, int bits, int8_t *w_codes, float *w_scale,
+                              void *stream) {
+  fq_status s = check_prologue(w, ldw, 4, col_scale, N, K, b, bits, 1.0f, w_codes, w_scale);
+  if (s != FQ_OK) return s;
+  if (N == 0) return ok();
+  hipError_t e = fq::launch_fwht_quant(w, true, ldw, col_scale, N, (int)K, b, bits, 1.0f,
+                                       inv_sqrt_pow2(b), reinterpret_cast<uint8_t *>(w_codes), K,
+                                       w_scale, fq::kOutInt8, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "quantize_weights launch");
+  return ok();
+}
+
+size_t fq_packed_weight_bytes(int64_t N, int64_t K, int bits) {
+  if (N < 0 || K < 0 || (bits != 4 && bits != 8)) return 0;
+  return (size_t)N * (size_t)K * (size_t)bits / 8;
+}
+
+fq_status fq_pack_weights(const int8_t *w_codes, int64_t N, int64_t K, int bits, void *w_packed,
+                          void *stream) {
+  fq_status s;
+  if (N < 0) return fail(FQ_ERR_SHAPE, "N=%lld < 0", (long long)N);
+  if (N % 16) return fail(FQ_ERR_UNSUPPORTED, "N=%lld is not a multiple of 16", (long long)N);
+  if ((s = check_k(K)) != FQ_OK) return s;
+  if ((s = check_bits(bits)) != FQ_OK) return s;
+  if (N == 0) return ok();
+  if (!w_codes || !w_packed) return fail(FQ_ERR_NULL, "w_codes and w_packed must be non-NULL");
+  if (!aligned16(w_codes) || !aligned16(w_packed)) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  hipError_t e = fq::launch_pack_weights(w_codes, N, (int)K, bits, static_cast<uint8_t *>(w_packed),
+                                         static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pack launch");
+  return ok();
+}
+
+fq_status fq_unpack_weights(const void *w_packed, int64_t N, int64_t K, int bits, int8_t *w_codes,
+                            void *stream) {
+  fq_status s;
+  if (N < 0) return fail(FQ_ERR_SHAPE, "N=%lld < 0", (long long)N);
+  if (N % 16) return fail(FQ_ERR_UNSUPPORTED, "N=%lld is not a multiple of 16", (long long)N);
+  if ((s = check_k(K)) != FQ_OK) return s;
+  if ((s = check_bits(bits)) != FQ_OK) return s;
+  if (N == 0) return ok();
+  if (!w_codes || !w_packed) return fail(FQ_ERR_NULL, "w_codes and w_packed must be non-NULL");
+  if (!aligned16(w_codes) || !aligned16(w_packed)) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  hipError_t e = fq::launch_unpack_weights(static_cast<const uint8_t *>(w_packed), N, (int)K, bits,
+                                           w_codes, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "unpack launch");
+  return ok();
+}
+
+size_t fq_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
+  if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
+  return fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
+}
+
+fq_status fq_gemm_w4a4(const void *a_codes, const float *delta, const void *w_packed,
+                       const float *w_scale, const float *bias, void *y_bf16, int64_t ldy,
+                       int32_t *acc_out, int64_t M, int64_t N, int64_t K, void *ws,
+                       size_t ws_bytes, void *stream) {
+  return gemm_entry(4, a_codes, delta, w_packed, w_scale, bias, y_bf16, ldy, acc_out, M, N, K, ws,
+                    ws_bytes, stream);
+}
+
+fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_packed,
+                       const float *w_scale, const float *bias, void *y_bf16, int64_t ldy,
+                       int32_t *acc_out, int64_t M, int64_t N, int64_t K, void *ws,
+                       size_t ws_bytes, void *stream) {
+  return gemm_entry(8, a_codes, delta, w_packed, w_scale, bias, y_bf16, ldy, acc_out, M, N, K, ws,
+                    ws_bytes, stream);
+}
+
+// fq_linear workspace: [split-K counters (fixed size, first)][codes][delta][split-K partials]
+size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
+  if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
+  return fq::kCounterRegionBytes + align256((size_t)M * (size_t)K) + align256((size_t)M * 4) +
+         fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
+}
+
+fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
+                    int64_t K, int64_t N, int b, int bits, float clip_ratio, const void *w_packed,
+                    const float *w_scale, const float *bias, void *y_bf16, int64_t ldy, void *ws,
+                    size_t ws_bytes, void *stream) {
+  // validate both stages before enqueueing either
+  fq_status s = check_prologue_shape(ldx, 8, M, K, b, bits, clip_ratio);
+  if (s != FQ_OK) return s;
+  if (M > 0 && smooth_inv && !aligned16(smooth_inv)) return fail(FQ_ERR_ALIGN, "smooth_inv must be 16-byte aligned");
+  s = check_gemm(x_bf16, w_scale, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K);
+  if (s != FQ_OK) return s;
+  if (M == 0 || N == 0) return ok();
+  const size_t codes_bytes = align256((size_t)M * (size_t)K);
+  const size_t delta_bytes = align256((size_t)M * 4);
+  const size_t need = fq_linear_workspace_bytes(M, N, K, bits);
+  if (!ws || ws_bytes < need)
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  // the GEMM sees [counters][partials]: codes and delta sit between the two regions
+  uint8_t *codes = static_cast<uint8_t *>(ws) + fq::kCounterRegionBytes;
+  float *delta = reinterpret_cast<float *>(codes + codes_bytes);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int fmt = bits == 4 ? fq::kOutPerm8 : fq::kOutInt8;
+  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, M, (int)K, b, bits, clip_ratio,
+                                       inv_sqrt_pow2(b), codes, K, delta, fmt, st);
+  if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
+  return gemm_common(codes, fq::kAInt8, K, delta, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N,
+                     K, bits, ws, ws_bytes, st, codes_bytes + delta_bytes);
+}
+
+}  // extern "C"

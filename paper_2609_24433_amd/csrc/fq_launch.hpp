@@ -1,0 +1,68 @@
+// Host-side launchers of the gfx950 kernels (internal to libfq; not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fq {
+
+// Output layouts of the prologue.
+constexpr int kOutNibble = 0;  // canonical signed-INT4: channel 2i low nibble of byte i
+constexpr int kOutInt8 = 1;    // canonical int8, one byte per channel
+constexpr int kOutPerm8 = 2;   // int8, channels of each group of 8 stored as 0 2 4 6 1 3 5 7
+
+// Activation operand formats of the GEMM.
+constexpr int kANibble = 0;  // canonical nibbles (widened in the kernel)
+constexpr int kAInt8 = 1;    // canonical int8 (W8A8) or kOutPerm8 order (W4A4)
+
+hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const float *chan_mult,
+                             int64_t M, int K, int b, int bits, float clip_ratio, float cb,
+                             uint8_t *codes, int64_t ld_codes, float *delta, int out_fmt,
+                             hipStream_t s);
+
+hipError_t launch_pack_weights(const int8_t *codes, int64_t N, int K, int bits, uint8_t *packed,
+                               hipStream_t s);
+hipError_t launch_unpack_weights(const uint8_t *packed, int64_t N, int K, int bits, int8_t *codes,
+                                 hipStream_t s);
+
+// Split-K arrival counters occupy the first kCounterRegionBytes of every GEMM workspace,
+// one 32-bit counter per output tile; every call leaves them at zero.
+constexpr size_t kCounterRegionBytes = 65536;
+constexpr int64_t kMaxCounters = kCounterRegionBytes / 4;
+
+// GEMM plan: which kernel, its tiling and its split of K.
+struct GemmPlan {
+  int kind;     // 0 = streaming (M <= 64), 1 = tiled
+  int mt;       // streaming: 16-row tiles covering M
+  int bm, bn;   // tiled: workgroup tile
+  int splits;   // K slices
+  int ksteps;   // 128-wide k steps per slice
+  int red_atomic;  // K slices combined with device atomics (else partial buffers)
+  int64_t tiles;        // output tiles (counter slots)
+  size_t partial_bytes; // split-K partial sums
+  size_t counter_bytes;
+};
+
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits);
+size_t gemm_plan_workspace(const GemmPlan &pl);
+
+struct GemmArgs {
+  const uint8_t *a;
+  int64_t lda;  // bytes per activation row
+  int a_fmt;
+  const float *delta;
+  const uint8_t *w;
+  const float *w_scale;
+  const float *bias;
+  uint16_t *y;
+  int64_t ldy;
+  int32_t *acc_out;
+  int64_t M, N, K;
+  int bits;
+};
+
+// ws: [counters (kCounterRegionBytes)][gap bytes, untouched][partials]
+hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, size_t gap, hipStream_t s);
+
+}  // namespace fq

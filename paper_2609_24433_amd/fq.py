@@ -1,0 +1,195 @@
+"""Python binding of libfq (the C ABI in include/fq.h), over torch device tensors.
+
+Argument marshalling only: tensors are used for their device pointers and torch's
+current HIP stream; every step of the projection runs in the library's kernels.
+If libfq.so is missing the import fails loudly; there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfq.so")
+
+FQ_OK = 0
+_STATUS = {1: "FQ_ERR_NULL", 2: "FQ_ERR_SHAPE", 3: "FQ_ERR_UNSUPPORTED", 4: "FQ_ERR_ALIGN",
+           5: "FQ_ERR_WORKSPACE", 6: "FQ_ERR_HIP"}
+
+EXPORTED = ["fq_fwht_quant", "fq_quantize_weights", "fq_packed_weight_bytes", "fq_pack_weights",
+            "fq_unpack_weights", "fq_gemm_workspace_bytes", "fq_gemm_w4a4", "fq_gemm_w8a8",
+            "fq_linear_workspace_bytes", "fq_linear", "fq_status_string", "fq_last_error"]
+
+
+class FQError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                          "(python -m paper_2609_24433_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    sig = {
+        "fq_fwht_quant": [vp, i64, vp, i64, i64, i32, i32, f32, vp, vp, vp],
+        "fq_quantize_weights": [vp, i64, vp, i64, i64, i32, i32, vp, vp, vp],
+        "fq_pack_weights": [vp, i64, i64, i32, vp, vp],
+        "fq_unpack_weights": [vp, i64, i64, i32, vp, vp],
+        "fq_gemm_w4a4": [vp, vp, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
+        "fq_gemm_w8a8": [vp, vp, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
+        "fq_linear": [vp, i64, vp, i64, i64, i64, i32, i32, f32, vp, vp, vp, vp, i64, vp, sz, vp],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    for name, args in {"fq_packed_weight_bytes": [i64, i64, i32],
+                       "fq_gemm_workspace_bytes": [i64, i64, i64, i32],
+                       "fq_linear_workspace_bytes": [i64, i64, i64, i32]}.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = sz
+    lib.fq_status_string.argtypes = [ctypes.c_int]
+    lib.fq_status_string.restype = ctypes.c_char_p
+    lib.fq_last_error.argtypes = []
+    lib.fq_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+LIB = _load()
+
+
+def _check(rc: int) -> None:
+    if rc != FQ_OK:
+        raise FQError(rc, LIB.fq_last_error().decode())
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream: Optional[torch.cuda.Stream] = None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ---------------------------------------------------------------- raw C-ABI calls (pointers)
+
+def fwht_quant_raw(x_ptr, ldx, smooth_ptr, M, K, b, bits, clip_ratio, codes_ptr, delta_ptr, stream_ptr):
+    _check(LIB.fq_fwht_quant(x_ptr, ldx, smooth_ptr, M, K, b, bits, clip_ratio, codes_ptr, delta_ptr,
+                             stream_ptr))
+
+
+# ---------------------------------------------------------------- tensor API
+
+def code_bytes(K: int, bits: int) -> int:
+    return K * bits // 8
+
+
+def fwht_quant(x: torch.Tensor, b: int, bits: int, clip_ratio: float = 1.0,
+               smooth_inv: Optional[torch.Tensor] = None, out_codes: Optional[torch.Tensor] = None,
+               out_delta: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Prologue: x bf16 [M, K] (row stride x.stride(0)) -> (codes uint8 [M, K*bits/8], delta fp32 [M])."""
+    M, K = x.shape
+    assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
+    codes = out_codes if out_codes is not None else torch.empty((M, code_bytes(K, bits)), dtype=torch.uint8, device=x.device)
+    delta = out_delta if out_delta is not None else torch.empty((M,), dtype=torch.float32, device=x.device)
+    _check(LIB.fq_fwht_quant(_p(x), x.stride(0) if M else K, _p(smooth_inv), M, K, b, bits, clip_ratio, _p(codes),
+                             _p(delta), _stream()))
+    return codes, delta
+
+
+def quantize_weights(w: torch.Tensor, b: int, bits: int,
+                     col_scale: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Offline fold + RTN: w fp32 [N, K] -> (codes int8 [N, K], scales fp32 [N])."""
+    N, K = w.shape
+    assert w.dtype == torch.float32 and w.stride(1) == 1
+    codes = torch.empty((N, K), dtype=torch.int8, device=w.device)
+    scale = torch.empty((N,), dtype=torch.float32, device=w.device)
+    _check(LIB.fq_quantize_weights(_p(w), w.stride(0), _p(col_scale), N, K, b, bits, _p(codes), _p(scale),
+                                   _stream()))
+    return codes, scale
+
+
+def packed_weight_bytes(N: int, K: int, bits: int) -> int:
+    return int(LIB.fq_packed_weight_bytes(N, K, bits))
+
+
+def pack_weights(codes: torch.Tensor, bits: int) -> torch.Tensor:
+    N, K = codes.shape
+    assert codes.dtype == torch.int8 and codes.is_contiguous()
+    out = torch.empty((packed_weight_bytes(N, K, bits),), dtype=torch.uint8, device=codes.device)
+    _check(LIB.fq_pack_weights(_p(codes), N, K, bits, _p(out), _stream()))
+    return out
+
+
+def unpack_weights(packed: torch.Tensor, N: int, K: int, bits: int) -> torch.Tensor:
+    out = torch.empty((N, K), dtype=torch.int8, device=packed.device)
+    _check(LIB.fq_unpack_weights(_p(packed), N, K, bits, _p(out), _stream()))
+    return out
+
+
+def gemm_workspace_bytes(M: int, N: int, K: int, bits: int) -> int:
+    return int(LIB.fq_gemm_workspace_bytes(M, N, K, bits))
+
+
+def linear_workspace_bytes(M: int, N: int, K: int, bits: int) -> int:
+    return int(LIB.fq_linear_workspace_bytes(M, N, K, bits))
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    """A zero-filled workspace (the split-K counters must start at zero)."""
+    return torch.zeros((max(nbytes, 256),), dtype=torch.uint8, device=device)
+
+
+def gemm(a_codes: torch.Tensor, delta: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor,
+         N: int, K: int, bits: int, bias: Optional[torch.Tensor] = None, want_acc: bool = False,
+         ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None):
+    """Integer GEMM + eq. (8) epilogue.  Returns y bf16 [M, N] (and int32 acc if want_acc)."""
+    M = a_codes.shape[0]
+    y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=a_codes.device)
+    acc = torch.empty((M, N), dtype=torch.int32, device=a_codes.device) if want_acc else None
+    if ws is None:
+        ws = workspace(gemm_workspace_bytes(M, N, K, bits), a_codes.device)
+    fn = LIB.fq_gemm_w4a4 if bits == 4 else LIB.fq_gemm_w8a8
+    _check(fn(_p(a_codes), _p(delta), _p(w_packed), _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N, _p(acc),
+              M, N, K, _p(ws), ws.numel(), _stream()))
+    return (y, acc) if want_acc else y
+
+
+def linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: int, b: int, bits: int,
+           clip_ratio: float = 1.0, smooth_inv: Optional[torch.Tensor] = None,
+           bias: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Fused projection: bf16 x [M, K] -> bf16 y [M, N]."""
+    M, K = x.shape
+    assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
+    y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    if ws is None:
+        ws = workspace(linear_workspace_bytes(M, N, K, bits), x.device)
+    _check(LIB.fq_linear(_p(x), x.stride(0) if M else K, _p(smooth_inv), M, K, N, b, bits, clip_ratio, _p(w_packed),
+                         _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N, _p(ws), ws.numel(), _stream()))
+    return y
+
+
+class QuantLinear:
+    """One consumer projection: folded, rounded and packed weights kept resident on the device."""
+
+    def __init__(self, w: torch.Tensor, b: int, bits: int, col_scale: Optional[torch.Tensor] = None,
+                 bias: Optional[torch.Tensor] = None):
+        self.N, self.K = w.shape
+        self.b, self.bits = b, bits
+        codes, self.w_scale = quantize_weights(w, b, bits, col_scale)
+        self.w_packed = pack_weights(codes, bits)
+        self.bias = bias
+
+    def __call__(self, x: torch.Tensor, clip_ratio: float = 1.0, smooth_inv: Optional[torch.Tensor] = None,
+                 ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+        return linear(x, self.w_packed, self.w_scale, self.N, self.b, self.bits, clip_ratio, smooth_inv,
+                      self.bias, ws, out)

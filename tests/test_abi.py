@@ -1,0 +1,132 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point the
+header declares, sizes its workspaces, and rejects bad arguments before enqueueing
+anything (all calls here fail validation or are no-ops, so no kernel is launched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_24433_amd import fq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fq.h")
+
+NULL = None
+FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: every call below fails validation first
+MISALIGNED = ctypes.c_void_p(0x10004)
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(fq_[a-z0-9_]+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    syms = declared_symbols()
+    assert set(syms) == set(fq.EXPORTED), syms
+
+
+@pytest.mark.parametrize("name", declared_symbols())
+def test_library_exports_symbol(name):
+    assert hasattr(fq.LIB, name)
+
+
+def test_status_strings():
+    for s in range(7):
+        assert fq.LIB.fq_status_string(s)
+    assert fq.LIB.fq_status_string(99) == b"unknown status"
+
+
+def test_sizes():
+    assert fq.packed_weight_bytes(2048, 16384, 4) == 2048 * 16384 // 2
+    assert fq.packed_weight_bytes(2048, 16384, 8) == 2048 * 16384
+    assert fq.packed_weight_bytes(16, 128, 3) == 0
+    assert fq.gemm_workspace_bytes(0, 16, 128, 4) == 0
+    # linear workspace holds int8 codes and scales at least
+    assert fq.linear_workspace_bytes(50, 2048, 16384, 4) >= 50 * 16384 + 50 * 4
+    for M in (1, 16, 50, 64, 65, 816, 4096):
+        assert fq.gemm_workspace_bytes(M, 2048, 16384, 4) % 256 == 0
+
+
+def call_quant(x=FAKE, ldx=1024, smooth=NULL, M=4, K=1024, b=64, bits=4, r=1.0, codes=FAKE, delta=FAKE):
+    return fq.LIB.fq_fwht_quant(x, ldx, smooth, M, K, b, bits, r, codes, delta, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=NULL), 1), (dict(codes=NULL), 1), (dict(delta=NULL), 1),
+    (dict(M=-1), 2), (dict(ldx=1000), 2), (dict(b=128, K=1024 + 128 + 64), 3),
+    (dict(K=1024 + 64), 3), (dict(K=64), 3), (dict(K=65536), 3),
+    (dict(b=3), 3), (dict(b=512), 3), (dict(b=0), 3), (dict(bits=2), 3), (dict(bits=16), 3),
+    (dict(r=0.0), 3), (dict(r=1.5), 3), (dict(r=float("nan")), 3),
+    (dict(x=MISALIGNED), 4), (dict(codes=MISALIGNED), 4), (dict(ldx=1028), 4),
+    (dict(smooth=MISALIGNED), 4),
+])
+def test_fwht_quant_rejects(kw, status):
+    assert call_quant(**kw) == status
+    assert fq.LIB.fq_last_error()
+
+
+def test_fwht_quant_k_not_multiple_of_b():
+    assert call_quant(K=1152, ldx=1152, b=256) == 2
+
+
+def test_zero_rows_are_noops():
+    assert call_quant(M=0, x=NULL, codes=NULL, delta=NULL) == 0
+    assert fq.LIB.fq_gemm_w4a4(NULL, NULL, NULL, NULL, NULL, NULL, 16, NULL, 0, 16, 128, NULL, 0, None) == 0
+    assert fq.LIB.fq_linear(NULL, 1024, NULL, 0, 1024, 256, 64, 4, 1.0, NULL, NULL, NULL, NULL, 256, NULL, 0,
+                            None) == 0
+
+
+def call_gemm(bits=4, a=FAKE, delta=FAKE, w=FAKE, sw=FAKE, bias=NULL, y=FAKE, ldy=256, acc=NULL,
+              M=50, N=256, K=1024, ws=FAKE, ws_bytes=1 << 30):
+    fn = fq.LIB.fq_gemm_w4a4 if bits == 4 else fq.LIB.fq_gemm_w8a8
+    return fn(a, delta, w, sw, bias, y, ldy, acc, M, N, K, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("kw,status", [
+    (dict(a=NULL), 1), (dict(delta=NULL), 1), (dict(w=NULL), 1), (dict(sw=NULL), 1), (dict(y=NULL), 1),
+    (dict(M=-3), 2), (dict(ldy=128), 2), (dict(N=-16), 2),
+    (dict(N=250, ldy=256), 3), (dict(K=1000), 3), (dict(K=0), 3),
+    (dict(bias=MISALIGNED), 4), (dict(acc=MISALIGNED), 4), (dict(ldy=260), 4), (dict(w=MISALIGNED), 4),
+    (dict(ws=NULL, ws_bytes=0, M=50, N=2048, ldy=2048, K=16384), 5),
+    (dict(ws_bytes=16, M=50, N=2048, ldy=2048, K=16384), 5),
+])
+def test_gemm_rejects(bits, kw, status):
+    assert call_gemm(bits=bits, **kw) == status
+
+
+def call_linear(x=FAKE, ldx=1024, M=50, K=1024, N=256, b=64, bits=4, r=1.0, w=FAKE, sw=FAKE, bias=NULL,
+                y=FAKE, ldy=256, ws=FAKE, ws_bytes=1 << 30, smooth=NULL):
+    return fq.LIB.fq_linear(x, ldx, smooth, M, K, N, b, bits, r, w, sw, bias, y, ldy, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=NULL), 1), (dict(w=NULL), 1), (dict(y=NULL), 1), (dict(sw=NULL), 1),
+    (dict(ldx=512), 2), (dict(ldy=100), 2), (dict(b=5), 3), (dict(bits=6), 3), (dict(N=40, ldy=40), 3),
+    (dict(r=-1.0), 3), (dict(ws=NULL, ws_bytes=0), 5), (dict(ws_bytes=100), 5), (dict(ws=MISALIGNED), 4),
+    (dict(smooth=MISALIGNED), 4),
+])
+def test_linear_rejects(kw, status):
+    assert call_linear(**kw) == status
+
+
+@pytest.mark.parametrize("fn", ["fq_pack_weights", "fq_unpack_weights"])
+def test_pack_rejects(fn):
+    f = getattr(fq.LIB, fn)
+    assert f(NULL, 32, 128, 4, FAKE, None) == 1
+    assert f(FAKE, 30, 128, 4, FAKE, None) == 3
+    assert f(FAKE, 32, 100, 4, FAKE, None) == 3
+    assert f(FAKE, 32, 128, 5, FAKE, None) == 3
+    assert f(FAKE, -16, 128, 4, FAKE, None) == 2
+    assert f(MISALIGNED, 32, 128, 4, FAKE, None) == 4
+    assert f(FAKE, 0, 128, 4, FAKE, None) == 0
+
+
+def test_quantize_weights_rejects():
+    f = fq.LIB.fq_quantize_weights
+    assert f(NULL, 128, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 1
+    assert f(FAKE, 130, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 4
+    assert f(FAKE, 64, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 2
+    assert f(FAKE, 128, NULL, 16, 128, 64, 7, FAKE, FAKE, None) == 3
