@@ -97,12 +97,11 @@ size_t fq_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
  *   w_scale   fp32 [N]; bias: fp32 [N] or NULL.
  *   y_bf16    [M, ldy] bf16 output: y = bf16_rne(fp32(acc) * (w_scale[j] * delta[t]) + bias[j]).
  *   acc_out   int32 [M, N] raw accumulators, or NULL (for verification).
- *   ws        workspace of at least fq_gemm_workspace_bytes(M, N, K, bits) bytes (0 when
- *             the shape needs no split of K; ws may then be NULL).  When non-empty, its
- *             first 64 KiB hold split-K arrival counters: they must be zero before the
- *             first call (zero-fill a new workspace once) and every call leaves them
- *             zero, so one workspace serves calls of any shape.  Calls that share a
- *             workspace race unless they are ordered, e.g. on one stream.
+ *   ws        scratch of at least fq_gemm_workspace_bytes(M, N, K, bits) bytes (0 when
+ *             the shape needs no split of K; ws may then be NULL).  It needs no
+ *             initialization; it holds the INT32 partial sums of a split K between the
+ *             GEMM kernel and its epilogue.  Calls that share a workspace race unless
+ *             they are ordered, e.g. on one stream.
  * Accumulation is exact: |acc| <= K q^2 < 2^31 for K <= 32768 at INT4 and
  * K <= 32768 at INT8 (127^2 * 32768 < 2^31 holds up to K = 133152). */
 fq_status fq_gemm_w4a4(const void *a_codes, const float *delta, const void *w_packed,
@@ -114,8 +113,8 @@ fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_pa
                        int32_t *acc_out, int64_t M, int64_t N, int64_t K, void *ws,
                        size_t ws_bytes, void *stream);
 
-/* Workspace bytes fq_linear needs: 64 KiB of split-K counters first (same zero-fill
- * contract as the GEMM workspace), then the activation codes, scales and partial sums. */
+/* Workspace bytes fq_linear needs: the intermediate activation codes and scales, and the
+ * split-K partial sums.  Scratch with no initialization requirement. */
 size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
 
 /* The whole runtime projection for one consumer (Alg. 1 runtime; eqs. (5), (8)):

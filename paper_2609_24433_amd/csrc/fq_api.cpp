@@ -107,14 +107,12 @@ fq_status check_gemm(const void *a, const float *delta, const void *w, const flo
   return FQ_OK;
 }
 
-// `gap`: bytes between the counter region and the partial sums (fq_linear keeps its codes
-// and scales there); the GEMM's own entry points use gap = 0.
 fq_status gemm_common(const void *a_codes, int a_fmt, int64_t lda, const float *delta,
                       const void *w_packed, const float *w_scale, const float *bias, void *y,
                       int64_t ldy, int32_t *acc_out, int64_t M, int64_t N, int64_t K, int bits,
-                      void *ws, size_t ws_bytes, hipStream_t stream, size_t gap = 0) {
+                      void *ws, size_t ws_bytes, hipStream_t stream) {
   const fq::GemmPlan pl = fq::plan_gemm(M, N, K, bits);
-  const size_t need = fq::gemm_plan_workspace(pl) + (pl.splits > 1 ? gap : 0);
+  const size_t need = fq::gemm_plan_workspace(pl);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   if (need > 0 && !aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
@@ -133,7 +131,7 @@ fq_status gemm_common(const void *a_codes, int a_fmt, int64_t lda, const float *
   g.N = N;
   g.K = K;
   g.bits = bits;
-  hipError_t e = fq::launch_gemm(g, pl, ws, gap, stream);
+  hipError_t e = fq::launch_gemm(g, pl, ws, stream);
   if (e != hipSuccess) return hip_fail(e, "gemm launch");
   return ok();
 }
@@ -255,10 +253,10 @@ fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_pa
                     ws_bytes, stream);
 }
 
-// fq_linear workspace: [split-K counters (fixed size, first)][codes][delta][split-K partials]
+// fq_linear workspace: [codes (kernel-native int8)][delta][split-K partials]
 size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
   if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
-  return fq::kCounterRegionBytes + align256((size_t)M * (size_t)K) + align256((size_t)M * 4) +
+  return align256((size_t)M * (size_t)K) + align256((size_t)M * 4) +
          fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
 }
 
@@ -279,16 +277,16 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, in
   if (!ws || ws_bytes < need)
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
-  // the GEMM sees [counters][partials]: codes and delta sit between the two regions
-  uint8_t *codes = static_cast<uint8_t *>(ws) + fq::kCounterRegionBytes;
+  uint8_t *codes = static_cast<uint8_t *>(ws);
   float *delta = reinterpret_cast<float *>(codes + codes_bytes);
+  void *gws = codes + codes_bytes + delta_bytes;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int fmt = bits == 4 ? fq::kOutPerm8 : fq::kOutInt8;
   hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, M, (int)K, b, bits, clip_ratio,
                                        inv_sqrt_pow2(b), codes, K, delta, fmt, st);
   if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
   return gemm_common(codes, fq::kAInt8, K, delta, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N,
-                     K, bits, ws, ws_bytes, st, codes_bytes + delta_bytes);
+                     K, bits, gws, ws_bytes - codes_bytes - delta_bytes, st);
 }
 
 }  // extern "C"

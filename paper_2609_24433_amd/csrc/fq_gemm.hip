@@ -15,14 +15,15 @@
 // 128*kt + 32*(l/16) + [0, 32), stored contiguously at byte l * lane_bytes.  A wave
 // therefore fetches a whole tile with one fully coalesced 16/32-byte load per lane.
 //
-// Two kernels:
-//   gemm_stream (M <= 64): the weights are streamed once; each workgroup owns 64 output
-//     channels (one 16-channel tile per wave) and one slice of K; activation tiles are
-//     shared through LDS; weight tiles go straight from HBM to registers with a
-//     several-step prefetch ring.  K slices are combined exactly in INT32 by the last
-//     workgroup to finish its output tile.
-//   gemm_tile (M > 64): 128 x 128 output tiles, 2 x 2 waves of 64 x 64, both operands
-//     double-buffered through LDS, optional split-K with the same exact combination.
+// Two GEMM kernels:
+//   gemm_stream (M <= 64): streams the weights once; a workgroup owns 64 output
+//     channels and a slice of K (optionally split again between two wave groups that
+//     add up in LDS); the activation slice is staged to LDS in one batch.
+//   gemm_tile (M > 64): 128 x 128 output tiles fed through a ring of LDS stages.
+// When K is split across workgroups, each slice writes its raw INT32 tile to a
+// partial buffer and a small epilogue kernel adds the slices (exact) and rescales;
+// the kernel boundary orders the two, so no atomics or cache-wide fences are needed.
+// Output tiles are staged through LDS so that global stores are 16-byte coalesced.
 #include "fq_device.hpp"
 #include "fq_launch.hpp"
 
@@ -155,10 +156,8 @@ struct GemmParams {
   int64_t ldy;
   int32_t *acc_out;
   int M, N, K;
-  int ksteps;  // k steps of 128 per split
-  int32_t *partial;
-  uint32_t *counters;
-  int red_atomic;  // 1: K slices combine with device atomics into one [M, N] buffer
+  int ksteps;        // k steps of 128 per K slice
+  int32_t *partial;  // [slices][M][N] raw accumulators when K is split
 };
 
 template <int BITS, int AFMT>
@@ -170,16 +169,6 @@ struct Fmt {
   static constexpr int shift = BITS == 8 ? 0 : (AFMT == kANibble ? 8 : 4);
 };
 
-// Activation operand of lane (row, g) for k-chunk c from a row of one k step.
-template <int AFMT>
-__device__ __forceinline__ v4i a_operand(const uint8_t *row, int g, int c) {
-  if constexpr (AFMT == kANibble) {
-    return widen8(*reinterpret_cast<const v2i *>(row + g * 16 + c * 8));
-  } else {
-    return *reinterpret_cast<const v4i *>(row + g * 32 + c * 16);
-  }
-}
-
 // Weight operand of lane l for k-chunk c from one tile.
 template <int BITS>
 __device__ __forceinline__ v4i w_operand(const uint8_t *tile, int l, int c) {
@@ -190,304 +179,386 @@ __device__ __forceinline__ v4i w_operand(const uint8_t *tile, int l, int c) {
   }
 }
 
-// Eq. (8) epilogue for one 16 x 16 accumulator tile held by a wave: lane l holds rows
-// 4*(l/16) + r (r = 0..3) of column l % 16.
-template <int SHIFT>
-__device__ __forceinline__ void epilogue16(const GemmParams &p, v4i acc, int m_base, int n_base,
-                                           int lane) {
-  const int n = n_base + (lane & 15);
-  if (n >= p.N) return;
-  const float sw = p.w_scale[n];
-  const float bj = p.bias ? p.bias[n] : 0.0f;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int m = m_base + 4 * (lane >> 4) + r;
-    if (m < p.M) {
-      const int a = acc[r] >> SHIFT;
-      if (p.acc_out) p.acc_out[(int64_t)m * p.N + n] = a;
-      const float sc = sw * p.delta[m];
-      const float yv = (float)a * sc + bj;
-      p.y[(int64_t)m * p.ldy + n] = (uint16_t)f32_to_bf16(yv);
-    }
-  }
+__device__ __forceinline__ void lds_fence() { asm volatile("" ::: "memory"); }
+
+// Workgroup barrier that waits only for this wave's LDS accesses.  __syncthreads() also
+// waits for every outstanding global load (vmcnt(0)), which would drain a prefetch ring.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  lds_fence();
 }
 
-// Split-K: publish this workgroup's raw partial tile; returns true in the one workgroup
-// that arrives last for the output tile, after adding every other slice's partial into
-// `acc` (integer addition: exact, order-free).  Partial layout: [split][M][N].
-template <int TI, int TJ>
-__device__ __forceinline__ bool splitk_combine(const GemmParams &p, v4i (&acc)[TI][TJ],
-                                               const int (&m_base)[TI], const int (&n_base)[TJ],
-                                               int lane, int split, int nsplit, int tile_id) {
-  __shared__ int s_last;
-  const int64_t slice = (int64_t)p.M * p.N;
-  if (p.red_atomic) {
-    // every slice adds into one zeroed [M, N] buffer; the last arrival reads the totals
-    // back with exchanges that also re-zero the buffer for the next call
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int n = n_base[j] + (lane & 15);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m_base[i] + 4 * (lane >> 4) + r;
-          if (m < p.M && n < p.N)
-            __hip_atomic_fetch_add(&p.partial[(int64_t)m * p.N + n], acc[i][j][r], __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      const uint32_t prev = __hip_atomic_fetch_add(&p.counters[tile_id], 1u, __ATOMIC_RELAXED,
-                                                   __HIP_MEMORY_SCOPE_AGENT);
-      s_last = (prev == (uint32_t)(nsplit - 1));
-    }
-    __syncthreads();
-    if (!s_last) return false;
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int n = n_base[j] + (lane & 15);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m_base[i] + 4 * (lane >> 4) + r;
-          if (m < p.M && n < p.N)
-            acc[i][j][r] = __hip_atomic_exchange(&p.partial[(int64_t)m * p.N + n], 0, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-        }
-      }
-    if (threadIdx.x == 0)
-      __hip_atomic_store(&p.counters[tile_id], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return true;
-  }
+// ---------------- output stage ----------------
+//
+// A wave holds 16 x 16 accumulator tiles in the MFMA layout (lane l: rows 4*(l/16)+r,
+// column l%16).  The workgroup's whole R x C output tile is written to LDS first and
+// then leaves in 16-byte row chunks: either the final bf16 y (eq. (8) rescale applied
+// by the lane that owns the value) or the raw INT32 slice of a split K.
+
+struct EpiParams {  // per-lane rescale factors, loaded before the main loop
+  float sw, bj;
+};
+
+__device__ __forceinline__ float rescale(int acc_shifted, float sw, float dt, float bj) {
+  return (float)acc_shifted * (sw * dt) + bj;
+}
+
+// Stage one wave's tile (rows row0 + 16 i + 4 g + r, cols col0 + 16 j + l%16) in LDS.
+// mode_final: bf16 with rescale; else raw int32.
+template <int TI, int TJ, int SHIFT, bool FINAL>
+__device__ __forceinline__ void stage_tiles(uint8_t *lds, int C, const v4i (&acc)[TI][TJ], int row0,
+                                            int col0, int lane, const float (&dt)[TI][4],
+                                            const EpiParams (&ep)[TJ]) {
+  const int g = lane >> 4, cl = lane & 15;
+  const int stride = FINAL ? C * 2 + 16 : C * 4 + 16;
 #pragma unroll
   for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-      const int n = n_base[j] + (lane & 15);
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int m = m_base[i] + 4 * (lane >> 4) + r;
-        if (m < p.M && n < p.N) p.partial[split * slice + (int64_t)m * p.N + n] = acc[i][j][r];
-      }
-    }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t prev = atomicAdd(&p.counters[tile_id], 1u);
-    s_last = (prev == (uint32_t)(nsplit - 1));
-  }
-  __syncthreads();
-  if (!s_last) return false;
-  __threadfence();
-  for (int z = 0; z < nsplit; ++z) {
-    if (z == split) continue;
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) {
-        const int n = n_base[j] + (lane & 15);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m_base[i] + 4 * (lane >> 4) + r;
-          if (m < p.M && n < p.N)
-            acc[i][j][r] += p.partial[z * slice + (int64_t)m * p.N + n];
+        const int row = row0 + 16 * i + 4 * g + r, col = col0 + 16 * j + cl;
+        if constexpr (FINAL) {
+          const float v = rescale(acc[i][j][r] >> SHIFT, ep[j].sw, dt[i][r], ep[j].bj);
+          *reinterpret_cast<uint16_t *>(lds + row * stride + col * 2) = (uint16_t)f32_to_bf16(v);
+        } else {
+          *reinterpret_cast<int32_t *>(lds + row * stride + col * 4) = acc[i][j][r];
         }
       }
+}
+
+// Copy the staged R x C tile (origin m0, n0) to global memory in 16-byte chunks.
+template <bool FINAL>
+__device__ __forceinline__ void store_staged(const uint8_t *lds, int R, int C, int m0, int n0,
+                                             const GemmParams &p, int split, int nthreads) {
+  const int stride = FINAL ? C * 2 + 16 : C * 4 + 16;
+  const int cpr = FINAL ? C / 8 : C / 4;  // 16-byte chunks per row
+  for (int q = threadIdx.x; q < R * cpr; q += nthreads) {
+    const int row = q / cpr, ch = q % cpr;
+    const int m = m0 + row;
+    const int n = n0 + ch * (FINAL ? 8 : 4);
+    if (m < p.M && n < p.N) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(lds + row * stride + ch * 16);
+      if constexpr (FINAL)
+        *reinterpret_cast<uint4 *>(p.y + (int64_t)m * p.ldy + n) = v;
+      else
+        *reinterpret_cast<uint4 *>(p.partial + ((int64_t)split * p.M + m) * p.N + n) = v;
+    }
   }
-  if (threadIdx.x == 0) p.counters[tile_id] = 0u;  // ready for the next call
-  return true;
+}
+
+// Raw accumulators for verification (acc_out != NULL): direct stores, not a fast path.
+template <int TI, int TJ, int SHIFT>
+__device__ __forceinline__ void store_acc_out(const GemmParams &p, const v4i (&acc)[TI][TJ],
+                                              int m_base, int n_base, int lane) {
+  const int g = lane >> 4, cl = lane & 15;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m_base + 16 * i + 4 * g + r, n = n_base + 16 * j + cl;
+        if (m < p.M && n < p.N) p.acc_out[(int64_t)m * p.N + n] = acc[i][j][r] >> SHIFT;
+      }
+}
+
+template <int TI, int TJ>
+__device__ __forceinline__ void load_epi(const GemmParams &p, int m_base, int n_base, int lane,
+                                         float (&dt)[TI][4], EpiParams (&ep)[TJ]) {
+  const int g = lane >> 4, cl = lane & 15;
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = min(m_base + 16 * i + 4 * g + r, p.M - 1);
+      dt[i][r] = p.delta[m];
+    }
+#pragma unroll
+  for (int j = 0; j < TJ; ++j) {
+    const int n = min(n_base + 16 * j + cl, p.N - 1);
+    ep[j].sw = p.w_scale[n];
+    ep[j].bj = p.bias ? p.bias[n] : 0.0f;
+  }
+}
+
+// ---------------- split-K epilogue ----------------
+// Adds the K slices of the raw INT32 partials (exact, fixed order), divides out the
+// widening scale and applies the eq. (8) rescale; 8 output columns per thread.
+template <int SHIFT>
+__global__ __launch_bounds__(256) void splitk_epilogue_kernel(GemmParams p, int slices) {
+  const int cpr = p.N / 8;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)p.M * cpr) return;
+  const int m = (int)(idx / cpr), n = (int)(idx % cpr) * 8;
+  int a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  for (int z = 0; z < slices; ++z) {
+    const int4 *src = reinterpret_cast<const int4 *>(p.partial + ((int64_t)z * p.M + m) * p.N + n);
+    const int4 u = src[0], v = src[1];
+    a[0] += u.x; a[1] += u.y; a[2] += u.z; a[3] += u.w;
+    a[4] += v.x; a[5] += v.y; a[6] += v.z; a[7] += v.w;
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) a[i] >>= SHIFT;
+  if (p.acc_out) {
+    int4 *d = reinterpret_cast<int4 *>(p.acc_out + (int64_t)m * p.N + n);
+    d[0] = make_int4(a[0], a[1], a[2], a[3]);
+    d[1] = make_int4(a[4], a[5], a[6], a[7]);
+  }
+  const float dt = p.delta[m];
+  const float4 s0 = *reinterpret_cast<const float4 *>(p.w_scale + n);
+  const float4 s1 = *reinterpret_cast<const float4 *>(p.w_scale + n + 4);
+  const float sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+  float bj[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (p.bias) {
+    const float4 b0 = *reinterpret_cast<const float4 *>(p.bias + n);
+    const float4 b1 = *reinterpret_cast<const float4 *>(p.bias + n + 4);
+    bj[0] = b0.x; bj[1] = b0.y; bj[2] = b0.z; bj[3] = b0.w;
+    bj[4] = b1.x; bj[5] = b1.y; bj[6] = b1.z; bj[7] = b1.w;
+  }
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    o[i] = f32_to_bf16(rescale(a[2 * i], sw[2 * i], dt, bj[2 * i])) |
+           (f32_to_bf16(rescale(a[2 * i + 1], sw[2 * i + 1], dt, bj[2 * i + 1])) << 16);
+  *reinterpret_cast<uint4 *>(p.y + (int64_t)m * p.ldy + n) = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
 // ---------------- streaming kernel (M <= 64) ----------------
+//
+// Workgroup = 4 x WK waves: 64 output channels (one 16-channel tile per wave column) x a
+// K slice of WK * KT k steps; wave group kg takes KT consecutive steps of the slice.
+// Every wave first issues the loads of all KT of its weight tiles (they stay in flight
+// while the activation slice is staged), the activation slice (rows < M) goes to LDS in
+// one batch, and the MFMA loop then runs out of registers and LDS.  The WK groups add
+// up through LDS; the 64-channel tile leaves through the LDS output stage.
 
-constexpr int kStreamPF = 4;  // weight k steps in flight per wave
-
-template <int BITS, int AFMT, int MT>
-__global__ __launch_bounds__(256) void gemm_stream_kernel(GemmParams p) {
+template <int BITS, int AFMT, int MT, int KT, int WK>
+__global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
   using F = Fmt<BITS, AFMT>;
-  constexpr int AROWP = F::arow + 16;
-  constexpr int ASTAGE = MT * 16 * AROWP;
-  constexpr int ACHUNKS = MT * 16 * F::arow / 16;
-  constexpr int LU4 = F::lb / 16;  // uint4 per lane per weight tile
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * ASTAGE];
+  constexpr int NTHREADS = 256 * WK;
+  constexpr int LU4 = F::lb / 16;           // 16-byte loads per lane per weight tile
+  constexpr int AROW = WK * KT * F::arow;   // activation bytes per row in the slice
+  constexpr int AROWP = AROW + 16;          // padded LDS row stride
+  constexpr int ROWS = MT * 16;
+  constexpr int CPR = AROW / 16;            // 16-byte chunks per row
+  constexpr int ACH = ROWS * CPR;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
+  const int wn = wave & 3, kg = wave >> 2;
   const int nblk = blockIdx.x;
   const int split = blockIdx.y;
   const int nsplit = gridDim.y;
   const int ktot = p.K / kTileK;
-  const int ks_begin = split * p.ksteps;
-  const int nk = min(p.ksteps, ktot - ks_begin);
-  const int ntile = nblk * 4 + wave;  // this wave's 16-channel tile
+  const int slice_begin = split * WK * KT;
+  const int ks_begin = slice_begin + kg * KT;
+  const int nk = max(0, min(KT, ktot - ks_begin));
+  const int ntile = nblk * 4 + wn;
   const bool n_ok = ntile * 16 < p.N;
 
-  const uint8_t *wbase = p.w + ((int64_t)ntile * ktot + ks_begin) * F::tb + lane * F::lb;
-
-  // activation tile loader: chunk q -> row q / (arow/16), 16-byte column q % (arow/16)
-  uint4 areg[(ACHUNKS + 255) / 256];
-  auto load_a = [&](int ks) {
+  // 1. all weight tiles of this wave in flight
+  uint4 wreg[KT][LU4];
+  const uint8_t *wbase = p.w + ((int64_t)min(ntile, p.N / 16 - 1) * ktot + ks_begin) * F::tb + lane * F::lb;
 #pragma unroll
-    for (int i = 0; i < (ACHUNKS + 255) / 256; ++i) {
-      const int q = i * 256 + tid;
-      areg[i] = make_uint4(0, 0, 0, 0);
-      if (q < ACHUNKS) {
-        const int row = q / (F::arow / 16), col = q % (F::arow / 16);
-        if (row < p.M)
-          areg[i] = *reinterpret_cast<const uint4 *>(p.a + (int64_t)row * p.lda +
-                                                     (int64_t)(ks_begin + ks) * F::arow + col * 16);
-      }
-    }
-  };
-  auto store_a = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < (ACHUNKS + 255) / 256; ++i) {
-      const int q = i * 256 + tid;
-      if (q < ACHUNKS) {
-        const int row = q / (F::arow / 16), col = q % (F::arow / 16);
-        *reinterpret_cast<uint4 *>(lds + buf * ASTAGE + row * AROWP + col * 16) = areg[i];
-      }
-    }
-  };
-
-  uint4 wring[kStreamPF][LU4];
-#pragma unroll
-  for (int s = 0; s < kStreamPF; ++s)
+  for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
     for (int u = 0; u < LU4; ++u)
-      wring[s][u] = (n_ok && s < nk) ? reinterpret_cast<const uint4 *>(wbase + (int64_t)s * F::tb)[u]
-                                     : make_uint4(0, 0, 0, 0);
+      wreg[kt][u] = (kt < nk) ? reinterpret_cast<const uint4 *>(wbase + (int64_t)kt * F::tb)[u]
+                              : make_uint4(0, 0, 0, 0);
 
-  v4i acc[MT];
+  float dt[MT][4];
+  EpiParams ep[1];
+  if (nsplit == 1) load_epi<MT, 1>(p, 0, ntile * 16, lane, dt, ep);
+
+  // 2. activation slice -> LDS (rows >= M are not loaded: they only feed rows >= M)
+  const uint8_t *abase = p.a + (int64_t)slice_begin * F::arow;
+  const int valid_cols = min(WK * KT, ktot - slice_begin) * (F::arow / 16);
 #pragma unroll
-  for (int i = 0; i < MT; ++i) acc[i] = v4i{0, 0, 0, 0};
-
-  if (nk > 0) {
-    load_a(0);
-    store_a(0);
+  for (int i = 0; i < (ACH + NTHREADS - 1) / NTHREADS; ++i) {
+    const int q = i * NTHREADS + tid;
+    if (q < ACH) {
+      const int row = q / CPR, col = q % CPR;
+      if (row < p.M && col < valid_cols)
+        *reinterpret_cast<uint4 *>(lds + row * AROWP + col * 16) =
+            *reinterpret_cast<const uint4 *>(abase + (int64_t)row * p.lda + col * 16);
+    }
   }
   __syncthreads();
 
-  for (int ks0 = 0; ks0 < nk; ks0 += kStreamPF) {
+  // 3. MFMA over the wave's k steps
+  v4i acc[MT][1];
 #pragma unroll
-    for (int s = 0; s < kStreamPF; ++s) {
-      const int ks = ks0 + s;
-      if (ks < nk) {
-        if (ks + 1 < nk) load_a(ks + 1);
-        uint4 wcur[LU4];
+  for (int i = 0; i < MT; ++i) acc[i][0] = v4i{0, 0, 0, 0};
+  const uint8_t *arow = lds + (lane & 15) * AROWP + kg * KT * F::arow;
 #pragma unroll
-        for (int u = 0; u < LU4; ++u) wcur[u] = wring[s][u];
-        if (n_ok && ks + kStreamPF < nk) {
+  for (int kt = 0; kt < KT; ++kt) {
+    if (kt < nk) {
 #pragma unroll
-          for (int u = 0; u < LU4; ++u)
-            wring[s][u] = reinterpret_cast<const uint4 *>(wbase + (int64_t)(ks + kStreamPF) * F::tb)[u];
+      for (int c = 0; c < 2; ++c) {
+        v4i bop;
+        if constexpr (BITS == 4) {
+          v2i h;
+          h.x = (int)(c == 0 ? wreg[kt][0].x : wreg[kt][0].z);
+          h.y = (int)(c == 0 ? wreg[kt][0].y : wreg[kt][0].w);
+          bop = widen8(h);
+        } else {
+          const uint4 t = wreg[kt][c];
+          bop = v4i{(int)t.x, (int)t.y, (int)t.z, (int)t.w};
         }
-        const uint8_t *abuf = lds + (ks & 1) * ASTAGE;
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          v4i bop;
-          if constexpr (BITS == 4) {
-            v2i h;
-            h.x = (int)(c == 0 ? wcur[0].x : wcur[0].z);
-            h.y = (int)(c == 0 ? wcur[0].y : wcur[0].w);
-            bop = widen8(h);
-          } else {
-            const uint4 t = wcur[c];
-            bop = v4i{(int)t.x, (int)t.y, (int)t.z, (int)t.w};
-          }
-#pragma unroll
-          for (int i = 0; i < MT; ++i) {
-            const v4i aop = a_operand<AFMT>(abuf + (i * 16 + (lane & 15)) * AROWP, lane >> 4, c);
-            acc[i] = mfma16x16x64(aop, bop, acc[i]);
-          }
+        for (int i = 0; i < MT; ++i) {
+          const uint8_t *q = arow + i * 16 * AROWP + kt * F::arow;
+          v4i aop;
+          if constexpr (AFMT == kANibble)
+            aop = widen8(*reinterpret_cast<const v2i *>(q + (lane >> 4) * 16 + c * 8));
+          else
+            aop = *reinterpret_cast<const v4i *>(q + (lane >> 4) * 32 + c * 16);
+          acc[i][0] = mfma16x16x64(aop, bop, acc[i][0]);
         }
-        if (ks + 1 < nk) store_a((ks + 1) & 1);
-        __syncthreads();
       }
     }
   }
 
-  int m_base[MT];
+  // 4. wave groups add up in LDS, then the 64-channel tile leaves through the LDS stage
+  __syncthreads();  // the activation slice is no longer read
+  if constexpr (WK == 2) {
+    v4i *red = reinterpret_cast<v4i *>(lds);
+    if (kg == 1) {
 #pragma unroll
-  for (int i = 0; i < MT; ++i) m_base[i] = i * 16;
-  int n_base[1] = {ntile * 16};
-  v4i acc2[MT][1];
+      for (int i = 0; i < MT; ++i) red[(wn * MT + i) * 64 + lane] = acc[i][0];
+    }
+    __syncthreads();
+    if (kg == 0) {
 #pragma unroll
-  for (int i = 0; i < MT; ++i) acc2[i][0] = acc[i];
-  if (nsplit > 1) {
-    if (!splitk_combine<MT, 1>(p, acc2, m_base, n_base, lane, split, nsplit, nblk)) return;
+      for (int i = 0; i < MT; ++i) acc[i][0] += red[(wn * MT + i) * 64 + lane];
+    }
+    __syncthreads();
   }
-  if (!n_ok) return;
-#pragma unroll
-  for (int i = 0; i < MT; ++i) epilogue16<F::shift>(p, acc2[i][0], m_base[i], n_base[0], lane);
+  uint8_t *stage = lds + (WK == 2 ? 4 * MT * 64 * 16 : 0);
+  if (kg == 0) {
+    if (p.acc_out && nsplit == 1 && n_ok) store_acc_out<MT, 1, F::shift>(p, acc, 0, ntile * 16, lane);
+    if (nsplit == 1)
+      stage_tiles<MT, 1, F::shift, true>(stage, 64, acc, 0, wn * 16, lane, dt, ep);
+    else
+      stage_tiles<MT, 1, F::shift, false>(stage, 64, acc, 0, wn * 16, lane, dt, ep);
+  }
+  __syncthreads();
+  if (nsplit == 1)
+    store_staged<true>(stage, ROWS, 64, 0, nblk * 64, p, 0, NTHREADS);
+  else
+    store_staged<false>(stage, ROWS, 64, 0, nblk * 64, p, split, NTHREADS);
+}
+
+template <int BITS, int AFMT, int MT, int KT, int WK>
+static size_t stream_lds_bytes() {
+  const size_t slice = (size_t)MT * 16 * (WK * KT * Fmt<BITS, AFMT>::arow + 16);
+  const size_t out = (WK == 2 ? (size_t)4 * MT * 64 * 16 : 0) + (size_t)MT * 16 * (64 * 4 + 16);
+  return slice > out ? slice : out;
 }
 
 // ---------------- tiled kernel (M > 64) ----------------
+//
+// BM x BN output tile per workgroup (2 x 2 waves), k steps of 128 channels.  Operands
+// move HBM/L2 -> LDS with gfx950's direct-to-LDS loads (global_load_lds_dwordx4: each
+// wave instruction fills one contiguous KB of LDS, no registers involved) into a ring of
+// STAGES buffers, so loads for k step ks + STAGES - 1 are in flight while step ks is
+// multiplied.  Activation rows are XOR-swizzled in 16-byte chunks so the 16 rows a
+// wave reads at once fall into distinct LDS banks; weight tiles keep their
+// lane-contiguous kernel-native layout, which is already conflict-free.
 
-template <int BITS, int AFMT, int BM, int BN>
+// 16 bytes per lane from global memory straight into LDS; a wave fills the contiguous
+// KB at `lds_dst` (lane l -> lds_dst + 16 l).  The builtin exists only for the device
+// pass, so the host pass (which only needs the kernel stub) sees an empty body.
+__device__ __forceinline__ void load_to_lds16(const void *src, void *lds_dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
+#else
+  (void)src;
+  (void)lds_dst;
+#endif
+}
+
+// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+template <int AFMT>
+__device__ __forceinline__ int a_swizzle(int row) {
+  return AFMT == kANibble ? ((row >> 1) & 3) : ((row >> 1) & 7);
+}
+
+// Logical tile order that keeps consecutive tiles (same activation rows) on one XCD:
+// the hardware hands workgroup p to XCD p % 8.
+__device__ __forceinline__ int xcd_remap(int p, int total) {
+  if ((total & 7) != 0) return p;
+  return (p & 7) * (total >> 3) + (p >> 3);
+}
+
+template <int BITS, int AFMT, int BM, int BN, int STAGES>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   using F = Fmt<BITS, AFMT>;
-  constexpr int AROWP = F::arow + 16;
-  constexpr int NT = BN / 16;
-  constexpr int ASTAGE = BM * AROWP;
+  constexpr int CPR = F::arow / 16;              // 16-byte activation chunks per row per step
+  constexpr int NT = BN / 16;                    // weight tiles per step
+  constexpr int ASTAGE = BM * F::arow;
   constexpr int BSTAGE = NT * F::tb;
-  constexpr int ACH = BM * F::arow / 16 / 256;  // 16-byte activation chunks per thread
-  constexpr int BCH = NT * F::tb / 16 / 256;    // 16-byte weight chunks per thread
-  constexpr int TM = BM / 32, TN = NT / 2;      // 16x16 tiles per wave (2 x 2 waves)
-  static_assert(ACH >= 1 && BCH >= 1, "tile too small for 256 threads");
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * (ASTAGE + BSTAGE)];
+  constexpr int STAGE = ASTAGE + BSTAGE;
+  constexpr int IA = BM * CPR / 256;             // activation load instructions per wave per step
+  constexpr int IB = BSTAGE / 1024 / 4;          // weight load instructions per wave per step
+  constexpr int LPS = IA + IB;                   // loads per wave per step
+  constexpr int TM = BM / 32, TN = NT / 2;       // 16 x 16 tiles per wave
+  static_assert(IA >= 1 && IB >= 1, "tile too small");
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int ntiles_n = (p.N + BN - 1) / BN;
-  const int tile_id = blockIdx.x;
+  const int ntiles_m = (p.M + BM - 1) / BM;
+  const int total = ntiles_n * ntiles_m * gridDim.y;
+  const int logical = xcd_remap(blockIdx.x + blockIdx.y * gridDim.x, total);
+  const int tile_id = logical % (ntiles_n * ntiles_m);
+  const int split = logical / (ntiles_n * ntiles_m);
+  const int nsplit = gridDim.y;
   const int tn = tile_id % ntiles_n, tm = tile_id / ntiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
-  const int split = blockIdx.y, nsplit = gridDim.y;
   const int ktot = p.K / kTileK;
   const int ks_begin = split * p.ksteps;
   const int nk = min(p.ksteps, ktot - ks_begin);
 
-  uint4 ar[ACH], br[BCH];
-  auto load = [&](int ks) {
-    const int kk = ks_begin + ks;
+  // per-lane global sources of this wave's load instructions (k step 0 of the slice)
+  const uint8_t *asrc[IA];
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int q = i * 256 + tid;
-      const int row = q / (F::arow / 16), col = q % (F::arow / 16);
-      ar[i] = (m0 + row < p.M)
-                  ? *reinterpret_cast<const uint4 *>(p.a + (int64_t)(m0 + row) * p.lda +
-                                                     (int64_t)kk * F::arow + col * 16)
-                  : make_uint4(0, 0, 0, 0);
-    }
+  for (int i = 0; i < IA; ++i) {
+    const int slot = (wave * IA + i) * 64 + lane;
+    const int row = slot / CPR, pos = slot % CPR;
+    const int logical_chunk = pos ^ a_swizzle<AFMT>(row);
+    const int grow = min(m0 + row, p.M - 1);  // rows past M load row M-1: they only feed rows >= M
+    asrc[i] = p.a + (int64_t)grow * p.lda + (int64_t)ks_begin * F::arow + logical_chunk * 16;
+  }
+  const uint8_t *bsrc[IB];
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int q = i * 256 + tid;
-      const int t = q / (F::tb / 16), off = (q % (F::tb / 16)) * 16;
-      const int nb = n0 / 16 + t;
-      br[i] = (nb * 16 < p.N)
-                  ? *reinterpret_cast<const uint4 *>(p.w + ((int64_t)nb * ktot + kk) * F::tb + off)
-                  : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto store = [&](int buf) {
-    uint8_t *la = lds + buf * (ASTAGE + BSTAGE);
-    uint8_t *lb = la + ASTAGE;
+  for (int i = 0; i < IB; ++i) {
+    const int j = wave * IB + i;                 // KB index inside the weight stage
+    const int t = j / (F::tb / 1024), h = j % (F::tb / 1024);
+    const int nb = min(n0 / 16 + t, p.N / 16 - 1);  // tiles past N load the last tile
+    bsrc[i] = p.w + ((int64_t)nb * ktot + ks_begin) * F::tb + h * 1024 + lane * 16;
+  }
+  auto issue = [&](int ks) {
+    uint8_t *st = lds + (ks % STAGES) * STAGE;
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int q = i * 256 + tid;
-      const int row = q / (F::arow / 16), col = q % (F::arow / 16);
-      *reinterpret_cast<uint4 *>(la + row * AROWP + col * 16) = ar[i];
-    }
+    for (int i = 0; i < IA; ++i)
+      load_to_lds16(asrc[i] + (int64_t)ks * F::arow, st + (wave * IA + i) * 1024);
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) *reinterpret_cast<uint4 *>(lb + (i * 256 + tid) * 16) = br[i];
+    for (int i = 0; i < IB; ++i)
+      load_to_lds16(bsrc[i] + (int64_t)ks * F::tb, st + ASTAGE + (wave * IB + i) * 1024);
   };
 
   v4i acc[TM][TN];
@@ -496,21 +567,40 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
 
-  if (nk > 0) {
-    load(0);
-    store(0);
-  }
-  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s);
+
+  const int m_wave = m0 + wm * (BM / 2), n_wave = n0 + wn * (BN / 2);
+  float dt[TM][4];
+  EpiParams ep[TN];
+  if (nsplit == 1) load_epi<TM, TN>(p, m_wave, n_wave, lane, dt, ep);
+
   for (int ks = 0; ks < nk; ++ks) {
-    if (ks + 1 < nk) load(ks + 1);
-    const uint8_t *la = lds + (ks & 1) * (ASTAGE + BSTAGE);
+    // loads of step ks are done once at most the later steps' loads are outstanding
+    const int later = min(STAGES - 2, nk - 1 - ks);
+    if (later >= 2) wait_vmcnt<2 * LPS>();
+    else if (later == 1) wait_vmcnt<LPS>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (ks + STAGES - 1 < nk) issue(ks + STAGES - 1);  // refills the stage read at ks - 1
+    const uint8_t *la = lds + (ks % STAGES) * STAGE;
     const uint8_t *lb = la + ASTAGE;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       v4i af[TM], bf[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = a_operand<AFMT>(la + (wm * (BM / 2) + i * 16 + (lane & 15)) * AROWP, lane >> 4, c);
+      for (int i = 0; i < TM; ++i) {
+        const int row = wm * (BM / 2) + i * 16 + (lane & 15);
+        const int g = lane >> 4;
+        if constexpr (AFMT == kANibble) {
+          const uint8_t *q = la + row * F::arow + ((g ^ a_swizzle<AFMT>(row)) * 16) + c * 8;
+          af[i] = widen8(*reinterpret_cast<const v2i *>(q));
+        } else {
+          const uint8_t *q = la + row * F::arow + (((2 * g + c) ^ a_swizzle<AFMT>(row)) * 16);
+          af[i] = *reinterpret_cast<const v4i *>(q);
+        }
+      }
 #pragma unroll
       for (int j = 0; j < TN; ++j) bf[j] = w_operand<BITS>(lb + (wn * TN + j) * F::tb, lane, c);
 #pragma unroll
@@ -518,22 +608,27 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x64(af[i], bf[j], acc[i][j]);
     }
-    if (ks + 1 < nk) store((ks + 1) & 1);
-    __syncthreads();
   }
 
-  int m_base[TM], n_base[TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i) m_base[i] = m0 + wm * (BM / 2) + i * 16;
-#pragma unroll
-  for (int j = 0; j < TN; ++j) n_base[j] = n0 + (wn * TN + j) * 16;
-  if (nsplit > 1) {
-    if (!splitk_combine<TM, TN>(p, acc, m_base, n_base, lane, split, nsplit, tile_id)) return;
+  // output through the LDS stage (the ring is free once every wave is past its last step)
+  __syncthreads();
+  if (nsplit == 1) {
+    if (p.acc_out) store_acc_out<TM, TN, F::shift>(p, acc, m_wave, n_wave, lane);
+    stage_tiles<TM, TN, F::shift, true>(lds, BN, acc, wm * (BM / 2), wn * (BN / 2), lane, dt, ep);
+    __syncthreads();
+    store_staged<true>(lds, BM, BN, m0, n0, p, 0, 256);
+  } else {
+    stage_tiles<TM, TN, F::shift, false>(lds, BN, acc, wm * (BM / 2), wn * (BN / 2), lane, dt, ep);
+    __syncthreads();
+    store_staged<false>(lds, BM, BN, m0, n0, p, split, 256);
   }
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) epilogue16<F::shift>(p, acc[i][j], m_base[i], n_base[j], lane);
+}
+
+template <int BITS, int AFMT, int BM, int BN, int STAGES>
+static constexpr size_t tile_lds_bytes() {
+  constexpr size_t ring = (size_t)STAGES * (BM * Fmt<BITS, AFMT>::arow + BN / 16 * Fmt<BITS, AFMT>::tb);
+  constexpr size_t out = (size_t)BM * (BN * 4 + 16);
+  return ring > out ? ring : out;
 }
 
 // ----------------------------------------------------------------------------------------
@@ -541,9 +636,9 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Development tuning override, read once: FQ_TUNE="splits=<n>,red=<0|1>".
+// Development tuning override, read once: FQ_TUNE="splits=<n>".
 struct Tune {
-  int splits = 0, red = -1;
+  int splits = 0;
 };
 static Tune read_tune() {
   Tune t;
@@ -551,8 +646,6 @@ static Tune read_tune() {
   if (!e) return t;
   const char *s = strstr(e, "splits=");
   if (s) t.splits = atoi(s + 7);
-  s = strstr(e, "red=");
-  if (s) t.red = atoi(s + 4);
   return t;
 }
 
@@ -562,62 +655,99 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
   GemmPlan pl{};
   const int ktot = (int)(K / kTileK);
   if (M <= 64) {
+    // weight streaming: 8 k steps per wave, two wave groups per workgroup once K is long
     pl.kind = 0;
     pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-    const int64_t nblk = (N + 63) / 64;
-    // aim for about two workgroups per compute unit, slices of at least 4 k steps
-    int64_t want = (512 + nblk - 1) / nblk;
-    int64_t maxs = ktot / 4 > 0 ? ktot / 4 : 1;
-    int64_t s = want < maxs ? want : maxs;
-    if (s < 1) s = 1;
-    pl.ksteps = (int)((ktot + s - 1) / s);
+    pl.kt = ktot >= 8 ? 8 : (ktot >= 4 ? 4 : (ktot >= 2 ? 2 : 1));
+    pl.wk = ktot >= 16 ? 2 : 1;
+    if (tune.splits > 0) {
+      int per = (ktot + tune.splits - 1) / tune.splits;  // k steps per slice
+      pl.wk = per >= 16 ? 2 : 1;
+      int kt = (per + pl.wk - 1) / pl.wk;
+      pl.kt = kt >= 8 ? 8 : (kt >= 4 ? 4 : (kt >= 2 ? 2 : 1));
+    }
+    pl.ksteps = pl.kt * pl.wk;
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
-    pl.tiles = nblk;
+    pl.tiles = (N + 63) / 64;
   } else {
     pl.kind = 1;
     pl.bm = 128;
     pl.bn = 128;
     const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
     int64_t s = 1;
-    while (tiles * s < 256 && s < 4 && ktot / (s * 2) >= 8) s *= 2;
+    while (tiles * s < 200 && s < 4 && ktot / (s * 2) >= 32) s *= 2;
+    if (tune.splits > 0) s = tune.splits < ktot ? tune.splits : ktot;
     pl.ksteps = (int)((ktot + s - 1) / s);
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
     pl.tiles = tiles;
   }
-  if (tune.splits > 0) {
-    int64_t sp = tune.splits < ktot ? tune.splits : ktot;
-    pl.ksteps = (int)((ktot + sp - 1) / sp);
-    pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
-  }
-  pl.red_atomic = tune.red == 1 ? 1 : 0;
-  if (pl.tiles > kMaxCounters) {  // too many output tiles to count: no split
-    pl.ksteps = ktot;
-    pl.splits = 1;
-  }
-  pl.partial_bytes = pl.splits > 1 ? align256((size_t)(pl.red_atomic ? 1 : pl.splits) * M * N * 4) : 0;
-  pl.counter_bytes = pl.splits > 1 ? kCounterRegionBytes : 0;
+  pl.partial_bytes = pl.splits > 1 ? align256((size_t)pl.splits * M * N * 4) : 0;
   return pl;
 }
 
-size_t gemm_plan_workspace(const GemmPlan &pl) { return pl.partial_bytes + pl.counter_bytes; }
+size_t gemm_plan_workspace(const GemmPlan &pl) { return pl.partial_bytes; }
 
-template <int BITS, int AFMT>
-static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStream_t s) {
-  if (pl.kind == 0) {
-    dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
-    switch (pl.mt) {
-      case 1: hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, 1>), grid, dim3(256), 0, s, p); break;
-      case 2: hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, 2>), grid, dim3(256), 0, s, p); break;
-      default: hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, 4>), grid, dim3(256), 0, s, p); break;
-    }
-  } else {
-    dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
-    hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128>), grid, dim3(256), 0, s, p);
+template <typename Kern>
+static hipError_t allow_lds(Kern kern, size_t lds, bool &done) {
+  if (lds > 65536 && !done) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    done = true;
   }
+  return hipSuccess;
+}
+
+template <int BITS, int AFMT, int MT, int KT, int WK>
+static hipError_t launch_stream(const GemmParams &p, dim3 grid, hipStream_t s) {
+  const size_t lds = stream_lds_bytes<BITS, AFMT, MT, KT, WK>();
+  static bool attr = false;
+  hipError_t e = allow_lds(&gemm_stream_kernel<BITS, AFMT, MT, KT, WK>, lds, attr);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, MT, KT, WK>), grid, dim3(256 * WK), lds, s, p);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, size_t gap, hipStream_t s) {
+template <int BITS, int AFMT, int MT>
+static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, dim3 grid, hipStream_t s) {
+  if (wk == 2) return launch_stream<BITS, AFMT, MT, 8, 2>(p, grid, s);
+  switch (kt) {
+    case 1: return launch_stream<BITS, AFMT, MT, 1, 1>(p, grid, s);
+    case 2: return launch_stream<BITS, AFMT, MT, 2, 1>(p, grid, s);
+    case 4: return launch_stream<BITS, AFMT, MT, 4, 1>(p, grid, s);
+    default: return launch_stream<BITS, AFMT, MT, 8, 1>(p, grid, s);
+  }
+}
+
+template <int BITS, int AFMT>
+static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStream_t s) {
+  hipError_t e;
+  if (pl.kind == 0) {
+    dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
+    switch (pl.mt) {
+      case 1: e = launch_stream_mt<BITS, AFMT, 1>(p, pl.kt, pl.wk, grid, s); break;
+      case 2: e = launch_stream_mt<BITS, AFMT, 2>(p, pl.kt, pl.wk, grid, s); break;
+      default: e = launch_stream_mt<BITS, AFMT, 4>(p, pl.kt, pl.wk, grid, s); break;
+    }
+  } else {
+    dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
+    constexpr int ST = 3;
+    constexpr size_t lds = tile_lds_bytes<BITS, AFMT, 128, 128, ST>();
+    static bool attr = false;
+    e = allow_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST>, lds, attr);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128, ST>), grid, dim3(256), lds, s, p);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess || pl.splits == 1) return e;
+  const int64_t threads = (int64_t)p.M * (p.N / 8);
+  const unsigned blocks = (unsigned)((threads + 255) / 256);
+  hipLaunchKernelGGL((splitk_epilogue_kernel<Fmt<BITS, AFMT>::shift>), dim3(blocks), dim3(256), 0, s, p,
+                     pl.splits);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   GemmParams p;
   p.a = g.a;
@@ -633,12 +763,7 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, size_t g
   p.N = (int)g.N;
   p.K = (int)g.K;
   p.ksteps = pl.ksteps;
-  p.red_atomic = pl.red_atomic;
-  // counters first, at a fixed offset, so that calls of any shape can share a workspace
-  p.counters = pl.splits > 1 ? reinterpret_cast<uint32_t *>(ws) : nullptr;
-  p.partial = pl.splits > 1 ? reinterpret_cast<int32_t *>(reinterpret_cast<uint8_t *>(ws) +
-                                                          kCounterRegionBytes + gap)
-                            : nullptr;
+  p.partial = pl.splits > 1 ? reinterpret_cast<int32_t *>(ws) : nullptr;
   if (g.bits == 4)
     return g.a_fmt == kANibble ? launch_gemm_t<4, kANibble>(p, pl, s) : launch_gemm_t<4, kAInt8>(p, pl, s);
   return launch_gemm_t<8, kAInt8>(p, pl, s);

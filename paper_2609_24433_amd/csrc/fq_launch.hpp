@@ -26,22 +26,16 @@ hipError_t launch_pack_weights(const int8_t *codes, int64_t N, int K, int bits, 
 hipError_t launch_unpack_weights(const uint8_t *packed, int64_t N, int K, int bits, int8_t *codes,
                                  hipStream_t s);
 
-// Split-K arrival counters occupy the first kCounterRegionBytes of every GEMM workspace,
-// one 32-bit counter per output tile; every call leaves them at zero.
-constexpr size_t kCounterRegionBytes = 65536;
-constexpr int64_t kMaxCounters = kCounterRegionBytes / 4;
-
 // GEMM plan: which kernel, its tiling and its split of K.
 struct GemmPlan {
   int kind;     // 0 = streaming (M <= 64), 1 = tiled
   int mt;       // streaming: 16-row tiles covering M
+  int kt, wk;   // streaming: k steps per wave, wave groups along K per workgroup
   int bm, bn;   // tiled: workgroup tile
-  int splits;   // K slices
+  int splits;   // K slices (each slice: ksteps k steps); > 1 adds an epilogue kernel
   int ksteps;   // 128-wide k steps per slice
-  int red_atomic;  // K slices combined with device atomics (else partial buffers)
-  int64_t tiles;        // output tiles (counter slots)
-  size_t partial_bytes; // split-K partial sums
-  size_t counter_bytes;
+  int64_t tiles;        // output tiles along the grid's x dimension
+  size_t partial_bytes; // split-K INT32 partials [splits][M][N]
 };
 
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits);
@@ -62,7 +56,7 @@ struct GemmArgs {
   int bits;
 };
 
-// ws: [counters (kCounterRegionBytes)][gap bytes, untouched][partials]
-hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, size_t gap, hipStream_t s);
+// ws: at least gemm_plan_workspace(pl) bytes of scratch (no initialization needed)
+hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s);
 
 }  // namespace fq

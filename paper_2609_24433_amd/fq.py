@@ -144,8 +144,8 @@ def linear_workspace_bytes(M: int, N: int, K: int, bits: int) -> int:
 
 
 def workspace(nbytes: int, device) -> torch.Tensor:
-    """A zero-filled workspace (the split-K counters must start at zero)."""
-    return torch.zeros((max(nbytes, 256),), dtype=torch.uint8, device=device)
+    """Scratch for the GEMM / fused-linear entry points (no initialization needed)."""
+    return torch.empty((max(nbytes, 256),), dtype=torch.uint8, device=device)
 
 
 def gemm(a_codes: torch.Tensor, delta: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor,
