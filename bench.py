@@ -5,12 +5,13 @@ denoising step; q/k/v/o 1024->1024 with k/v 1024->256, gate/up 1024->4096, down
 4096->1024; all W4A4 with Hadamard block 128; 10 denoising steps with fresh seeded
 activations and shared weights).  One step = one denoising step of the whole hot path
 as Alg. 1 runs it at runtime: each of the 4 activation sites is transformed and
-quantized once (fq_fwht_quant) and each of the 7 consumers runs its integer GEMM with
-the rescale epilogue (fq_gemm_w4a4).  Weights are folded, rounded and packed on the
+quantized once and its consumers (q|k|v, o, gate|up, down) run their integer GEMMs
+with the rescale epilogue -- one fused projection (fq_linear) per site, the consumers of
+a site packed as one weight matrix.  Weights are folded, rounded and packed on the
 device before timing; inputs are resident in HBM when the timed region starts.
 
-Each step is captured once per denoising step into a HIP graph (11 kernels) and the
-timed region replays K of them.  Prints ONE JSON line.
+Each denoising step is captured into a HIP graph and the timed region replays K of
+them.  Prints ONE JSON line.
 
   python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points]
 """
@@ -67,8 +68,11 @@ def linear_bytes(M, N, K, bits, bias=False):
 # --------------------------------------------------------------------------- workload
 
 class ExpertStep:
-    """Device state of the action-expert layer: packed weights, 10 steps of activations,
-    code/scale/output buffers and split-K workspaces."""
+    """Device state of the action-expert layer.  Consumers of one activation site share
+    that site's transform and quantization (Alg. 1 runtime; Sec. III-B shared sites), so
+    their folded weights are packed as one matrix (q|k|v, gate|up): per-output-channel
+    scales make this exactly the same as separate consumers.  One fused projection
+    (fq_linear) runs per site."""
 
     def __init__(self, torch, fq, synth, dev, n_steps=10):
         self.torch, self.fq = torch, fq
@@ -76,85 +80,93 @@ class ExpertStep:
         wl = self.wl
         self.b = wl.b
         self.sites = wl.sites()
+        self.site_projs = {s: [p for p in wl.projections if p.site == s] for s in self.sites}
+        self.site_N = {s: sum(p.N for p in ps) for s, ps in self.site_projs.items()}
+        self.w_host = {s: np.concatenate([wl.projection_weight(p) for p in ps], axis=0)
+                       for s, ps in self.site_projs.items()}
         self.lin = {}
-        for p in wl.projections:
-            w = torch.from_numpy(wl.projection_weight(p)).to(dev)
-            self.lin[p.name] = fq.QuantLinear(w, wl.b, p.bits)
+        for s in self.sites:
+            w = torch.from_numpy(self.w_host[s]).to(dev)
+            self.lin[s] = fq.QuantLinear(w, wl.b, 4)
             del w
         self.x = {s: [wl.site_activation(s, t).to(dev) for t in range(n_steps)] for s in self.sites}
         M = wl.M
-        self.codes = {s: torch.empty((M, K // 2), dtype=torch.uint8, device=dev) for s, K in self.sites.items()}
-        self.delta = {s: torch.empty((M,), dtype=torch.float32, device=dev) for s in self.sites}
-        self.y = {p.name: torch.empty((M, p.N), dtype=torch.bfloat16, device=dev) for p in wl.projections}
-        self.ws = {p.name: fq.workspace(fq.gemm_workspace_bytes(M, p.N, p.K, p.bits), dev)
-                   for p in wl.projections}
+        self.y = {s: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for s, N in self.site_N.items()}
+        self.ws = {s: fq.workspace(fq.linear_workspace_bytes(M, self.site_N[s], K, 4), dev)
+                   for s, K in self.sites.items()}
         self.n_steps = n_steps
 
-    def run(self, t, events=None):
-        """Enqueue one denoising step.  events: optional dict name -> list of (start, end)."""
-        fq, wl = self.fq, self.wl
-        for s, K in self.sites.items():
-            if events is not None:
-                e0 = self.torch.cuda.Event(enable_timing=True)
-                e0.record()
-            fq.fwht_quant(self.x[s][t], self.b, 4, out_codes=self.codes[s], out_delta=self.delta[s])
-            if events is not None:
-                e1 = self.torch.cuda.Event(enable_timing=True)
-                e1.record()
-                events.setdefault(f"fwht_quant_{s}", []).append((e0, e1))
-            for p in wl.projections:
-                if p.site != s:
-                    continue
-                L = self.lin[p.name]
-                if events is not None:
-                    e0 = self.torch.cuda.Event(enable_timing=True)
-                    e0.record()
-                fq.gemm(self.codes[s], self.delta[s], L.w_packed, L.w_scale, p.N, p.K, p.bits,
-                        ws=self.ws[p.name], out=self.y[p.name])
-                if events is not None:
-                    e1 = self.torch.cuda.Event(enable_timing=True)
-                    e1.record()
-                    events.setdefault(f"gemm_{p.name}", []).append((e0, e1))
+    def run_site(self, s, t):
+        self.lin[s](self.x[s][t], ws=self.ws[s], out=self.y[s])
+
+    def run(self, t):
+        """Enqueue one denoising step: the 4 sites in order."""
+        for s in self.sites:
+            self.run_site(s, t)
 
 
 def check_step(st, oracle, torch):
-    """One projection of step 0 against the oracle (bf16 within 1e-2 of the row absmax)."""
-    wl = st.wl
-    p = next(q for q in wl.projections if q.name == "down")
+    """Every site of step 0 against the oracle (bf16 within 1e-2 of the row absmax)."""
     st.run(0)
     torch.cuda.synchronize()
-    wc, s_w = oracle.quantize_weights(wl.projection_weight(p), wl.b, p.bits)
-    _, _, _, y_ref = oracle.linear(st.x[p.site][0].cpu(), wc, s_w, wl.b, p.bits)
-    yg = st.y[p.name].float().cpu().numpy().astype(np.float64)
-    tol = 1e-2 * np.abs(y_ref).max(axis=1, keepdims=True)
-    ok = bool(np.all(np.abs(yg - y_ref) <= tol))
-    if not ok:
-        raise SystemExit("bench parity check failed: GPU output differs from the oracle")
+    for s in st.sites:
+        wc, s_w = oracle.quantize_weights(st.w_host[s], st.b, 4)
+        _, _, _, y_ref = oracle.linear(st.x[s][0].cpu(), wc, s_w, st.b, 4)
+        yg = st.y[s].float().cpu().numpy().astype(np.float64)
+        tol = 1e-2 * np.abs(y_ref).max(axis=1, keepdims=True)
+        if not np.all(np.abs(yg - y_ref) <= tol):
+            raise SystemExit(f"bench parity check failed at site {s}: GPU output differs from the oracle")
 
 
 def cpu_baseline(st, oracle, torch, budget_s=15.0):
-    """The oracle on the host cores: whole denoising steps (4 site prologues + 7 consumers)
-    until about budget_s seconds are spent."""
-    wl = st.wl
-    wq = {p.name: oracle.quantize_weights(wl.projection_weight(p), wl.b, p.bits) for p in wl.projections}
+    """The oracle on the host cores: whole denoising steps (4 site prologues + the 7
+    consumers' contractions and rescales) until about budget_s seconds are spent."""
+    wq = {s: oracle.quantize_weights(st.w_host[s], st.b, 4) for s in st.sites}
     xs = {s: [a.cpu() for a in st.x[s]] for s in st.sites}
     steps, t0 = 0, time.perf_counter()
     while True:
         t = steps % st.n_steps
         for s in st.sites:
-            codes, delta = oracle.fwht_quant(xs[s][t], wl.b, 4)
-            for p in wl.projections:
-                if p.site == s:
-                    wc, s_w = wq[p.name]
-                    oracle.dequant(oracle.gemm(codes, wc), delta, s_w)
+            codes, delta = oracle.fwht_quant(xs[s][t], st.b, 4)
+            wc, s_w = wq[s]
+            oracle.dequant(oracle.gemm(codes, wc), delta, s_w)
         steps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or steps >= 10 * st.n_steps:
             break
-    ops = wl.ops_per_step() * steps
+    ops = st.wl.ops_per_step() * steps
     return {"value": ops / el / 1e12, "unit": "TOPS", "cores": oracle.max_threads(), "kind": "oracle",
             "sample": f"{steps} denoising steps of the action-expert layer (M=50, 7 projections), "
                       f"{el:.1f} s"}
+
+
+def graph_of(torch, fn, reps):
+    """Capture `reps` back-to-back calls of fn(i) into one HIP graph."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        fn(0)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            for i in range(reps):
+                fn(i)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    return g
+
+
+def time_graph(torch, g, replays):
+    """Average seconds per replay of g, HIP events on the replay stream."""
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(replays):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1e3 / replays
 
 
 def time_graph_steps(torch, graphs, K, W):
@@ -195,48 +207,27 @@ def measure_points(torch, fq, synth, dev, log_fn):
             ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
             call = lambda i: fq.gemm(codes, delta, wp[i % copies], lin.w_scale, N, K, bits, ws=ws, out=y)
             nbytes = gemm_bytes(M, N, K, bits)
-        for i in range(3):
-            call(i)
-        torch.cuda.synchronize()
-        reps = copies
-        g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            with torch.cuda.graph(g, stream=s):
-                for i in range(reps):
-                    call(i)
-        torch.cuda.current_stream().wait_stream(s)
-        g.replay()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        n_rep = max(1, 200 // reps)
-        e0.record()
-        for _ in range(n_rep):
-            g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / (n_rep * reps)
+        g = graph_of(torch, call, copies)
+        us = time_graph(torch, g, max(1, 200 // copies)) / copies * 1e6
         ops = 2.0 * M * N * K
-        tops = ops / us / 1e6
-        gbs = nbytes / us / 1e3
-        t_roof = max(nbytes / HBM_PEAK_GBS / 1e3, ops / INT8_PEAK_TOPS / 1e6)
-        bound = "hbm" if nbytes / HBM_PEAK_GBS / 1e3 >= ops / INT8_PEAK_TOPS / 1e6 else "mfma"
+        t_hbm = nbytes / HBM_PEAK_GBS / 1e3
+        t_mfma = ops / INT8_PEAK_TOPS / 1e6
         rec = {"name": name, "kind": kind, "M": M, "K": K, "N": N, "b": b, "bits": bits,
-               "us": round(us, 3), "TOPS": round(tops, 2), "GBps": round(gbs, 1), "bound": bound,
-               "roofline_frac": round(t_roof / us, 4)}
+               "us": round(us, 3), "TOPS": round(ops / us / 1e6, 2), "GBps": round(nbytes / us / 1e3, 1),
+               "bound": "hbm" if t_hbm >= t_mfma else "mfma",
+               "roofline_frac": round(max(t_hbm, t_mfma) / us, 4)}
         log_fn(json.dumps(rec))
         out.append(rec)
-        del wp, lin, ws
+        del wp, lin, ws, g
         torch.cuda.empty_cache()
 
     run_point("down_w4a4_m50_linear", 50, 16384, 2048, 128, 4, "linear")
     run_point("down_w4a4_m50_gemm", 50, 16384, 2048, 128, 4, "gemm")
     run_point("down_w8a8_m50_linear", 50, 16384, 2048, 128, 8, "linear")
-    run_point("gate_w4a4_m816_gemm", 816, 2048, 16384, 128, 4, "gemm")
-    run_point("down_w4a4_m816_gemm", 816, 16384, 2048, 128, 4, "gemm")
+    run_point("gate_w4a4_m816_linear", 816, 2048, 16384, 128, 4, "linear")
     run_point("down_w4a4_m816_linear", 816, 16384, 2048, 128, 4, "linear")
-    run_point("down_w8a8_m816_gemm", 816, 16384, 2048, 128, 8, "gemm")
+    run_point("down_w4a4_m816_gemm", 816, 16384, 2048, 128, 4, "gemm")
+    run_point("down_w8a8_m816_linear", 816, 16384, 2048, 128, 8, "linear")
     run_point("down_w4a4_m4096_gemm", 4096, 16384, 2048, 128, 4, "gemm")
     return out
 
@@ -261,43 +252,25 @@ def main():
     log(args, "parity check ok")
 
     # one graph per denoising step
-    graphs = []
-    s = torch.cuda.Stream()
-    s.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(s):
-        for t in range(st.n_steps):
-            st.run(t)
-        torch.cuda.synchronize()
-        for t in range(st.n_steps):
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=s):
-                st.run(t)
-            graphs.append(g)
-    torch.cuda.current_stream().wait_stream(s)
-    torch.cuda.synchronize()
-
+    graphs = [graph_of(torch, lambda i, t=t: st.run(t), 1) for t in range(st.n_steps)]
     elapsed = time_graph_steps(torch, graphs, K_steps, W)
     ops_step = st.wl.ops_per_step()
     value = ops_step * K_steps / elapsed / 1e12
     ms_step = elapsed * 1e3 / K_steps
     log(args, f"graph replay: {ms_step * 1e3:.2f} us/step, {value:.3f} TOPS")
 
-    # per-kernel durations: the same steps launched eagerly with events around every call
-    events = {}
-    n_ev = min(K_steps, 50)
-    for i in range(n_ev):
-        st.run(i % st.n_steps, events)
-    torch.cuda.synchronize()
-    per_kernel = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) * 1e3 for k, v in events.items()}
+    # per-site fused projection duration: a graph of 50 back-to-back calls per site
+    # (weights resident, as across the denoising steps), HIP events around the replays
     M = st.wl.M
-    kbytes = {}
-    for p in st.wl.projections:
-        kbytes[f"gemm_{p.name}"] = gemm_bytes(M, p.N, p.K, p.bits)
+    per_site = {}
     for s_, K in st.sites.items():
-        kbytes[f"fwht_quant_{s_}"] = quant_bytes(M, K, 4)
-    dom = max(per_kernel, key=lambda k: per_kernel[k])
-    ach = kbytes[dom] / per_kernel[dom] / 1e3  # GB/s
-    log(args, "per-kernel us: " + ", ".join(f"{k}={v:.2f}" for k, v in sorted(per_kernel.items())))
+        g = graph_of(torch, lambda i, s_=s_: st.run_site(s_, i % st.n_steps), 50)
+        per_site[s_] = time_graph(torch, g, 4) / 50 * 1e6
+    dom = max(per_site, key=lambda k: per_site[k])
+    Kd, Nd = st.sites[dom], st.site_N[dom]
+    dom_bytes = linear_bytes(M, Nd, Kd, 4)
+    ach = dom_bytes / per_site[dom] / 1e3  # GB/s
+    log(args, "per-site fused projection us: " + ", ".join(f"{k}={v:.2f}" for k, v in per_site.items()))
 
     rec = {
         "metric": "W4A4 fused-linear TOPS and us/projection at M=50 and M=816; % of roofline",
@@ -306,12 +279,16 @@ def main():
         "vs_baseline": None, "dtype": "int4 (int8 MFMA, int32 acc) / fp32 prologue / bf16 io",
         "data": "synthetic (seeded N(0,1) tokens with 0.5% outlier channels x50; N(0,0.02) weights)",
         "config": {"workload": "action-expert layer, width 1024, M=50 tokens per denoising step, "
-                               "q/k/v/o/gate/up/down W4A4, block 128, 10 steps of fresh activations",
-                   "M": M, "b": st.wl.b, "projections": 7, "sites": 4, "kernels_per_step": 11,
-                   "us_per_projection": round(ms_step * 1e3 / 7, 3)},
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                               "q/k/v/o/gate/up/down W4A4, block 128, 10 steps of fresh activations; "
+                               "one fused projection per activation site (q|k|v and gate|up grouped)",
+                   "M": M, "b": st.wl.b, "projections": 7, "sites": 4,
+                   "us_per_projection": round(ms_step * 1e3 / 7, 3),
+                   "us_per_site": {k: round(v, 3) for k, v in per_site.items()}},
+        "roofline": {"bound": "hbm", "kernel": f"fq_linear site {dom} (prologue + GEMM), "
+                                               f"M={M} K={Kd} N={Nd}",
+                     "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel_us": round(per_kernel[dom], 3), "algorithmic_bytes": kbytes[dom]},
+                     "kernel_us": round(per_site[dom], 3), "algorithmic_bytes": dom_bytes},
     }
     if not args.no_points:
         rec["points"] = measure_points(torch, fq, synth, dev, lambda m: log(args, m))

@@ -325,26 +325,59 @@ __global__ __launch_bounds__(256) void splitk_epilogue_kernel(GemmParams p, int 
   *reinterpret_cast<uint4 *>(p.y + (int64_t)m * p.ldy + n) = make_uint4(o[0], o[1], o[2], o[3]);
 }
 
+// 16 bytes per lane from global memory straight into LDS; a wave fills the contiguous
+// KB at `lds_dst` (lane l -> lds_dst + 16 l).  The builtin exists only for the device
+// pass, so the host pass (which only needs the kernel stub) sees an empty body.
+__device__ __forceinline__ void load_to_lds16(const void *src, void *lds_dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
+#else
+  (void)src;
+  (void)lds_dst;
+#endif
+}
+
+// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // ---------------- streaming kernel (M <= 64) ----------------
 //
 // Workgroup = 4 x WK waves: 64 output channels (one 16-channel tile per wave column) x a
 // K slice of WK * KT k steps; wave group kg takes KT consecutive steps of the slice.
-// Every wave first issues the loads of all KT of its weight tiles (they stay in flight
-// while the activation slice is staged), the activation slice (rows < M) goes to LDS in
-// one batch, and the MFMA loop then runs out of registers and LDS.  The WK groups add
-// up through LDS; the 64-channel tile leaves through the LDS output stage.
+// Every wave first issues the loads of all KT of its weight tiles into registers; the
+// activation slice (MT * 16 rows) then goes to LDS with direct-to-LDS loads, all in
+// flight at once.  The slice's 16-byte chunks are XOR-swizzled inside each row so that
+// the 16 rows a wave reads at once hit distinct banks without padding (a direct-to-LDS
+// wave instruction fills one contiguous KB).  The MFMA loop double-buffers its
+// activation operands in registers, one k step ahead.  The WK groups add up through
+// LDS and the 64-channel tile leaves through the LDS output stage.
+
+template <int AROW>
+__device__ __forceinline__ int slice_swizzle(int row) {
+  // chunks per row; rows per 256 bytes of LDS when a row is shorter than that
+  constexpr int CPR = AROW / 16;
+  constexpr int RP = AROW >= 256 ? 1 : 256 / AROW;
+  constexpr int MASK = CPR < 16 ? CPR - 1 : 15;
+  return (row / RP) & MASK;
+}
 
 template <int BITS, int AFMT, int MT, int KT, int WK>
 __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
   using F = Fmt<BITS, AFMT>;
   constexpr int NTHREADS = 256 * WK;
+  constexpr int NWAVES = 4 * WK;
   constexpr int LU4 = F::lb / 16;           // 16-byte loads per lane per weight tile
   constexpr int AROW = WK * KT * F::arow;   // activation bytes per row in the slice
-  constexpr int AROWP = AROW + 16;          // padded LDS row stride
   constexpr int ROWS = MT * 16;
   constexpr int CPR = AROW / 16;            // 16-byte chunks per row
-  constexpr int ACH = ROWS * CPR;
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  constexpr int SLICE_KB = ROWS * AROW / 1024;
+  constexpr int IA = (SLICE_KB + NWAVES - 1) / NWAVES;  // direct-to-LDS loads per wave
+  static_assert(ROWS * AROW % 1024 == 0, "slice must be whole KB");
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -370,32 +403,58 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
       wreg[kt][u] = (kt < nk) ? reinterpret_cast<const uint4 *>(wbase + (int64_t)kt * F::tb)[u]
                               : make_uint4(0, 0, 0, 0);
 
+  // 2. activation slice -> LDS, direct loads, swizzled chunks.  Rows past M read row M-1
+  // and chunks past the end of K read chunk 0: both only reach results that are dropped.
+  const uint8_t *abase = p.a + (int64_t)slice_begin * F::arow;
+  const int valid_cols = min(WK * KT, ktot - slice_begin) * (F::arow / 16);
+#pragma unroll
+  for (int i = 0; i < IA; ++i) {
+    const int kb = wave * IA + i;  // KB of the slice this instruction fills
+    if (kb < SLICE_KB) {
+      const int slot = kb * 64 + lane;
+      const int row = slot / CPR, pos = slot % CPR;
+      int col = pos ^ slice_swizzle<AROW>(row);
+      if (col >= valid_cols) col = 0;
+      const int grow = min(row, p.M - 1);
+      load_to_lds16(abase + (int64_t)grow * p.lda + col * 16, lds + kb * 1024);
+    }
+  }
+
   float dt[MT][4];
   EpiParams ep[1];
   if (nsplit == 1) load_epi<MT, 1>(p, 0, ntile * 16, lane, dt, ep);
 
-  // 2. activation slice -> LDS (rows >= M are not loaded: they only feed rows >= M)
-  const uint8_t *abase = p.a + (int64_t)slice_begin * F::arow;
-  const int valid_cols = min(WK * KT, ktot - slice_begin) * (F::arow / 16);
-#pragma unroll
-  for (int i = 0; i < (ACH + NTHREADS - 1) / NTHREADS; ++i) {
-    const int q = i * NTHREADS + tid;
-    if (q < ACH) {
-      const int row = q / CPR, col = q % CPR;
-      if (row < p.M && col < valid_cols)
-        *reinterpret_cast<uint4 *>(lds + row * AROWP + col * 16) =
-            *reinterpret_cast<const uint4 *>(abase + (int64_t)row * p.lda + col * 16);
-    }
-  }
-  __syncthreads();
+  wait_vmcnt<0>();
+  lds_barrier();
 
-  // 3. MFMA over the wave's k steps
+  // 3. MFMA over the wave's k steps, activation operands one step ahead in registers
   v4i acc[MT][1];
 #pragma unroll
   for (int i = 0; i < MT; ++i) acc[i][0] = v4i{0, 0, 0, 0};
-  const uint8_t *arow = lds + (lane & 15) * AROWP + kg * KT * F::arow;
+  const int r16 = lane & 15, g = lane >> 4;
+  auto load_a = [&](int kt, v4i (&dst)[MT][2]) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int row = i * 16 + r16;
+      const uint8_t *rp = lds + row * AROW;
+      const int swz = slice_swizzle<AROW>(row);
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        if constexpr (AFMT == kANibble) {
+          const int chunk = (kg * KT + kt) * 4 + g;  // 64-byte rows per step: 4 chunks
+          dst[i][c] = widen8(*reinterpret_cast<const v2i *>(rp + ((chunk ^ swz) * 16) + c * 8));
+        } else {
+          const int chunk = (kg * KT + kt) * 8 + 2 * g + c;
+          dst[i][c] = *reinterpret_cast<const v4i *>(rp + ((chunk ^ swz) * 16));
+        }
+      }
+    }
+  };
+  v4i abuf[2][MT][2];
+  load_a(0, abuf[0]);
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
+    if (kt + 1 < KT) load_a(kt + 1, abuf[(kt + 1) & 1]);
     if (kt < nk) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
@@ -410,15 +469,7 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
           bop = v4i{(int)t.x, (int)t.y, (int)t.z, (int)t.w};
         }
 #pragma unroll
-        for (int i = 0; i < MT; ++i) {
-          const uint8_t *q = arow + i * 16 * AROWP + kt * F::arow;
-          v4i aop;
-          if constexpr (AFMT == kANibble)
-            aop = widen8(*reinterpret_cast<const v2i *>(q + (lane >> 4) * 16 + c * 8));
-          else
-            aop = *reinterpret_cast<const v4i *>(q + (lane >> 4) * 32 + c * 16);
-          acc[i][0] = mfma16x16x64(aop, bop, acc[i][0]);
-        }
+        for (int i = 0; i < MT; ++i) acc[i][0] = mfma16x16x64(abuf[kt & 1][i][c], bop, acc[i][0]);
       }
     }
   }
@@ -455,7 +506,7 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
 
 template <int BITS, int AFMT, int MT, int KT, int WK>
 static size_t stream_lds_bytes() {
-  const size_t slice = (size_t)MT * 16 * (WK * KT * Fmt<BITS, AFMT>::arow + 16);
+  const size_t slice = (size_t)MT * 16 * (WK * KT * Fmt<BITS, AFMT>::arow);
   const size_t out = (WK == 2 ? (size_t)4 * MT * 64 * 16 : 0) + (size_t)MT * 16 * (64 * 4 + 16);
   return slice > out ? slice : out;
 }
@@ -469,25 +520,6 @@ static size_t stream_lds_bytes() {
 // multiplied.  Activation rows are XOR-swizzled in 16-byte chunks so the 16 rows a
 // wave reads at once fall into distinct LDS banks; weight tiles keep their
 // lane-contiguous kernel-native layout, which is already conflict-free.
-
-// 16 bytes per lane from global memory straight into LDS; a wave fills the contiguous
-// KB at `lds_dst` (lane l -> lds_dst + 16 l).  The builtin exists only for the device
-// pass, so the host pass (which only needs the kernel stub) sees an empty body.
-__device__ __forceinline__ void load_to_lds16(const void *src, void *lds_dst) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
-#else
-  (void)src;
-  (void)lds_dst;
-#endif
-}
-
-// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
 
 template <int AFMT>
 __device__ __forceinline__ int a_swizzle(int row) {

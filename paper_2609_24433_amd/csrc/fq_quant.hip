@@ -2,14 +2,17 @@
 // per token row, blockwise Sylvester FWHT in fp32, row absmax, symmetric round-to-nearest
 // quantization and packing.  The same kernel rounds offline weight rows (r = 1).
 //
-// Work layout: a row of K channels is split into 16-channel chunks.  A workgroup of 256
-// threads holds RPW = 256 / TPR rows; thread tau of a row owns chunks c*TPR + tau.
-//   pass 1: each thread loads its chunks (coalesced 16-byte loads), applies the optional
-//           per-channel multiplier and the butterfly stages h = 1..8 in registers;
-//   pass 2 (b > 16): the row goes through LDS once; each thread then holds whole
-//           "columns" (channels col + 16*m of one block) and runs stages h = 16..b/2;
-//   the row absmax is reduced across the row's threads, codes are formed in registers,
-//   and (b > 16) returned to natural order through LDS before packing and storing.
+// Work layout: a row of K channels is split into 16-channel chunks.  A workgroup of NT
+// threads (256, or 1024 when there are few rows) holds RPW = NT / TPR rows; thread tau
+// of a row owns chunks c*TPR + tau.
+//   loads: every chunk of the thread is requested up front (coalesced 16-byte loads);
+//   pass 1: the optional per-channel multiplier and the butterfly stages h = 1..8 run in
+//           registers;
+//   pass 2 (b > 16): the row goes through LDS; each thread takes whole "columns"
+//           (channels col + 16*m of one block), runs stages h = 16..b/2 and writes the
+//           results back in place, then reloads its own chunks;
+//   the row absmax is reduced across the row's threads, and each thread quantizes,
+//   packs and stores its chunks in natural channel order.
 // Every stage is the pair update (a, c) -> (a + c, a - c) in fp32 in ascending h, so the
 // result does not depend on where the data lives; no multiply-add is contracted.
 #include "fq_device.hpp"
@@ -33,37 +36,39 @@ struct QuantParams {
   int tpr_log2;
 };
 
+// Raw 16-channel chunk as loaded: bf16 = 2 x 16 bytes, fp32 = 4 x 16 bytes.
 template <typename Tin>
-struct ChunkLoader;
+struct Chunk {
+  static constexpr int U4 = sizeof(Tin) == 2 ? 2 : 4;
+  uint4 u[U4];
+};
 
-template <>
-struct ChunkLoader<uint16_t> {  // bf16 bit patterns
-  static __device__ __forceinline__ void load(const void *base, int64_t off, float (&v)[16]) {
-    const uint4 *p = reinterpret_cast<const uint4 *>(reinterpret_cast<const uint16_t *>(base) + off);
-    uint4 a = p[0], b = p[1];
-    uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+template <typename Tin>
+__device__ __forceinline__ void load_chunk(const void *base, int64_t off, Chunk<Tin> &c) {
+  const uint4 *p = reinterpret_cast<const uint4 *>(reinterpret_cast<const Tin *>(base) + off);
+#pragma unroll
+  for (int i = 0; i < Chunk<Tin>::U4; ++i) c.u[i] = p[i];
+}
+
+template <typename Tin>
+__device__ __forceinline__ void unpack_chunk(const Chunk<Tin> &c, float (&v)[16]) {
+  if constexpr (sizeof(Tin) == 2) {
+    const uint32_t w[8] = {c.u[0].x, c.u[0].y, c.u[0].z, c.u[0].w, c.u[1].x, c.u[1].y, c.u[1].z, c.u[1].w};
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       v[2 * i] = bf16_lo(w[i]);
       v[2 * i + 1] = bf16_hi(w[i]);
     }
-  }
-};
-
-template <>
-struct ChunkLoader<float> {
-  static __device__ __forceinline__ void load(const void *base, int64_t off, float (&v)[16]) {
-    const float4 *p = reinterpret_cast<const float4 *>(reinterpret_cast<const float *>(base) + off);
+  } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float4 t = p[i];
-      v[4 * i] = t.x;
-      v[4 * i + 1] = t.y;
-      v[4 * i + 2] = t.z;
-      v[4 * i + 3] = t.w;
+      v[4 * i] = __uint_as_float(c.u[i].x);
+      v[4 * i + 1] = __uint_as_float(c.u[i].y);
+      v[4 * i + 2] = __uint_as_float(c.u[i].z);
+      v[4 * i + 3] = __uint_as_float(c.u[i].w);
     }
   }
-};
+}
 
 // In-place butterfly over n consecutive register values, stages h = 1 .. hmax/2.
 template <int N, int HMAX>
@@ -82,33 +87,42 @@ __device__ __forceinline__ void butterfly(float (&v)[N]) {
   }
 }
 
-__device__ __forceinline__ int quantize1(float u, float inv, float qf) {
-  float t = u * inv;
-  float k = __builtin_rintf(t);  // round half to even
-  k = fminf(fmaxf(k, -qf), qf);
-  return (int)k;
+// code = clamp(rne(u * inv), -q, q), returned as the fp32 bit pattern 0x4B400000 + code,
+// whose low byte is the two's-complement code.  t is first clamped to
+// [-(q + 0.49), q + 0.49]: every t that rounds to a value beyond +-q lands on +-(q + 0.49),
+// which rounds to +-q, and no other t moves, so the clamp after rounding is implied.
+// Adding 1.5 * 2^23 then rounds to the nearest integer, ties to even, exactly as rint
+// does for |t| < 2^22.
+__device__ __forceinline__ int quantize_bits(float u, float inv, float lim) {
+  const float t = __builtin_amdgcn_fmed3f(u * inv, -lim, lim);
+  return __float_as_int(t + 12582912.0f);
 }
 
-// Pack 16 codes (natural channel order) and store them for one chunk.
-__device__ __forceinline__ void store_chunk(uint8_t *row_out, int chunk, const int (&c)[16],
-                                            int out_fmt) {
+// Pack 16 quantized bit patterns (natural channel order; low byte = code) and store them.
+__device__ __forceinline__ void store_chunk_bits(uint8_t *row_out, int chunk, const int (&c)[16],
+                                                 int out_fmt) {
   if (out_fmt == kOutNibble) {
-    uint32_t w0 = 0, w1 = 0;
+    uint32_t w[2];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      uint32_t byte = ((uint32_t)c[2 * i] & 0xFu) | (((uint32_t)c[2 * i + 1] & 0xFu) << 4);
-      if (i < 4)
-        w0 |= byte << (8 * i);
-      else
-        w1 |= byte << (8 * (i - 4));
+    for (int h = 0; h < 2; ++h) {
+      uint32_t b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        b[i] = ((uint32_t)c[8 * h + 2 * i] & 0xFu) | ((uint32_t)c[8 * h + 2 * i + 1] << 4);
+      // low bytes of b[0..3] -> one word
+      const uint32_t lo = __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u);
+      const uint32_t hi = __builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu);
+      w[h] = lo | hi;
     }
-    *reinterpret_cast<uint2 *>(row_out + (int64_t)chunk * 8) = make_uint2(w0, w1);
+    *reinterpret_cast<uint2 *>(row_out + (int64_t)chunk * 8) = make_uint2(w[0], w[1]);
   } else {
     uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      w[i] = ((uint32_t)c[4 * i] & 0xFFu) | (((uint32_t)c[4 * i + 1] & 0xFFu) << 8) |
-             (((uint32_t)c[4 * i + 2] & 0xFFu) << 16) | (((uint32_t)c[4 * i + 3] & 0xFFu) << 24);
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t lo = __builtin_amdgcn_perm((uint32_t)c[4 * i + 1], (uint32_t)c[4 * i], 0x0c0c0400u);
+      const uint32_t hi = __builtin_amdgcn_perm((uint32_t)c[4 * i + 3], (uint32_t)c[4 * i + 2], 0x04000c0cu);
+      w[i] = lo | hi;
+    }
     if (out_fmt == kOutPerm8) {
       // per group of 8 channels: bytes c0 c2 c4 c6 c1 c3 c5 c7 (the order in which the
       // GEMM widens nibble-packed weights)
@@ -125,62 +139,75 @@ __device__ __forceinline__ void store_chunk(uint8_t *row_out, int chunk, const i
   }
 }
 
-template <typename Tin, int LOG2B, int CPT>
-__global__ __launch_bounds__(256) void fwht_quant_kernel(QuantParams p) {
+// NT threads per workgroup; a row is handled by TPR = 2^tpr_log2 consecutive threads,
+// each owning CPT chunks (chunk c * TPR + tau).
+template <typename Tin, int LOG2B, int CPT, int NT>
+__global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   constexpr int B = 1 << LOG2B;
-  constexpr int B1 = B < 16 ? B : 16;           // stages done in pass 1
-  constexpr int MPU = B > 16 ? B / 16 : 1;      // elements per pass-2 unit
+  constexpr int B1 = B < 16 ? B : 16;              // stages done in pass 1
+  constexpr int MPU = B > 16 ? B / 16 : 1;         // elements per pass-2 unit
   constexpr int UPT = B > 16 ? 256 * CPT / B : 1;  // pass-2 units per thread
+  constexpr int NWAVES = NT / kWave;
   extern __shared__ float smem[];
-  __shared__ float red[4];
+  __shared__ float red[NWAVES];
 
   const int tid = threadIdx.x;
   const int TPR = 1 << p.tpr_log2;
-  const int RPW = 256 >> p.tpr_log2;
+  const int RPW = NT >> p.tpr_log2;
   const int row_local = tid >> p.tpr_log2;
   const int tau = tid & (TPR - 1);
   const int64_t row = (int64_t)blockIdx.x * RPW + row_local;
   const bool row_ok = row < p.M;
+  const int64_t row_c = row_ok ? row : p.M - 1;  // loads of rows past M read row M - 1
   const int K = p.K;
   const int nchunks = K >> 4;
   const int q = (1 << (p.bits - 1)) - 1;
   const float qf = (float)q;
 
-  // ---- pass 1: load, optional multiplier, stages h < 16 ------------------------------
-  float v1[CPT][16];
+  // ---- all loads first (branch-free: out-of-range chunks read chunk 0) ----------------
+  Chunk<Tin> raw[CPT];
+  float4 cm[CPT][4];
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
     const int j = c * TPR + tau;
-    if (row_ok && j < nchunks) {
-      ChunkLoader<Tin>::load(p.x, row * p.ldx + (int64_t)j * 16, v1[c]);
-      if (p.chan_mult) {
-        const float4 *m4 = reinterpret_cast<const float4 *>(p.chan_mult + j * 16);
+    const int jc = j < nchunks ? j : 0;
+    load_chunk<Tin>(p.x, row_c * p.ldx + (int64_t)jc * 16, raw[c]);
+    if (p.chan_mult) {
+      const float4 *m4 = reinterpret_cast<const float4 *>(p.chan_mult + jc * 16);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float4 m = m4[i];
-          v1[c][4 * i] = v1[c][4 * i] * m.x;
-          v1[c][4 * i + 1] = v1[c][4 * i + 1] * m.y;
-          v1[c][4 * i + 2] = v1[c][4 * i + 2] * m.z;
-          v1[c][4 * i + 3] = v1[c][4 * i + 3] * m.w;
-        }
-      }
-      butterfly<16, B1>(v1[c]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) v1[c][i] = 0.0f;
+      for (int i = 0; i < 4; ++i) cm[c][i] = m4[i];
     }
   }
 
+  // ---- pass 1: optional multiplier, stages h < 16 in registers -------------------------
+  float v1[CPT][16];
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) {
+    unpack_chunk<Tin>(raw[c], v1[c]);
+    if (p.chan_mult) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v1[c][4 * i] = v1[c][4 * i] * cm[c][i].x;
+        v1[c][4 * i + 1] = v1[c][4 * i + 1] * cm[c][i].y;
+        v1[c][4 * i + 2] = v1[c][4 * i + 2] * cm[c][i].z;
+        v1[c][4 * i + 3] = v1[c][4 * i + 3] * cm[c][i].w;
+      }
+    }
+    butterfly<16, B1>(v1[c]);
+  }
+
   float amax = 0.0f;
-  float v2[UPT][MPU];
-  float *srow = smem + (int64_t)row_local * K;
+  // row buffer: 16 floats of padding after every b-block, so that the 16-lane groups of
+  // a wave, which read different blocks in pass 2, fall into different LDS banks
+  const int KP = B > 16 ? K + 16 * (K / B) : K;
+  float *srow = smem + (int64_t)row_local * KP;
   if constexpr (B > 16) {
-    // ---- pass 2: columns through LDS, stages h = 16 .. b/2 ----------------------------
+    // ---- pass 2: columns through LDS, stages h = 16 .. b/2, results back in place ------
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       const int j = c * TPR + tau;
       if (j < nchunks) {
-        float4 *d = reinterpret_cast<float4 *>(srow + j * 16);
+        float4 *d = reinterpret_cast<float4 *>(srow + j * 16 + 16 * (j * 16 / B));
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           d[i] = make_float4(v1[c][4 * i], v1[c][4 * i + 1], v1[c][4 * i + 2], v1[c][4 * i + 3]);
@@ -192,22 +219,42 @@ __global__ __launch_bounds__(256) void fwht_quant_kernel(QuantParams p) {
     for (int i = 0; i < UPT; ++i) {
       const int u = i * TPR + tau;
       if (u < nunits) {
-        const int base = (u >> 4) * B + (u & 15);
+        const int base = (u >> 4) * (B + 16) + (u & 15);
+        float v2[MPU];
 #pragma unroll
-        for (int m = 0; m < MPU; ++m) v2[i][m] = srow[base + 16 * m];
-        butterfly<MPU, MPU>(v2[i]);
+        for (int m = 0; m < MPU; ++m) v2[m] = srow[base + 16 * m];
+        butterfly<MPU, MPU>(v2);
 #pragma unroll
-        for (int m = 0; m < MPU; ++m) amax = fmaxf(amax, fabsf(v2[i][m]));
-      } else {
+        for (int m = 0; m < MPU; ++m) {
+          amax = fmaxf(amax, fabsf(v2[m]));
+          srow[base + 16 * m] = v2[m];
+        }
+      }
+    }
+    __syncthreads();
 #pragma unroll
-        for (int m = 0; m < MPU; ++m) v2[i][m] = 0.0f;
+    for (int c = 0; c < CPT; ++c) {
+      const int j = c * TPR + tau;
+      const int jc = j < nchunks ? j : 0;
+      const float4 *d = reinterpret_cast<const float4 *>(srow + jc * 16 + 16 * (jc * 16 / B));
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 t = d[i];
+        v1[c][4 * i] = t.x;
+        v1[c][4 * i + 1] = t.y;
+        v1[c][4 * i + 2] = t.z;
+        v1[c][4 * i + 3] = t.w;
       }
     }
   } else {
 #pragma unroll
-    for (int c = 0; c < CPT; ++c)
+    for (int c = 0; c < CPT; ++c) {
+      const int j = c * TPR + tau;
+      if (j < nchunks) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(v1[c][i]));
+        for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(v1[c][i]));
+      }
+    }
   }
 
   // ---- row absmax across the row's threads -------------------------------------------
@@ -228,47 +275,18 @@ __global__ __launch_bounds__(256) void fwht_quant_kernel(QuantParams p) {
   const float inv = zero ? 0.0f : qf / rA;
   if (row_ok && tau == 0) p.delta[row] = zero ? 0.0f : (rA * p.cb) / qf;
 
-  uint8_t *row_out = p.codes + row * p.ld_codes;
-  if constexpr (B > 16) {
-    // codes back to natural order through LDS (as bytes), then pack per chunk
-    __syncthreads();  // every pass-2 read of srow is done
-    int8_t *crow = reinterpret_cast<int8_t *>(smem) + (int64_t)row_local * K;
-    const int nunits = (K / B) * 16;
+  // ---- quantize and pack in natural channel order ------------------------------------
+  if (row_ok) {
+    uint8_t *row_out = p.codes + row * p.ld_codes;
+    const float lim = qf + 0.49f;
 #pragma unroll
-    for (int i = 0; i < UPT; ++i) {
-      const int u = i * TPR + tau;
-      if (u < nunits) {
-        const int base = (u >> 4) * B + (u & 15);
+    for (int c = 0; c < CPT; ++c) {
+      const int j = c * TPR + tau;
+      if (j < nchunks) {
+        int cc[16];
 #pragma unroll
-        for (int m = 0; m < MPU; ++m) crow[base + 16 * m] = (int8_t)(zero ? 0 : quantize1(v2[i][m], inv, qf));
-      }
-    }
-    __syncthreads();
-    if (row_ok) {
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) {
-        const int j = c * TPR + tau;
-        if (j < nchunks) {
-          uint4 raw = *reinterpret_cast<const uint4 *>(crow + j * 16);
-          uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-          int cc[16];
-#pragma unroll
-          for (int i = 0; i < 16; ++i) cc[i] = (int)(int8_t)((w[i >> 2] >> (8 * (i & 3))) & 0xFFu);
-          store_chunk(row_out, j, cc, p.out_fmt);
-        }
-      }
-    }
-  } else {
-    if (row_ok) {
-#pragma unroll
-      for (int c = 0; c < CPT; ++c) {
-        const int j = c * TPR + tau;
-        if (j < nchunks) {
-          int cc[16];
-#pragma unroll
-          for (int i = 0; i < 16; ++i) cc[i] = zero ? 0 : quantize1(v1[c][i], inv, qf);
-          store_chunk(row_out, j, cc, p.out_fmt);
-        }
+        for (int i = 0; i < 16; ++i) cc[i] = quantize_bits(v1[c][i], inv, lim);
+        store_chunk_bits(row_out, j, cc, p.out_fmt);
       }
     }
   }
@@ -276,47 +294,71 @@ __global__ __launch_bounds__(256) void fwht_quant_kernel(QuantParams p) {
 
 // ---------------------------------------------------------------------------------------
 
-static int cpt_for(int K) {
+// Threads per workgroup and chunks per thread: wide workgroups (1024 threads, one chunk
+// per thread) when there are few rows, so a long row is spread over more threads;
+// 256-thread workgroups otherwise.
+struct QuantShape {
+  int nt, cpt, tpr_log2;
+};
+
+static QuantShape quant_shape(int64_t M, int K) {
   const int nchunks = K / 16;
-  int cpt = 1;
-  while (nchunks > 256 * cpt) cpt *= 2;
-  return cpt;
+  QuantShape q;
+  q.nt = (M < 256 && nchunks > 256) ? 1024 : 256;
+  q.cpt = 1;
+  while (nchunks > q.nt * q.cpt) q.cpt *= 2;
+  int tpr = 8;
+  while (tpr < q.nt && tpr * q.cpt < nchunks) tpr *= 2;
+  q.tpr_log2 = 0;
+  while ((1 << q.tpr_log2) < tpr) ++q.tpr_log2;
+  return q;
 }
 
-template <typename Tin, int LOG2B, int CPT>
-static void allow_large_lds(size_t smem) {
-  // more than 64 KB of dynamic LDS (K > 16384 with b > 16) must be requested explicitly
-  if (smem > 65536)
-    (void)hipFuncSetAttribute(reinterpret_cast<const void *>(&fwht_quant_kernel<Tin, LOG2B, CPT>),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-}
-
-template <typename Tin, int LOG2B>
-static hipError_t launch_b(const QuantParams &p, int cpt, size_t smem, int grid, hipStream_t s) {
-  if (cpt == 8) allow_large_lds<Tin, LOG2B, 8>(smem);
-  switch (cpt) {
-    case 1: hipLaunchKernelGGL((fwht_quant_kernel<Tin, LOG2B, 1>), dim3(grid), dim3(256), smem, s, p); break;
-    case 2: hipLaunchKernelGGL((fwht_quant_kernel<Tin, LOG2B, 2>), dim3(grid), dim3(256), smem, s, p); break;
-    case 4: hipLaunchKernelGGL((fwht_quant_kernel<Tin, LOG2B, 4>), dim3(grid), dim3(256), smem, s, p); break;
-    case 8: hipLaunchKernelGGL((fwht_quant_kernel<Tin, LOG2B, 8>), dim3(grid), dim3(256), smem, s, p); break;
-    default: return hipErrorInvalidValue;
+template <typename Tin, int LOG2B, int CPT, int NT>
+static hipError_t launch_one(const QuantParams &p, size_t smem, int grid, hipStream_t s) {
+  static bool attr = false;  // more than 64 KB of dynamic LDS must be requested once
+  if (smem > 65536 && !attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&fwht_quant_kernel<Tin, LOG2B, CPT, NT>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+    attr = true;
   }
+  hipLaunchKernelGGL((fwht_quant_kernel<Tin, LOG2B, CPT, NT>), dim3(grid), dim3(NT), smem, s, p);
   return hipGetLastError();
 }
 
+template <typename Tin, int LOG2B>
+static hipError_t launch_b(const QuantParams &p, const QuantShape &q, size_t smem, int grid,
+                           hipStream_t s) {
+  if (q.nt == 1024) {
+    switch (q.cpt) {
+      case 1: return launch_one<Tin, LOG2B, 1, 1024>(p, smem, grid, s);
+      case 2: return launch_one<Tin, LOG2B, 2, 1024>(p, smem, grid, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
+  switch (q.cpt) {
+    case 1: return launch_one<Tin, LOG2B, 1, 256>(p, smem, grid, s);
+    case 2: return launch_one<Tin, LOG2B, 2, 256>(p, smem, grid, s);
+    case 4: return launch_one<Tin, LOG2B, 4, 256>(p, smem, grid, s);
+    case 8: return launch_one<Tin, LOG2B, 8, 256>(p, smem, grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <typename Tin>
-static hipError_t launch_t(const QuantParams &p, int log2b, int cpt, size_t smem, int grid,
+static hipError_t launch_t(const QuantParams &p, int log2b, const QuantShape &q, size_t smem, int grid,
                            hipStream_t s) {
   switch (log2b) {
-    case 0: return launch_b<Tin, 0>(p, cpt, smem, grid, s);
-    case 1: return launch_b<Tin, 1>(p, cpt, smem, grid, s);
-    case 2: return launch_b<Tin, 2>(p, cpt, smem, grid, s);
-    case 3: return launch_b<Tin, 3>(p, cpt, smem, grid, s);
-    case 4: return launch_b<Tin, 4>(p, cpt, smem, grid, s);
-    case 5: return launch_b<Tin, 5>(p, cpt, smem, grid, s);
-    case 6: return launch_b<Tin, 6>(p, cpt, smem, grid, s);
-    case 7: return launch_b<Tin, 7>(p, cpt, smem, grid, s);
-    case 8: return launch_b<Tin, 8>(p, cpt, smem, grid, s);
+    case 0: return launch_b<Tin, 0>(p, q, smem, grid, s);
+    case 1: return launch_b<Tin, 1>(p, q, smem, grid, s);
+    case 2: return launch_b<Tin, 2>(p, q, smem, grid, s);
+    case 3: return launch_b<Tin, 3>(p, q, smem, grid, s);
+    case 4: return launch_b<Tin, 4>(p, q, smem, grid, s);
+    case 5: return launch_b<Tin, 5>(p, q, smem, grid, s);
+    case 6: return launch_b<Tin, 6>(p, q, smem, grid, s);
+    case 7: return launch_b<Tin, 7>(p, q, smem, grid, s);
+    case 8: return launch_b<Tin, 8>(p, q, smem, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -326,15 +368,11 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
                              uint8_t *codes, int64_t ld_codes, float *delta, int out_fmt,
                              hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  const int cpt = cpt_for(K);
-  int tpr = 8;
-  while (tpr < 256 && tpr * cpt * 16 < K) tpr *= 2;
-  int tpr_log2 = 0;
-  while ((1 << tpr_log2) < tpr) ++tpr_log2;
-  const int rpw = 256 / tpr;
+  const QuantShape q = quant_shape(M, K);
+  const int rpw = q.nt >> q.tpr_log2;
   int log2b = 0;
   while ((1 << log2b) < b) ++log2b;
-  const size_t smem = b > 16 ? (size_t)rpw * K * sizeof(float) : 0;
+  const size_t smem = b > 16 ? (size_t)rpw * (K + 16 * (K / b)) * sizeof(float) : 0;
   const int64_t grid64 = (M + rpw - 1) / rpw;
   if (grid64 > 0x7FFFFFFF) return hipErrorInvalidValue;
   QuantParams p;
@@ -350,16 +388,9 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
   p.ld_codes = ld_codes;
   p.delta = delta;
   p.out_fmt = out_fmt;
-  p.tpr_log2 = tpr_log2;
-  return x_is_f32 ? launch_t<float>(p, log2b, cpt, smem, (int)grid64, s)
-                  : launch_t<uint16_t>(p, log2b, cpt, smem, (int)grid64, s);
-}
-
-size_t fwht_quant_smem_bytes(int K, int b) {
-  const int cpt = cpt_for(K);
-  int tpr = 8;
-  while (tpr < 256 && tpr * cpt * 16 < K) tpr *= 2;
-  return b > 16 ? (size_t)(256 / tpr) * K * sizeof(float) : 0;
+  p.tpr_log2 = q.tpr_log2;
+  return x_is_f32 ? launch_t<float>(p, log2b, q, smem, (int)grid64, s)
+                  : launch_t<uint16_t>(p, log2b, q, smem, (int)grid64, s);
 }
 
 }  // namespace fq
