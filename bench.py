@@ -13,7 +13,7 @@ device before timing; inputs are resident in HBM when the timed region starts.
 Each denoising step is captured into a HIP graph and the timed region replays K of
 them.  Prints ONE JSON line.
 
-  python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points]
+  python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points] [--only-points]
 """
 from __future__ import annotations
 
@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-points", action="store_true")
+    ap.add_argument("--only-points", action="store_true",
+                    help="measure only the graded single projections (profiling aid)")
     ap.add_argument("--quiet", action="store_true")
     return ap.parse_args()
 
@@ -132,7 +134,7 @@ def cpu_baseline(st, oracle, torch, budget_s=15.0):
             oracle.dequant(oracle.gemm(codes, wc), delta, s_w)
         steps += 1
         el = time.perf_counter() - t0
-        if el >= budget_s or steps >= 10 * st.n_steps:
+        if el >= budget_s or steps >= 1000:
             break
     ops = st.wl.ops_per_step() * steps
     return {"value": ops / el / 1e12, "unit": "TOPS", "cores": oracle.max_threads(), "kind": "oracle",
@@ -246,6 +248,9 @@ def main():
     dev = torch.device("cuda:0")
     K_steps, W = args.steps, args.warmup
 
+    if args.only_points:
+        print(json.dumps({"points": measure_points(torch, fq, synth, dev, lambda m: log(args, m))}), flush=True)
+        return
     st = ExpertStep(torch, fq, synth, dev)
     import oracle  # the parity check and the CPU baseline only
     check_step(st, oracle, torch)
