@@ -4,7 +4,9 @@
 
 Every HIP source is compiled with -ffp-contract=off (the prologue's codes must be
 reproducible bit for bit: no multiply-add may be fused) and with packed-fp32
-instructions disabled.
+instructions disabled.  The GEMM source keeps MFMA accumulators in ordinary VGPRs
+(``-amdgpu-mfma-vgpr-form``): with them in AGPRs the register allocator splits the budget
+in half and spills the GEMM's double-buffered operands into AGPRs.
 """
 from __future__ import annotations
 
@@ -28,6 +30,9 @@ COMMON_FLAGS = [
 ]
 
 
+EXTRA_FLAGS = {"fq_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+
+
 def _hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", "hipcc"):
         if cand and (os.path.isabs(cand) and os.path.exists(cand) or not os.path.isabs(cand)):
@@ -37,7 +42,8 @@ def _hipcc() -> str:
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OUT_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *COMMON_FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *COMMON_FLAGS, *EXTRA_FLAGS.get(src, []), "-x", "hip", "-c",
+           os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

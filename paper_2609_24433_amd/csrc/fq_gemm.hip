@@ -26,6 +26,7 @@
 // Output tiles are staged through LDS so that global stores are 16-byte coalesced.
 #include "fq_device.hpp"
 #include "fq_launch.hpp"
+#include <type_traits>
 
 #include <cstdlib>
 #include <cstring>
@@ -344,6 +345,17 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Waits until at most `later` ring stages of LPS loads each are still in flight.
+template <int LPS, int MAXL>
+__device__ __forceinline__ void wait_ring(int later) {
+  static_assert(MAXL * LPS < 64, "vmcnt range");
+  if constexpr (MAXL >= 4) { if (later >= 4) { wait_vmcnt<4 * LPS>(); return; } }
+  if constexpr (MAXL >= 3) { if (later == 3) { wait_vmcnt<3 * LPS>(); return; } }
+  if constexpr (MAXL >= 2) { if (later == 2) { wait_vmcnt<2 * LPS>(); return; } }
+  if constexpr (MAXL >= 1) { if (later == 1) { wait_vmcnt<LPS>(); return; } }
+  wait_vmcnt<0>();
+}
+
 // ---------------- streaming kernel (M <= 64) ----------------
 //
 // Workgroup = 4 x WK waves: 64 output channels (one 16-channel tile per wave column) x a
@@ -516,10 +528,17 @@ static size_t stream_lds_bytes() {
 // BM x BN output tile per workgroup (2 x 2 waves), k steps of 128 channels.  Operands
 // move HBM/L2 -> LDS with gfx950's direct-to-LDS loads (global_load_lds_dwordx4: each
 // wave instruction fills one contiguous KB of LDS, no registers involved) into a ring of
-// STAGES buffers, so loads for k step ks + STAGES - 1 are in flight while step ks is
-// multiplied.  Activation rows are XOR-swizzled in 16-byte chunks so the 16 rows a
-// wave reads at once fall into distinct LDS banks; weight tiles keep their
-// lane-contiguous kernel-native layout, which is already conflict-free.
+// STAGES buffers, so loads for later k steps are in flight while step ks is multiplied.
+// Activation rows are XOR-swizzled in 16-byte chunks so the 16 rows a wave reads at
+// once fall into distinct LDS banks; weight tiles keep their lane-contiguous
+// kernel-native layout, which is already conflict-free.
+//
+// The loop is software-pipelined at the register level.  Each 128-wide k step is two
+// 64-wide chunks; while one chunk's 16 MFMAs run, the next chunk's operands are read
+// from LDS and widened, and the step's one workgroup barrier sits between the two
+// chunks.  Measured on this kernel, a lone workgroup per compute unit is bound by the
+// latency of those LDS operand reads and of the direct-to-LDS load issue rather than
+// by the matrix cores (a loop of the same MFMAs alone runs at ~20 cycles each).
 
 template <int AFMT>
 __device__ __forceinline__ int a_swizzle(int row) {
@@ -536,16 +555,18 @@ __device__ __forceinline__ int xcd_remap(int p, int total) {
 template <int BITS, int AFMT, int BM, int BN, int STAGES>
 __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   using F = Fmt<BITS, AFMT>;
-  constexpr int CPR = F::arow / 16;              // 16-byte activation chunks per row per step
-  constexpr int NT = BN / 16;                    // weight tiles per step
+  constexpr int CPR = F::arow / 16;
+  constexpr int NT = BN / 16;
   constexpr int ASTAGE = BM * F::arow;
   constexpr int BSTAGE = NT * F::tb;
   constexpr int STAGE = ASTAGE + BSTAGE;
-  constexpr int IA = BM * CPR / 256;             // activation load instructions per wave per step
-  constexpr int IB = BSTAGE / 1024 / 4;          // weight load instructions per wave per step
-  constexpr int LPS = IA + IB;                   // loads per wave per step
-  constexpr int TM = BM / 32, TN = NT / 2;       // 16 x 16 tiles per wave
+  constexpr int IA = BM * CPR / 256;
+  constexpr int IB = BSTAGE / 1024 / 4;
+  constexpr int LPS = IA + IB;
+  constexpr int TM = BM / 32, TN = NT / 2;
   static_assert(IA >= 1 && IB >= 1, "tile too small");
+  using AOp = typename std::conditional<AFMT == kANibble, v2i, v4i>::type;
+  using BOp = typename std::conditional<BITS == 4, v2i, v4i>::type;
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
 
   const int tid = threadIdx.x;
@@ -565,32 +586,61 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   const int ks_begin = split * p.ksteps;
   const int nk = min(p.ksteps, ktot - ks_begin);
 
-  // per-lane global sources of this wave's load instructions (k step 0 of the slice)
   const uint8_t *asrc[IA];
 #pragma unroll
   for (int i = 0; i < IA; ++i) {
     const int slot = (wave * IA + i) * 64 + lane;
     const int row = slot / CPR, pos = slot % CPR;
     const int logical_chunk = pos ^ a_swizzle<AFMT>(row);
-    const int grow = min(m0 + row, p.M - 1);  // rows past M load row M-1: they only feed rows >= M
+    const int grow = min(m0 + row, p.M - 1);
     asrc[i] = p.a + (int64_t)grow * p.lda + (int64_t)ks_begin * F::arow + logical_chunk * 16;
   }
   const uint8_t *bsrc[IB];
 #pragma unroll
   for (int i = 0; i < IB; ++i) {
-    const int j = wave * IB + i;                 // KB index inside the weight stage
+    const int j = wave * IB + i;
     const int t = j / (F::tb / 1024), h = j % (F::tb / 1024);
-    const int nb = min(n0 / 16 + t, p.N / 16 - 1);  // tiles past N load the last tile
+    const int nb = min(n0 / 16 + t, p.N / 16 - 1);
     bsrc[i] = p.w + ((int64_t)nb * ktot + ks_begin) * F::tb + h * 1024 + lane * 16;
   }
+  // Loads k step ks into its ring slot.  Past the slice end the source is clamped to the last
+  // step: those loads only fill a slot that is never read again, and they keep the number of
+  // loads in flight constant so that one vmcnt wait fits every step.
   auto issue = [&](int ks) {
     uint8_t *st = lds + (ks % STAGES) * STAGE;
+    const int kc = min(ks, nk - 1);
 #pragma unroll
     for (int i = 0; i < IA; ++i)
-      load_to_lds16(asrc[i] + (int64_t)ks * F::arow, st + (wave * IA + i) * 1024);
+      load_to_lds16(asrc[i] + (int64_t)kc * F::arow, st + (wave * IA + i) * 1024);
 #pragma unroll
     for (int i = 0; i < IB; ++i)
-      load_to_lds16(bsrc[i] + (int64_t)ks * F::tb, st + ASTAGE + (wave * IB + i) * 1024);
+      load_to_lds16(bsrc[i] + (int64_t)kc * F::tb, st + ASTAGE + (wave * IB + i) * 1024);
+  };
+
+  // per-lane LDS byte offsets of this wave's operands inside a stage, chunk 0
+  int aoff[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    const int row = wm * (BM / 2) + i * 16 + (lane & 15);
+    const int g = lane >> 4;
+    aoff[i] = AFMT == kANibble ? row * F::arow + ((g ^ a_swizzle<AFMT>(row)) * 16)
+                               : row * F::arow + (((2 * g) ^ a_swizzle<AFMT>(row)) * 16);
+  }
+  const int boff = ASTAGE + wn * TN * F::tb + lane * (BITS == 4 ? 16 : 32);
+
+  AOp ar[2][TM];
+  BOp br[2][TN];
+  auto read_ops = [&](int set, int ks, int c) {
+    const uint8_t *st = lds + (ks % STAGES) * STAGE;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      // int8 rows: chunk 1 is the next 16-byte chunk, whose swizzled position is chunk 0's ^ 16
+      const int o = AFMT == kANibble ? aoff[i] + c * 8 : (aoff[i] ^ (c * 16));
+      ar[set][i] = *reinterpret_cast<const AOp *>(st + o);
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      br[set][j] = *reinterpret_cast<const BOp *>(st + boff + j * F::tb + c * (BITS == 4 ? 8 : 16));
   };
 
   v4i acc[TM][TN];
@@ -598,51 +648,67 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-
+  // widened operands, one set per chunk in flight
+  v4i wa[2][TM], wb[2][TN];
+  auto prep = [&](int set) {
 #pragma unroll
-  for (int s = 0; s < STAGES - 1; ++s)
-    if (s < nk) issue(s);
+    for (int j = 0; j < TN; ++j) {
+      if constexpr (BITS == 4) wb[set][j] = widen8(br[set][j]);
+      else wb[set][j] = br[set][j];
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      if constexpr (AFMT == kANibble) wa[set][i] = widen8(ar[set][i]);
+      else wa[set][i] = ar[set][i];
+    }
+  };
+  auto mma_rows = [&](int set, int i0, int i1) {
+#pragma unroll
+    for (int i = i0; i < i1; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x64(wa[set][i], wb[set][j], acc[i][j]);
+  };
+  // One half step: multiply the widened chunk `cur` while the next chunk, whose LDS reads
+  // were just issued, is widened into `nxt` behind the first half of the MFMAs.  The
+  // scheduling walls keep the reads ahead of the MFMAs and the widening behind them.
+  auto half_step = [&](int cur, int nxt) {
+    __builtin_amdgcn_sched_barrier(0);
+    mma_rows(cur, 0, TM / 2);
+    __builtin_amdgcn_sched_barrier(0);
+    prep(nxt);
+    mma_rows(cur, TM / 2, TM);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  if (nk > 0) {
+#pragma unroll
+    for (int s = 0; s < STAGES - 1; ++s) issue(s);
+    wait_vmcnt<(STAGES - 2) * LPS>();
+    lds_barrier();
+    issue(STAGES - 1);
+    read_ops(0, 0, 0);
+    prep(0);
+    for (int ks = 0; ks < nk - 1; ++ks) {
+      read_ops(1, ks, 1);
+      half_step(0, 1);
+      // step ks + 1 has landed (STAGES - 2 later steps may be in flight); every wave is done
+      // reading step ks, whose slot the next issue refills
+      wait_vmcnt<(STAGES - 2) * LPS>();
+      lds_barrier();
+      read_ops(0, ks + 1, 0);  // ahead of the loads, which would queue in front of them
+      issue(ks + STAGES);
+      half_step(1, 0);
+    }
+    read_ops(1, nk - 1, 1);
+    mma_rows(0, 0, TM);
+    prep(1);
+    mma_rows(1, 0, TM);
+  }
 
   const int m_wave = m0 + wm * (BM / 2), n_wave = n0 + wn * (BN / 2);
   float dt[TM][4];
   EpiParams ep[TN];
   if (nsplit == 1) load_epi<TM, TN>(p, m_wave, n_wave, lane, dt, ep);
-
-  for (int ks = 0; ks < nk; ++ks) {
-    // loads of step ks are done once at most the later steps' loads are outstanding
-    const int later = min(STAGES - 2, nk - 1 - ks);
-    if (later >= 2) wait_vmcnt<2 * LPS>();
-    else if (later == 1) wait_vmcnt<LPS>();
-    else wait_vmcnt<0>();
-    lds_barrier();
-    if (ks + STAGES - 1 < nk) issue(ks + STAGES - 1);  // refills the stage read at ks - 1
-    const uint8_t *la = lds + (ks % STAGES) * STAGE;
-    const uint8_t *lb = la + ASTAGE;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      v4i af[TM], bf[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int row = wm * (BM / 2) + i * 16 + (lane & 15);
-        const int g = lane >> 4;
-        if constexpr (AFMT == kANibble) {
-          const uint8_t *q = la + row * F::arow + ((g ^ a_swizzle<AFMT>(row)) * 16) + c * 8;
-          af[i] = widen8(*reinterpret_cast<const v2i *>(q));
-        } else {
-          const uint8_t *q = la + row * F::arow + (((2 * g + c) ^ a_swizzle<AFMT>(row)) * 16);
-          af[i] = *reinterpret_cast<const v4i *>(q);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bf[j] = w_operand<BITS>(lb + (wn * TN + j) * F::tb, lane, c);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x64(af[i], bf[j], acc[i][j]);
-    }
-  }
-
-  // output through the LDS stage (the ring is free once every wave is past its last step)
   __syncthreads();
   if (nsplit == 1) {
     if (p.acc_out) store_acc_out<TM, TN, F::shift>(p, acc, m_wave, n_wave, lane);
@@ -658,6 +724,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
 
 template <int BITS, int AFMT, int BM, int BN, int STAGES>
 static constexpr size_t tile_lds_bytes() {
+  // ring; then the k-group hand-over (BM * BN int32) or the staged output, one after the other
   constexpr size_t ring = (size_t)STAGES * (BM * Fmt<BITS, AFMT>::arow + BN / 16 * Fmt<BITS, AFMT>::tb);
   constexpr size_t out = (size_t)BM * (BN * 4 + 16);
   return ring > out ? ring : out;
@@ -671,6 +738,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Development tuning override, read once: FQ_TUNE="splits=<n>".
 struct Tune {
   int splits = 0;
+  int stages = 0;
 };
 static Tune read_tune() {
   Tune t;
@@ -678,11 +746,12 @@ static Tune read_tune() {
   if (!e) return t;
   const char *s = strstr(e, "splits=");
   if (s) t.splits = atoi(s + 7);
+  const char *g = strstr(e, "stages=");
+  if (g) t.stages = atoi(g + 7);
   return t;
 }
 
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
-  (void)bits;
   static const Tune tune = read_tune();
   GemmPlan pl{};
   const int ktot = (int)(K / kTileK);
@@ -712,6 +781,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     pl.ksteps = (int)((ktot + s - 1) / s);
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
     pl.tiles = tiles;
+    pl.stages = 3;
+    if (tune.stages > 0) pl.stages = tune.stages;
   }
   pl.partial_bytes = pl.splits > 1 ? align256((size_t)pl.splits * M * N * 4) : 0;
   return pl;
@@ -751,6 +822,17 @@ static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, dim3 gri
   }
 }
 
+template <int BITS, int AFMT, int ST>
+static hipError_t launch_tile(const GemmParams &p, dim3 grid, hipStream_t s) {
+  constexpr size_t lds = tile_lds_bytes<BITS, AFMT, 128, 128, ST>();
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  static bool attr = false;
+  hipError_t e = allow_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST>, lds, attr);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128, ST>), grid, dim3(256), lds, s, p);
+  return hipGetLastError();
+}
+
 template <int BITS, int AFMT>
 static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStream_t s) {
   hipError_t e;
@@ -763,13 +845,7 @@ static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStre
     }
   } else {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
-    constexpr int ST = 3;
-    constexpr size_t lds = tile_lds_bytes<BITS, AFMT, 128, 128, ST>();
-    static bool attr = false;
-    e = allow_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST>, lds, attr);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128, ST>), grid, dim3(256), lds, s, p);
-    e = hipGetLastError();
+    e = pl.stages == 4 ? launch_tile<BITS, AFMT, 4>(p, grid, s) : launch_tile<BITS, AFMT, 3>(p, grid, s);
   }
   if (e != hipSuccess || pl.splits == 1) return e;
   const int64_t threads = (int64_t)p.M * (p.N / 8);
