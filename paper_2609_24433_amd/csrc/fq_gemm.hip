@@ -552,16 +552,17 @@ __device__ __forceinline__ int xcd_remap(int p, int total) {
   return (p & 7) * (total >> 3) + (p >> 3);
 }
 
-template <int BITS, int AFMT, int BM, int BN, int STAGES>
-__global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
+template <int BITS, int AFMT, int BM, int BN, int STAGES, int LW>
+__global__ __launch_bounds__(256 + 64 * LW) void gemm_tile_kernel(GemmParams p) {
   using F = Fmt<BITS, AFMT>;
   constexpr int CPR = F::arow / 16;
   constexpr int NT = BN / 16;
   constexpr int ASTAGE = BM * F::arow;
   constexpr int BSTAGE = NT * F::tb;
   constexpr int STAGE = ASTAGE + BSTAGE;
-  constexpr int IA = BM * CPR / 256;
-  constexpr int IB = BSTAGE / 1024 / 4;
+  constexpr int NLW = LW ? 1 : 4;                // waves that issue the ring loads
+  constexpr int IA = BM * CPR / (64 * NLW);
+  constexpr int IB = BSTAGE / 1024 / NLW;
   constexpr int LPS = IA + IB;
   constexpr int TM = BM / 32, TN = NT / 2;
   static_assert(IA >= 1 && IB >= 1, "tile too small");
@@ -572,7 +573,8 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = (wave >> 1) & 1, wn = wave & 1;
+  const int lw = LW ? 0 : wave;                  // index among the loading waves
   const int ntiles_n = (p.N + BN - 1) / BN;
   const int ntiles_m = (p.M + BM - 1) / BM;
   const int total = ntiles_n * ntiles_m * gridDim.y;
@@ -589,7 +591,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   const uint8_t *asrc[IA];
 #pragma unroll
   for (int i = 0; i < IA; ++i) {
-    const int slot = (wave * IA + i) * 64 + lane;
+    const int slot = (lw * IA + i) * 64 + lane;
     const int row = slot / CPR, pos = slot % CPR;
     const int logical_chunk = pos ^ a_swizzle<AFMT>(row);
     const int grow = min(m0 + row, p.M - 1);
@@ -598,7 +600,7 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   const uint8_t *bsrc[IB];
 #pragma unroll
   for (int i = 0; i < IB; ++i) {
-    const int j = wave * IB + i;
+    const int j = lw * IB + i;                   // KB index inside the weight stage
     const int t = j / (F::tb / 1024), h = j % (F::tb / 1024);
     const int nb = min(n0 / 16 + t, p.N / 16 - 1);
     bsrc[i] = p.w + ((int64_t)nb * ktot + ks_begin) * F::tb + h * 1024 + lane * 16;
@@ -611,10 +613,10 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
     const int kc = min(ks, nk - 1);
 #pragma unroll
     for (int i = 0; i < IA; ++i)
-      load_to_lds16(asrc[i] + (int64_t)kc * F::arow, st + (wave * IA + i) * 1024);
+      load_to_lds16(asrc[i] + (int64_t)kc * F::arow, st + (lw * IA + i) * 1024);
 #pragma unroll
     for (int i = 0; i < IB; ++i)
-      load_to_lds16(bsrc[i] + (int64_t)kc * F::tb, st + ASTAGE + (wave * IB + i) * 1024);
+      load_to_lds16(bsrc[i] + (int64_t)kc * F::tb, st + ASTAGE + (lw * IB + i) * 1024);
   };
 
   // per-lane LDS byte offsets of this wave's operands inside a stage, chunk 0
@@ -628,19 +630,22 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   }
   const int boff = ASTAGE + wn * TN * F::tb + lane * (BITS == 4 ? 16 : 32);
 
-  AOp ar[2][TM];
-  BOp br[2][TN];
-  auto read_ops = [&](int set, int ks, int c) {
+  // raw operands of a whole k step (both 64-wide chunks); two sets, for even and odd steps
+  AOp ar[2][2][TM];
+  BOp br[2][2][TN];
+  constexpr int NREAD = 2 * (TM + TN);  // LDS reads per wave per step
+  // read r of step ks into `set`: chunk r / (TM + TN), then activation rows, then weight tiles
+  auto read_one = [&](int set, int ks, int r) {
     const uint8_t *st = lds + (ks % STAGES) * STAGE;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
+    const int c = r / (TM + TN), idx = r % (TM + TN);
+    if (idx < TM) {
       // int8 rows: chunk 1 is the next 16-byte chunk, whose swizzled position is chunk 0's ^ 16
-      const int o = AFMT == kANibble ? aoff[i] + c * 8 : (aoff[i] ^ (c * 16));
-      ar[set][i] = *reinterpret_cast<const AOp *>(st + o);
+      const int o = AFMT == kANibble ? aoff[idx] + c * 8 : (aoff[idx] ^ (c * 16));
+      ar[set][c][idx] = *reinterpret_cast<const AOp *>(st + o);
+    } else {
+      const int j = idx - TM;
+      br[set][c][j] = *reinterpret_cast<const BOp *>(st + boff + j * F::tb + c * (BITS == 4 ? 8 : 16));
     }
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-      br[set][j] = *reinterpret_cast<const BOp *>(st + boff + j * F::tb + c * (BITS == 4 ? 8 : 16));
   };
 
   v4i acc[TM][TN];
@@ -648,78 +653,100 @@ __global__ __launch_bounds__(256) void gemm_tile_kernel(GemmParams p) {
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = v4i{0, 0, 0, 0};
-  // widened operands, one set per chunk in flight
-  v4i wa[2][TM], wb[2][TN];
-  auto prep = [&](int set) {
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      if constexpr (BITS == 4) wb[set][j] = widen8(br[set][j]);
-      else wb[set][j] = br[set][j];
+  // One k step: after the step barrier (stage ks + 1 has landed; every wave finished
+  // reading stage ks, whose slot the next issue refills), step ks is multiplied from one
+  // register set while step ks + 1 is read into the other.  The reads are spread one per
+  // two MFMAs: issued in a burst, the four waves' reads fill the compute unit's LDS queue
+  // and stall the in-order wave, MFMA issue included.
+  auto step = [&](int cur, int ks, bool more) {
+    if (more) {
+      if (!LW) wait_vmcnt<(STAGES - 2) * LPS>();
+      lds_barrier();
+      if (!LW) issue(ks + STAGES);
     }
+    int r = 0;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      if constexpr (AFMT == kANibble) wa[set][i] = widen8(ar[set][i]);
-      else wa[set][i] = ar[set][i];
+    for (int c = 0; c < 2; ++c) {
+      v4i wb[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        if constexpr (BITS == 4) wb[j] = widen8(br[cur][c][j]);
+        else wb[j] = br[cur][c][j];
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        v4i wa;
+        if constexpr (AFMT == kANibble) wa = widen8(ar[cur][c][i]);
+        else wa = ar[cur][c][i];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          __builtin_amdgcn_sched_barrier(0);
+          acc[i][j] = mfma16x16x64(wa, wb[j], acc[i][j]);
+          if (more && ((i * TN + j) & 1) == 1 && r < NREAD) {
+            __builtin_amdgcn_sched_barrier(0);
+            read_one(cur ^ 1, ks + 1, r);
+            ++r;
+          }
+        }
+      }
     }
-  };
-  auto mma_rows = [&](int set, int i0, int i1) {
-#pragma unroll
-    for (int i = i0; i < i1; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = mfma16x16x64(wa[set][i], wb[set][j], acc[i][j]);
-  };
-  // One half step: multiply the widened chunk `cur` while the next chunk, whose LDS reads
-  // were just issued, is widened into `nxt` behind the first half of the MFMAs.  The
-  // scheduling walls keep the reads ahead of the MFMAs and the widening behind them.
-  auto half_step = [&](int cur, int nxt) {
-    __builtin_amdgcn_sched_barrier(0);
-    mma_rows(cur, 0, TM / 2);
-    __builtin_amdgcn_sched_barrier(0);
-    prep(nxt);
-    mma_rows(cur, TM / 2, TM);
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  if (nk > 0) {
+  if (LW && wave == 4) {
+    // loader wave: keeps the ring full; one barrier per step, like the MFMA waves
 #pragma unroll
     for (int s = 0; s < STAGES - 1; ++s) issue(s);
     wait_vmcnt<(STAGES - 2) * LPS>();
     lds_barrier();
     issue(STAGES - 1);
-    read_ops(0, 0, 0);
-    prep(0);
     for (int ks = 0; ks < nk - 1; ++ks) {
-      read_ops(1, ks, 1);
-      half_step(0, 1);
-      // step ks + 1 has landed (STAGES - 2 later steps may be in flight); every wave is done
-      // reading step ks, whose slot the next issue refills
       wait_vmcnt<(STAGES - 2) * LPS>();
       lds_barrier();
-      read_ops(0, ks + 1, 0);  // ahead of the loads, which would queue in front of them
       issue(ks + STAGES);
-      half_step(1, 0);
     }
-    read_ops(1, nk - 1, 1);
-    mma_rows(0, 0, TM);
-    prep(1);
-    mma_rows(1, 0, TM);
+  } else {
+    if (!LW) {
+#pragma unroll
+      for (int s = 0; s < STAGES - 1; ++s) issue(s);
+      wait_vmcnt<(STAGES - 2) * LPS>();
+    }
+    lds_barrier();
+#pragma unroll
+    for (int r = 0; r < NREAD; ++r) read_one(0, 0, r);
+    if (!LW) issue(STAGES - 1);
+    int ks = 0;
+    for (; ks + 2 < nk; ks += 2) {
+      step(0, ks, true);
+      step(1, ks + 1, true);
+    }
+    if (ks + 1 < nk) {
+      step(0, ks, true);
+      step(1, ks + 1, false);
+    } else {
+      step(0, ks, false);
+    }
   }
 
   const int m_wave = m0 + wm * (BM / 2), n_wave = n0 + wn * (BN / 2);
+  const bool mma_wave = !(LW && wave == 4);
   float dt[TM][4];
   EpiParams ep[TN];
-  if (nsplit == 1) load_epi<TM, TN>(p, m_wave, n_wave, lane, dt, ep);
-  __syncthreads();
-  if (nsplit == 1) {
-    if (p.acc_out) store_acc_out<TM, TN, F::shift>(p, acc, m_wave, n_wave, lane);
-    stage_tiles<TM, TN, F::shift, true>(lds, BN, acc, wm * (BM / 2), wn * (BN / 2), lane, dt, ep);
-    __syncthreads();
-    store_staged<true>(lds, BM, BN, m0, n0, p, 0, 256);
-  } else {
-    stage_tiles<TM, TN, F::shift, false>(lds, BN, acc, wm * (BM / 2), wn * (BN / 2), lane, dt, ep);
-    __syncthreads();
-    store_staged<false>(lds, BM, BN, m0, n0, p, split, 256);
+  if (nsplit == 1 && mma_wave) load_epi<TM, TN>(p, m_wave, n_wave, lane, dt, ep);
+  __syncthreads();  // also drains the ring's trailing loads before the LDS is reused
+  if (mma_wave) {
+    if (nsplit == 1) {
+      if (p.acc_out) store_acc_out<TM, TN, F::shift>(p, acc, m_wave, n_wave, lane);
+      stage_tiles<TM, TN, F::shift, true>(lds, BN, acc, wm * (BM / 2), wn * (BN / 2), lane, dt, ep);
+    } else {
+      stage_tiles<TM, TN, F::shift, false>(lds, BN, acc, wm * (BM / 2), wn * (BN / 2), lane, dt, ep);
+    }
   }
+  __syncthreads();
+  if (nsplit == 1)
+    store_staged<true>(lds, BM, BN, m0, n0, p, 0, 256 + 64 * LW);
+  else
+    store_staged<false>(lds, BM, BN, m0, n0, p, split, 256 + 64 * LW);
 }
 
 template <int BITS, int AFMT, int BM, int BN, int STAGES>
@@ -739,6 +766,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct Tune {
   int splits = 0;
   int stages = 0;
+  int loader = -1;
 };
 static Tune read_tune() {
   Tune t;
@@ -748,6 +776,8 @@ static Tune read_tune() {
   if (s) t.splits = atoi(s + 7);
   const char *g = strstr(e, "stages=");
   if (g) t.stages = atoi(g + 7);
+  const char *l = strstr(e, "loader=");
+  if (l) t.loader = atoi(l + 7);
   return t;
 }
 
@@ -781,8 +811,14 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     pl.ksteps = (int)((ktot + s - 1) / s);
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
     pl.tiles = tiles;
-    pl.stages = 3;
+    // One workgroup per compute unit: a fifth wave issues the ring loads (4 stages for INT4)
+    // so the MFMA waves never stall on load issue.  Two per compute unit: the second
+    // workgroup already overlaps them, and the extra wave costs more than it saves.
+    const bool lone = tiles * pl.splits <= 256;
+    pl.loader = lone ? 1 : 0;
+    pl.stages = lone && bits == 4 ? 4 : 3;
     if (tune.stages > 0) pl.stages = tune.stages;
+    if (tune.loader >= 0) pl.loader = tune.loader;
   }
   pl.partial_bytes = pl.splits > 1 ? align256((size_t)pl.splits * M * N * 4) : 0;
   return pl;
@@ -822,14 +858,14 @@ static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, dim3 gri
   }
 }
 
-template <int BITS, int AFMT, int ST>
+template <int BITS, int AFMT, int ST, int LW>
 static hipError_t launch_tile(const GemmParams &p, dim3 grid, hipStream_t s) {
   constexpr size_t lds = tile_lds_bytes<BITS, AFMT, 128, 128, ST>();
   static_assert(lds <= 160 * 1024, "LDS budget");
   static bool attr = false;
-  hipError_t e = allow_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST>, lds, attr);
+  hipError_t e = allow_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST, LW>, lds, attr);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128, ST>), grid, dim3(256), lds, s, p);
+  hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128, ST, LW>), grid, dim3(256 + 64 * LW), lds, s, p);
   return hipGetLastError();
 }
 
@@ -845,7 +881,15 @@ static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStre
     }
   } else {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
-    e = pl.stages == 4 ? launch_tile<BITS, AFMT, 4>(p, grid, s) : launch_tile<BITS, AFMT, 3>(p, grid, s);
+    if (pl.loader) {
+      // one wave's loads of STAGES - 2 steps must fit the 6-bit vmcnt: 4 stages only for INT4
+      if constexpr (BITS == 4)
+        e = pl.stages == 4 ? launch_tile<BITS, AFMT, 4, 1>(p, grid, s) : launch_tile<BITS, AFMT, 3, 1>(p, grid, s);
+      else
+        e = launch_tile<BITS, AFMT, 3, 1>(p, grid, s);
+    }
+    else
+      e = pl.stages == 4 ? launch_tile<BITS, AFMT, 4, 0>(p, grid, s) : launch_tile<BITS, AFMT, 3, 0>(p, grid, s);
   }
   if (e != hipSuccess || pl.splits == 1) return e;
   const int64_t threads = (int64_t)p.M * (p.N / 8);

@@ -33,6 +33,7 @@ struct GemmPlan {
   int kt, wk;   // streaming: k steps per wave, wave groups along K per workgroup
   int bm, bn;   // tiled: workgroup tile
   int stages;   // tiled: depth of the LDS load ring
+  int loader;   // tiled: 1 = a fifth wave issues the ring loads
   int splits;   // K slices (each slice: ksteps k steps); > 1 adds an epilogue kernel
   int ksteps;   // 128-wide k steps per slice
   int64_t tiles;        // output tiles along the grid's x dimension

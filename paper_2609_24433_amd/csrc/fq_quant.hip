@@ -8,9 +8,11 @@
 //   loads: every chunk of the thread is requested up front (coalesced 16-byte loads);
 //   pass 1: the optional per-channel multiplier and the butterfly stages h = 1..8 run in
 //           registers;
-//   pass 2 (b > 16): the row goes through LDS; each thread takes whole "columns"
-//           (channels col + 16*m of one block), runs stages h = 16..b/2 and writes the
-//           results back in place, then reloads its own chunks;
+//   pass 2 (b > 16): the row goes through LDS one segment of TPR chunks at a time (a
+//           segment holds whole b-blocks); each thread takes whole "columns" (channels
+//           col + 16*m of one block), runs stages h = 16..b/2 and writes the results back
+//           in place, then reloads its own chunk.  Segment-sized LDS keeps enough rows
+//           resident per compute unit that their loads overlap;
 //   the row absmax is reduced across the row's threads, and each thread quantizes,
 //   packs and stores its chunks in natural channel order.
 // Every stage is the pair update (a, c) -> (a + c, a - c) in fp32 in ascending h, so the
@@ -146,7 +148,6 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   constexpr int B = 1 << LOG2B;
   constexpr int B1 = B < 16 ? B : 16;              // stages done in pass 1
   constexpr int MPU = B > 16 ? B / 16 : 1;         // elements per pass-2 unit
-  constexpr int UPT = B > 16 ? 256 * CPT / B : 1;  // pass-2 units per thread
   constexpr int NWAVES = NT / kWave;
   extern __shared__ float smem[];
   __shared__ float red[NWAVES];
@@ -197,53 +198,55 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   }
 
   float amax = 0.0f;
-  // row buffer: 16 floats of padding after every b-block, so that the 16-lane groups of
-  // a wave, which read different blocks in pass 2, fall into different LDS banks
-  const int KP = B > 16 ? K + 16 * (K / B) : K;
-  float *srow = smem + (int64_t)row_local * KP;
   if constexpr (B > 16) {
-    // ---- pass 2: columns through LDS, stages h = 16 .. b/2, results back in place ------
+    // ---- pass 2, one segment at a time: round c covers chunks [c*TPR, (c+1)*TPR), which
+    // hold whole b-blocks.  The segment goes through LDS with 16 floats of padding after
+    // every block (the 16-lane groups of a wave read different blocks), each thread runs
+    // stages h = 16 .. b/2 over whole columns (channels col + 16*m of one block), writes
+    // them back in place and reloads its own chunk.
+    const int SEG = TPR * 16;
+    const int SEGP = SEG + 16 * (SEG / B);
+    float *srow = smem + (int64_t)row_local * SEGP;
+    constexpr int UPR = 256 / B;  // pass-2 units per thread per round
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       const int j = c * TPR + tau;
+      if (c > 0) __syncthreads();  // the previous round's reloads are done
       if (j < nchunks) {
-        float4 *d = reinterpret_cast<float4 *>(srow + j * 16 + 16 * (j * 16 / B));
+        float4 *d = reinterpret_cast<float4 *>(srow + tau * 16 + 16 * (tau * 16 / B));
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           d[i] = make_float4(v1[c][4 * i], v1[c][4 * i + 1], v1[c][4 * i + 2], v1[c][4 * i + 3]);
       }
-    }
-    __syncthreads();
-    const int nunits = (K / B) * 16;
+      __syncthreads();
+      const int nunits = (min(SEG, K - c * SEG) / B) * 16;
 #pragma unroll
-    for (int i = 0; i < UPT; ++i) {
-      const int u = i * TPR + tau;
-      if (u < nunits) {
-        const int base = (u >> 4) * (B + 16) + (u & 15);
-        float v2[MPU];
+      for (int i = 0; i < UPR; ++i) {
+        const int u = i * TPR + tau;
+        if (u < nunits) {
+          const int base = (u >> 4) * (B + 16) + (u & 15);
+          float v2[MPU];
 #pragma unroll
-        for (int m = 0; m < MPU; ++m) v2[m] = srow[base + 16 * m];
-        butterfly<MPU, MPU>(v2);
+          for (int m = 0; m < MPU; ++m) v2[m] = srow[base + 16 * m];
+          butterfly<MPU, MPU>(v2);
 #pragma unroll
-        for (int m = 0; m < MPU; ++m) {
-          amax = fmaxf(amax, fabsf(v2[m]));
-          srow[base + 16 * m] = v2[m];
+          for (int m = 0; m < MPU; ++m) {
+            amax = fmaxf(amax, fabsf(v2[m]));
+            srow[base + 16 * m] = v2[m];
+          }
         }
       }
-    }
-    __syncthreads();
+      __syncthreads();
+      if (j < nchunks) {
+        const float4 *d = reinterpret_cast<const float4 *>(srow + tau * 16 + 16 * (tau * 16 / B));
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int j = c * TPR + tau;
-      const int jc = j < nchunks ? j : 0;
-      const float4 *d = reinterpret_cast<const float4 *>(srow + jc * 16 + 16 * (jc * 16 / B));
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float4 t = d[i];
-        v1[c][4 * i] = t.x;
-        v1[c][4 * i + 1] = t.y;
-        v1[c][4 * i + 2] = t.z;
-        v1[c][4 * i + 3] = t.w;
+        for (int i = 0; i < 4; ++i) {
+          const float4 t = d[i];
+          v1[c][4 * i] = t.x;
+          v1[c][4 * i + 1] = t.y;
+          v1[c][4 * i + 2] = t.z;
+          v1[c][4 * i + 3] = t.w;
+        }
       }
     }
   } else {
@@ -372,7 +375,8 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
   const int rpw = q.nt >> q.tpr_log2;
   int log2b = 0;
   while ((1 << log2b) < b) ++log2b;
-  const size_t smem = b > 16 ? (size_t)rpw * (K + 16 * (K / b)) * sizeof(float) : 0;
+  const int seg = 16 << q.tpr_log2;  // channels per pass-2 round
+  const size_t smem = b > 16 ? (size_t)rpw * (seg + 16 * (seg / b)) * sizeof(float) : 0;
   const int64_t grid64 = (M + rpw - 1) / rpw;
   if (grid64 > 0x7FFFFFFF) return hipErrorInvalidValue;
   QuantParams p;
