@@ -281,12 +281,17 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, in
   float *delta = reinterpret_cast<float *>(codes + codes_bytes);
   void *gws = codes + codes_bytes + delta_bytes;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int fmt = bits == 4 ? fq::kOutPerm8 : fq::kOutInt8;
+  // W4A4 codes between the two kernels: nibbles for the streaming GEMM (small M: halves its
+  // LDS slice), widened int8 in the GEMM's interleaved order for the tiled one (no
+  // activation widening in its inner loop).
+  const bool nibble = bits == 4 && fq::plan_gemm(M, N, K, bits).kind == 0;
+  const int fmt = bits == 8 ? fq::kOutInt8 : (nibble ? fq::kOutNibble : fq::kOutPerm8);
+  const int64_t lda = nibble ? K / 2 : K;
   hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, M, (int)K, b, bits, clip_ratio,
-                                       inv_sqrt_pow2(b), codes, K, delta, fmt, st);
+                                       inv_sqrt_pow2(b), codes, lda, delta, fmt, st);
   if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
-  return gemm_common(codes, fq::kAInt8, K, delta, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N,
-                     K, bits, gws, ws_bytes - codes_bytes - delta_bytes, st);
+  return gemm_common(codes, nibble ? fq::kANibble : fq::kAInt8, lda, delta, w_packed, w_scale, bias, y_bf16,
+                     ldy, nullptr, M, N, K, bits, gws, ws_bytes - codes_bytes - delta_bytes, st);
 }
 
 }  // extern "C"

@@ -358,8 +358,8 @@ __device__ __forceinline__ void wait_ring(int later) {
 
 // ---------------- streaming kernel (M <= 64) ----------------
 //
-// Workgroup = 4 x WK waves: 64 output channels (one 16-channel tile per wave column) x a
-// K slice of WK * KT k steps; wave group kg takes KT consecutive steps of the slice.
+// Workgroup = 4 x WK waves (WK = 1, 2 or 4): 64 output channels (one 16-channel tile per
+// wave column) x a K slice of WK * KT k steps; wave group kg takes KT consecutive steps.
 // Every wave first issues the loads of all KT of its weight tiles into registers; the
 // activation slice (MT * 16 rows) then goes to LDS with direct-to-LDS loads, all in
 // flight at once.  The slice's 16-byte chunks are XOR-swizzled inside each row so that
@@ -422,7 +422,8 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
 #pragma unroll
   for (int i = 0; i < IA; ++i) {
     const int kb = wave * IA + i;  // KB of the slice this instruction fills
-    if (kb < SLICE_KB) {
+    // a KB holding only rows past M is not loaded: those rows reach no stored output
+    if (kb < SLICE_KB && (kb * 64) / CPR < p.M) {
       const int slot = kb * 64 + lane;
       const int row = slot / CPR, pos = slot % CPR;
       int col = pos ^ slice_swizzle<AROW>(row);
@@ -488,20 +489,22 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
 
   // 4. wave groups add up in LDS, then the 64-channel tile leaves through the LDS stage
   __syncthreads();  // the activation slice is no longer read
-  if constexpr (WK == 2) {
+  if constexpr (WK > 1) {
     v4i *red = reinterpret_cast<v4i *>(lds);
-    if (kg == 1) {
+    if (kg > 0) {
 #pragma unroll
-      for (int i = 0; i < MT; ++i) red[(wn * MT + i) * 64 + lane] = acc[i][0];
+      for (int i = 0; i < MT; ++i) red[(((kg - 1) * 4 + wn) * MT + i) * 64 + lane] = acc[i][0];
     }
     __syncthreads();
     if (kg == 0) {
 #pragma unroll
-      for (int i = 0; i < MT; ++i) acc[i][0] += red[(wn * MT + i) * 64 + lane];
+      for (int g2 = 1; g2 < WK; ++g2)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[i][0] += red[(((g2 - 1) * 4 + wn) * MT + i) * 64 + lane];
     }
     __syncthreads();
   }
-  uint8_t *stage = lds + (WK == 2 ? 4 * MT * 64 * 16 : 0);
+  uint8_t *stage = lds + (size_t)(WK - 1) * 4 * MT * 64 * 16;
   if (kg == 0) {
     if (p.acc_out && nsplit == 1 && n_ok) store_acc_out<MT, 1, F::shift>(p, acc, 0, ntile * 16, lane);
     if (nsplit == 1)
@@ -519,7 +522,7 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
 template <int BITS, int AFMT, int MT, int KT, int WK>
 static size_t stream_lds_bytes() {
   const size_t slice = (size_t)MT * 16 * (WK * KT * Fmt<BITS, AFMT>::arow);
-  const size_t out = (WK == 2 ? (size_t)4 * MT * 64 * 16 : 0) + (size_t)MT * 16 * (64 * 4 + 16);
+  const size_t out = (size_t)(WK - 1) * 4 * MT * 64 * 16 + (size_t)MT * 16 * (64 * 4 + 16);
   return slice > out ? slice : out;
 }
 
@@ -765,6 +768,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Development tuning override, read once: FQ_TUNE="splits=<n>".
 struct Tune {
   int splits = 0;
+  int wk = 0, kt = 0;
   int stages = 0;
   int loader = -1;
 };
@@ -776,6 +780,10 @@ static Tune read_tune() {
   if (s) t.splits = atoi(s + 7);
   const char *g = strstr(e, "stages=");
   if (g) t.stages = atoi(g + 7);
+  const char *w = strstr(e, "wk=");
+  if (w) t.wk = atoi(w + 3);
+  const char *k = strstr(e, "kt=");
+  if (k) t.kt = atoi(k + 3);
   const char *l = strstr(e, "loader=");
   if (l) t.loader = atoi(l + 7);
   return t;
@@ -786,17 +794,30 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
   GemmPlan pl{};
   const int ktot = (int)(K / kTileK);
   if (M <= 64) {
-    // weight streaming: 8 k steps per wave, two wave groups per workgroup once K is long
+    // Weight streaming.  A workgroup stages its activation slice (all M rows, the slice's
+    // k steps) in LDS once for 4 wave columns of 16 channels; two wave groups of kt steps
+    // each split the slice and add up in LDS.  K of 8 or 16 steps is one slice (no split-K
+    // epilogue kernel); longer K is cut into slices of 8 steps (K <= 4096) or 16 steps,
+    // the shapes that measured fastest for M = 50.
     pl.kind = 0;
     pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-    pl.kt = ktot >= 8 ? 8 : (ktot >= 4 ? 4 : (ktot >= 2 ? 2 : 1));
-    pl.wk = ktot >= 16 ? 2 : 1;
+    if (ktot < 4) {
+      pl.wk = 1;
+      pl.kt = ktot >= 2 ? 2 : 1;
+    } else {
+      pl.wk = 2;
+      pl.kt = ktot <= 16 ? ktot / 2 : (ktot <= 32 ? 4 : 8);
+      if (pl.kt > 8) pl.kt = 8;
+      if (pl.kt == 3 || pl.kt == 5 || pl.kt == 6 || pl.kt == 7) pl.kt = pl.kt < 4 ? 2 : 4;
+    }
     if (tune.splits > 0) {
       int per = (ktot + tune.splits - 1) / tune.splits;  // k steps per slice
-      pl.wk = per >= 16 ? 2 : 1;
+      pl.wk = per > 16 && bits == 4 ? 4 : (per > 8 ? 2 : 1);
       int kt = (per + pl.wk - 1) / pl.wk;
       pl.kt = kt >= 8 ? 8 : (kt >= 4 ? 4 : (kt >= 2 ? 2 : 1));
     }
+    if (tune.wk > 0) pl.wk = tune.wk;
+    if (tune.kt > 0) pl.kt = tune.kt;
     pl.ksteps = pl.kt * pl.wk;
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
     pl.tiles = (N + 63) / 64;
@@ -849,7 +870,24 @@ static hipError_t launch_stream(const GemmParams &p, dim3 grid, hipStream_t s) {
 
 template <int BITS, int AFMT, int MT>
 static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, dim3 grid, hipStream_t s) {
-  if (wk == 2) return launch_stream<BITS, AFMT, MT, 8, 2>(p, grid, s);
+  if (wk == 4) {
+    switch (kt) {
+      case 1: return launch_stream<BITS, AFMT, MT, 1, 4>(p, grid, s);
+      case 2: return launch_stream<BITS, AFMT, MT, 2, 4>(p, grid, s);
+      case 4: return launch_stream<BITS, AFMT, MT, 4, 4>(p, grid, s);
+      default:
+        if constexpr (AFMT == kANibble) return launch_stream<BITS, AFMT, MT, 8, 4>(p, grid, s);
+        return hipErrorInvalidValue;  // a 32-step int8 slice does not fit in LDS
+    }
+  }
+  if (wk == 2) {
+    switch (kt) {
+      case 1: return launch_stream<BITS, AFMT, MT, 1, 2>(p, grid, s);
+      case 2: return launch_stream<BITS, AFMT, MT, 2, 2>(p, grid, s);
+      case 4: return launch_stream<BITS, AFMT, MT, 4, 2>(p, grid, s);
+      default: return launch_stream<BITS, AFMT, MT, 8, 2>(p, grid, s);
+    }
+  }
   switch (kt) {
     case 1: return launch_stream<BITS, AFMT, MT, 1, 1>(p, grid, s);
     case 2: return launch_stream<BITS, AFMT, MT, 2, 1>(p, grid, s);
