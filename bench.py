@@ -42,6 +42,10 @@ def parse():
     ap.add_argument("--only-points", action="store_true",
                     help="measure only the graded single projections (profiling aid)")
     ap.add_argument("--quiet", action="store_true")
+    ap.add_argument("--traffic-site", default=None,
+                    help="run only this site's fused projection 100 times (for HBM counter runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run a plain 256 MiB copy-like kernel 20 times (counter calibration)")
     return ap.parse_args()
 
 
@@ -65,6 +69,56 @@ def quant_bytes(M, K, bits):
 def linear_bytes(M, N, K, bits, bias=False):
     """bf16 x + packed W + s_w + bf16 y (+ bias); intermediate codes excluded."""
     return 2 * M * K + N * K * bits // 8 + 4 * N + 2 * M * N + (4 * N if bias else 0)
+
+
+# --------------------------------------------------------------------------- HBM traffic
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "site_traffic.json")
+CSRC = os.path.join(ROOT, "paper_2609_24433_amd", "csrc")
+
+
+def sources_digest():
+    """SHA-256 over the HIP/C++ sources: counter readings are void once the kernels change."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(site):
+    """HBM bytes per fused-projection call of `site` from the committed rocprofv3 counter
+    runs (FETCH_SIZE and WRITE_SIZE, each scaled by the same counter on a copy of known
+    size), or None when there is no reading for these sources and this site."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("sources_sha256") != sources_digest() or t.get("site") != site:
+        return None
+    fetch = t["fetch_kib_per_call"] * 1024 * t["copy_bytes_read"] / (t["copy_fetch_kib"] * 1024)
+    write = t["write_kib_per_call"] * 1024 * t["copy_bytes_written"] / (t["copy_write_kib"] * 1024)
+    return int(round(fetch + write))
+
+
+def traffic_run(torch, fq, synth, dev, site):
+    st = ExpertStep(torch, fq, synth, dev)
+    for i in range(100):
+        st.run_site(site, i % st.n_steps)
+    torch.cuda.synchronize()
+    print(json.dumps({"traffic_site": site, "calls": 100}), flush=True)
+
+
+def copy_calibration(torch, dev):
+    n = 64 << 20  # float32 elements: 256 MiB read and 256 MiB written per launch
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(20):
+        torch.add(a, 0.0, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 20}), flush=True)
 
 
 # --------------------------------------------------------------------------- workload
@@ -248,6 +302,12 @@ def main():
     dev = torch.device("cuda:0")
     K_steps, W = args.steps, args.warmup
 
+    if args.copy_calibration:
+        copy_calibration(torch, dev)
+        return
+    if args.traffic_site:
+        traffic_run(torch, fq, synth, dev, args.traffic_site)
+        return
     if args.only_points:
         print(json.dumps({"points": measure_points(torch, fq, synth, dev, lambda m: log(args, m))}), flush=True)
         return
@@ -292,7 +352,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": f"fq_linear site {dom} (prologue + GEMM), "
                                                f"M={M} K={Kd} N={Nd}",
                      "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom),
                      "kernel_us": round(per_site[dom], 3), "algorithmic_bytes": dom_bytes},
     }
     if not args.no_points:
