@@ -536,12 +536,14 @@ static size_t stream_lds_bytes() {
 // once fall into distinct LDS banks; weight tiles keep their lane-contiguous
 // kernel-native layout, which is already conflict-free.
 //
-// The loop is software-pipelined at the register level.  Each 128-wide k step is two
-// 64-wide chunks; while one chunk's 16 MFMAs run, the next chunk's operands are read
-// from LDS and widened, and the step's one workgroup barrier sits between the two
-// chunks.  Measured on this kernel, a lone workgroup per compute unit is bound by the
-// latency of those LDS operand reads and of the direct-to-LDS load issue rather than
-// by the matrix cores (a loop of the same MFMAs alone runs at ~20 cycles each).
+// The loop is software-pipelined at the register level: after the one barrier per k step,
+// the whole next step's operands are read from LDS into a second register set while the
+// current step's 32 MFMAs run, one read per two MFMAs.  Every read is 16 bytes per lane
+// (an 8-byte nibble operand brings both 64-wide chunks at once): 8-byte reads at a 16-byte
+// lane stride put two lanes on every bank and doubled the LDS time.  With at most one
+// workgroup per compute unit, a fifth wave issues the ring loads.  Measured at M = 816:
+// ~1000-1150 cycles per k step against 512 of MFMA issue; removing the ring loads changes
+// nothing, removing the LDS operand reads leaves ~700, the MFMA + widening loop alone ~660.
 
 template <int AFMT>
 __device__ __forceinline__ int a_swizzle(int row) {
@@ -567,7 +569,7 @@ __global__ __launch_bounds__(256 + 64 * LW) void gemm_tile_kernel(GemmParams p) 
   constexpr int IA = BM * CPR / (64 * NLW);
   constexpr int IB = BSTAGE / 1024 / NLW;
   constexpr int LPS = IA + IB;
-  constexpr int TM = BM / 32, TN = NT / 2;
+  constexpr int TM = BM / 32, TN = NT / 2;       // 2 x 2 waves of 64 x 64
   static_assert(IA >= 1 && IB >= 1, "tile too small");
   using AOp = typename std::conditional<AFMT == kANibble, v2i, v4i>::type;
   using BOp = typename std::conditional<BITS == 4, v2i, v4i>::type;
@@ -633,21 +635,42 @@ __global__ __launch_bounds__(256 + 64 * LW) void gemm_tile_kernel(GemmParams p) 
   }
   const int boff = ASTAGE + wn * TN * F::tb + lane * (BITS == 4 ? 16 : 32);
 
-  // raw operands of a whole k step (both 64-wide chunks); two sets, for even and odd steps
-  AOp ar[2][2][TM];
-  BOp br[2][2][TN];
-  constexpr int NREAD = 2 * (TM + TN);  // LDS reads per wave per step
-  // read r of step ks into `set`: chunk r / (TM + TN), then activation rows, then weight tiles
+  // Raw operands of a whole k step (both 64-wide chunks); two sets, for even and odd steps.
+  // Every LDS read is 16 bytes per lane: a nibble operand brings both chunks' 8-byte halves
+  // at once (lanes 16 bytes apart, conflict-free; 8-byte reads of one half would put two
+  // lanes on every bank), an int8 operand one chunk.
+  constexpr int RA = AFMT == kANibble ? 1 : 2;   // activation reads per row tile per step
+  constexpr int RB = BITS == 4 ? 1 : 2;          // weight reads per column tile per step
+  v4i ar[2][RA][TM];
+  v4i br[2][RB][TN];
+  constexpr int NREAD = RA * TM + RB * TN;       // LDS reads per wave per step
+  // read r of step ks into `set`: activation reads first, then weight reads
   auto read_one = [&](int set, int ks, int r) {
     const uint8_t *st = lds + (ks % STAGES) * STAGE;
-    const int c = r / (TM + TN), idx = r % (TM + TN);
-    if (idx < TM) {
+    if (r < RA * TM) {
+      const int c = r / TM, i = r % TM;
       // int8 rows: chunk 1 is the next 16-byte chunk, whose swizzled position is chunk 0's ^ 16
-      const int o = AFMT == kANibble ? aoff[idx] + c * 8 : (aoff[idx] ^ (c * 16));
-      ar[set][c][idx] = *reinterpret_cast<const AOp *>(st + o);
+      ar[set][c][i] = *reinterpret_cast<const v4i *>(st + (aoff[i] ^ (c * 16)));
     } else {
-      const int j = idx - TM;
-      br[set][c][j] = *reinterpret_cast<const BOp *>(st + boff + j * F::tb + c * (BITS == 4 ? 8 : 16));
+      const int q = r - RA * TM, c = q / TN, j = q % TN;
+      br[set][c][j] = *reinterpret_cast<const v4i *>(st + boff + j * F::tb + c * 16);
+    }
+  };
+  // operands of chunk c from a raw set
+  auto a_op = [&](int set, int c, int i) -> v4i {
+    if constexpr (AFMT == kANibble) {
+      const v4i &t = ar[set][0][i];
+      return widen8(c == 0 ? v2i{t.x, t.y} : v2i{t.z, t.w});
+    } else {
+      return ar[set][c][i];
+    }
+  };
+  auto b_op = [&](int set, int c, int j) -> v4i {
+    if constexpr (BITS == 4) {
+      const v4i &t = br[set][0][j];
+      return widen8(c == 0 ? v2i{t.x, t.y} : v2i{t.z, t.w});
+    } else {
+      return br[set][c][j];
     }
   };
 
@@ -670,22 +693,18 @@ __global__ __launch_bounds__(256 + 64 * LW) void gemm_tile_kernel(GemmParams p) 
     int r = 0;
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
-      v4i wb[TN];
+      v4i wa[TM];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) wa[i] = a_op(cur, c, i);
+      // weight tile outer: one widened weight operand live at a time
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        if constexpr (BITS == 4) wb[j] = widen8(br[cur][c][j]);
-        else wb[j] = br[cur][c][j];
-      }
+        const v4i wb = b_op(cur, c, j);
 #pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        v4i wa;
-        if constexpr (AFMT == kANibble) wa = widen8(ar[cur][c][i]);
-        else wa = ar[cur][c][i];
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
+        for (int i = 0; i < TM; ++i) {
           __builtin_amdgcn_sched_barrier(0);
-          acc[i][j] = mfma16x16x64(wa, wb[j], acc[i][j]);
-          if (more && ((i * TN + j) & 1) == 1 && r < NREAD) {
+          acc[i][j] = mfma16x16x64(wa[i], wb, acc[i][j]);
+          if (more && ((j * TM + i) & 1) == 1 && r < NREAD) {
             __builtin_amdgcn_sched_barrier(0);
             read_one(cur ^ 1, ks + 1, r);
             ++r;
@@ -733,11 +752,12 @@ __global__ __launch_bounds__(256 + 64 * LW) void gemm_tile_kernel(GemmParams p) 
 
   const int m_wave = m0 + wm * (BM / 2), n_wave = n0 + wn * (BN / 2);
   const bool mma_wave = !(LW && wave == 4);
+  const bool out_wave = mma_wave;  // the loader wave holds no results
   float dt[TM][4];
   EpiParams ep[TN];
-  if (nsplit == 1 && mma_wave) load_epi<TM, TN>(p, m_wave, n_wave, lane, dt, ep);
+  if (nsplit == 1 && out_wave) load_epi<TM, TN>(p, m_wave, n_wave, lane, dt, ep);
   __syncthreads();  // also drains the ring's trailing loads before the LDS is reused
-  if (mma_wave) {
+  if (out_wave) {
     if (nsplit == 1) {
       if (p.acc_out) store_acc_out<TM, TN, F::shift>(p, acc, m_wave, n_wave, lane);
       stage_tiles<TM, TN, F::shift, true>(lds, BN, acc, wm * (BM / 2), wn * (BN / 2), lane, dt, ep);
