@@ -358,8 +358,9 @@ __device__ __forceinline__ void wait_ring(int later) {
 
 // ---------------- streaming kernel (M <= 64) ----------------
 //
-// Workgroup = 4 x WK waves (WK = 1, 2 or 4): 64 output channels (one 16-channel tile per
-// wave column) x a K slice of WK * KT k steps; wave group kg takes KT consecutive steps.
+// Workgroup = WC x WK waves (WC, WK = 1, 2 or 4): 16 WC output channels (one 16-channel
+// tile per wave column) x a K slice of WK * KT k steps; wave group kg takes KT consecutive
+// steps.  Fewer wave columns spread a narrow projection's weights over more compute units.
 // Every wave first issues the loads of all KT of its weight tiles into registers; the
 // activation slice (MT * 16 rows) then goes to LDS with direct-to-LDS loads, all in
 // flight at once.  The slice's 16-byte chunks are XOR-swizzled inside each row so that
@@ -377,11 +378,12 @@ __device__ __forceinline__ int slice_swizzle(int row) {
   return (row / RP) & MASK;
 }
 
-template <int BITS, int AFMT, int MT, int KT, int WK>
-__global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
+template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
+__global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p) {
   using F = Fmt<BITS, AFMT>;
-  constexpr int NTHREADS = 256 * WK;
-  constexpr int NWAVES = 4 * WK;
+  constexpr int NTHREADS = 64 * WC * WK;
+  constexpr int NWAVES = WC * WK;
+  constexpr int NCOL = 16 * WC;             // output channels per workgroup
   constexpr int LU4 = F::lb / 16;           // 16-byte loads per lane per weight tile
   constexpr int AROW = WK * KT * F::arow;   // activation bytes per row in the slice
   constexpr int ROWS = MT * 16;
@@ -394,7 +396,7 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wn = wave & 3, kg = wave >> 2;
+  const int wn = wave % WC, kg = wave / WC;
   const int nblk = blockIdx.x;
   const int split = blockIdx.y;
   const int nsplit = gridDim.y;
@@ -402,7 +404,7 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
   const int slice_begin = split * WK * KT;
   const int ks_begin = slice_begin + kg * KT;
   const int nk = max(0, min(KT, ktot - ks_begin));
-  const int ntile = nblk * 4 + wn;
+  const int ntile = nblk * WC + wn;
   const bool n_ok = ntile * 16 < p.N;
 
   // 1. all weight tiles of this wave in flight
@@ -493,36 +495,36 @@ __global__ __launch_bounds__(256 * WK) void gemm_stream_kernel(GemmParams p) {
     v4i *red = reinterpret_cast<v4i *>(lds);
     if (kg > 0) {
 #pragma unroll
-      for (int i = 0; i < MT; ++i) red[(((kg - 1) * 4 + wn) * MT + i) * 64 + lane] = acc[i][0];
+      for (int i = 0; i < MT; ++i) red[(((kg - 1) * WC + wn) * MT + i) * 64 + lane] = acc[i][0];
     }
     __syncthreads();
     if (kg == 0) {
 #pragma unroll
       for (int g2 = 1; g2 < WK; ++g2)
 #pragma unroll
-        for (int i = 0; i < MT; ++i) acc[i][0] += red[(((g2 - 1) * 4 + wn) * MT + i) * 64 + lane];
+        for (int i = 0; i < MT; ++i) acc[i][0] += red[(((g2 - 1) * WC + wn) * MT + i) * 64 + lane];
     }
     __syncthreads();
   }
-  uint8_t *stage = lds + (size_t)(WK - 1) * 4 * MT * 64 * 16;
+  uint8_t *stage = lds + (size_t)(WK - 1) * WC * MT * 64 * 16;
   if (kg == 0) {
     if (p.acc_out && nsplit == 1 && n_ok) store_acc_out<MT, 1, F::shift>(p, acc, 0, ntile * 16, lane);
     if (nsplit == 1)
-      stage_tiles<MT, 1, F::shift, true>(stage, 64, acc, 0, wn * 16, lane, dt, ep);
+      stage_tiles<MT, 1, F::shift, true>(stage, NCOL, acc, 0, wn * 16, lane, dt, ep);
     else
-      stage_tiles<MT, 1, F::shift, false>(stage, 64, acc, 0, wn * 16, lane, dt, ep);
+      stage_tiles<MT, 1, F::shift, false>(stage, NCOL, acc, 0, wn * 16, lane, dt, ep);
   }
   __syncthreads();
   if (nsplit == 1)
-    store_staged<true>(stage, ROWS, 64, 0, nblk * 64, p, 0, NTHREADS);
+    store_staged<true>(stage, ROWS, NCOL, 0, nblk * NCOL, p, 0, NTHREADS);
   else
-    store_staged<false>(stage, ROWS, 64, 0, nblk * 64, p, split, NTHREADS);
+    store_staged<false>(stage, ROWS, NCOL, 0, nblk * NCOL, p, split, NTHREADS);
 }
 
-template <int BITS, int AFMT, int MT, int KT, int WK>
+template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
 static size_t stream_lds_bytes() {
   const size_t slice = (size_t)MT * 16 * (WK * KT * Fmt<BITS, AFMT>::arow);
-  const size_t out = (size_t)(WK - 1) * 4 * MT * 64 * 16 + (size_t)MT * 16 * (64 * 4 + 16);
+  const size_t out = (size_t)(WK - 1) * WC * MT * 64 * 16 + (size_t)MT * 16 * (16 * WC * 4 + 16);
   return slice > out ? slice : out;
 }
 
@@ -788,7 +790,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Development tuning override, read once: FQ_TUNE="splits=<n>".
 struct Tune {
   int splits = 0;
-  int wk = 0, kt = 0;
+  int wk = 0, kt = 0, wc = 0;
   int stages = 0;
   int loader = -1;
 };
@@ -804,6 +806,8 @@ static Tune read_tune() {
   if (w) t.wk = atoi(w + 3);
   const char *k = strstr(e, "kt=");
   if (k) t.kt = atoi(k + 3);
+  const char *c = strstr(e, "wc=");
+  if (c) t.wc = atoi(c + 3);
   const char *l = strstr(e, "loader=");
   if (l) t.loader = atoi(l + 7);
   return t;
@@ -815,20 +819,26 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
   const int ktot = (int)(K / kTileK);
   if (M <= 64) {
     // Weight streaming.  A workgroup stages its activation slice (all M rows, the slice's
-    // k steps) in LDS once for 4 wave columns of 16 channels; two wave groups of kt steps
-    // each split the slice and add up in LDS.  K of 8 or 16 steps is one slice (no split-K
-    // epilogue kernel); longer K is cut into slices of 8 steps (K <= 4096) or 16 steps,
-    // the shapes that measured fastest for M = 50.
+    // k steps) in LDS once for its wave columns of 16 channels; wave groups of kt steps
+    // split the slice and add up in LDS.  Shapes measured at M = 50: K of at most 16 steps
+    // is one slice over 4 groups (no split-K epilogue kernel); up to 32 steps, slices of
+    // 8 (4 groups of 2); longer K, slices of 16 (2 groups of 8).  Then the fewest wave
+    // columns that keep the grid within one workgroup per compute unit, which spreads a
+    // narrow projection's weight stream over as many compute units as possible.
     pl.kind = 0;
     pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
     if (ktot < 4) {
       pl.wk = 1;
       pl.kt = ktot >= 2 ? 2 : 1;
+    } else if (ktot <= 16) {
+      pl.wk = 4;
+      pl.kt = ktot <= 4 ? 1 : (ktot <= 8 ? 2 : 4);
+    } else if (ktot <= 32) {
+      pl.wk = 4;
+      pl.kt = 2;
     } else {
       pl.wk = 2;
-      pl.kt = ktot <= 16 ? ktot / 2 : (ktot <= 32 ? 4 : 8);
-      if (pl.kt > 8) pl.kt = 8;
-      if (pl.kt == 3 || pl.kt == 5 || pl.kt == 6 || pl.kt == 7) pl.kt = pl.kt < 4 ? 2 : 4;
+      pl.kt = 8;
     }
     if (tune.splits > 0) {
       int per = (ktot + tune.splits - 1) / tune.splits;  // k steps per slice
@@ -840,7 +850,14 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     if (tune.kt > 0) pl.kt = tune.kt;
     pl.ksteps = pl.kt * pl.wk;
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
-    pl.tiles = (N + 63) / 64;
+    pl.wc = 4;
+    for (int wc = 1; wc < 4; wc *= 2)
+      if (((N + 16 * wc - 1) / (16 * wc)) * pl.splits <= 256) {
+        pl.wc = wc;
+        break;
+      }
+    if (tune.wc > 0) pl.wc = tune.wc;
+    pl.tiles = (N + 16 * pl.wc - 1) / (16 * pl.wc);
   } else {
     pl.kind = 1;
     pl.bm = 128;
@@ -878,41 +895,50 @@ static hipError_t allow_lds(Kern kern, size_t lds, bool &done) {
   return hipSuccess;
 }
 
-template <int BITS, int AFMT, int MT, int KT, int WK>
+template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
 static hipError_t launch_stream(const GemmParams &p, dim3 grid, hipStream_t s) {
-  const size_t lds = stream_lds_bytes<BITS, AFMT, MT, KT, WK>();
+  const size_t lds = stream_lds_bytes<BITS, AFMT, MT, KT, WK, WC>();
   static bool attr = false;
-  hipError_t e = allow_lds(&gemm_stream_kernel<BITS, AFMT, MT, KT, WK>, lds, attr);
+  hipError_t e = allow_lds(&gemm_stream_kernel<BITS, AFMT, MT, KT, WK, WC>, lds, attr);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, MT, KT, WK>), grid, dim3(256 * WK), lds, s, p);
+  hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, MT, KT, WK, WC>), grid, dim3(64 * WC * WK), lds, s, p);
   return hipGetLastError();
 }
 
-template <int BITS, int AFMT, int MT>
-static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, dim3 grid, hipStream_t s) {
+template <int BITS, int AFMT, int MT, int WC>
+static hipError_t launch_stream_wc(const GemmParams &p, int kt, int wk, dim3 grid, hipStream_t s) {
   if (wk == 4) {
     switch (kt) {
-      case 1: return launch_stream<BITS, AFMT, MT, 1, 4>(p, grid, s);
-      case 2: return launch_stream<BITS, AFMT, MT, 2, 4>(p, grid, s);
-      case 4: return launch_stream<BITS, AFMT, MT, 4, 4>(p, grid, s);
+      case 1: return launch_stream<BITS, AFMT, MT, 1, 4, WC>(p, grid, s);
+      case 2: return launch_stream<BITS, AFMT, MT, 2, 4, WC>(p, grid, s);
+      case 4: return launch_stream<BITS, AFMT, MT, 4, 4, WC>(p, grid, s);
       default:
-        if constexpr (AFMT == kANibble) return launch_stream<BITS, AFMT, MT, 8, 4>(p, grid, s);
+        if constexpr (AFMT == kANibble) return launch_stream<BITS, AFMT, MT, 8, 4, WC>(p, grid, s);
         return hipErrorInvalidValue;  // a 32-step int8 slice does not fit in LDS
     }
   }
   if (wk == 2) {
     switch (kt) {
-      case 1: return launch_stream<BITS, AFMT, MT, 1, 2>(p, grid, s);
-      case 2: return launch_stream<BITS, AFMT, MT, 2, 2>(p, grid, s);
-      case 4: return launch_stream<BITS, AFMT, MT, 4, 2>(p, grid, s);
-      default: return launch_stream<BITS, AFMT, MT, 8, 2>(p, grid, s);
+      case 1: return launch_stream<BITS, AFMT, MT, 1, 2, WC>(p, grid, s);
+      case 2: return launch_stream<BITS, AFMT, MT, 2, 2, WC>(p, grid, s);
+      case 4: return launch_stream<BITS, AFMT, MT, 4, 2, WC>(p, grid, s);
+      default: return launch_stream<BITS, AFMT, MT, 8, 2, WC>(p, grid, s);
     }
   }
   switch (kt) {
-    case 1: return launch_stream<BITS, AFMT, MT, 1, 1>(p, grid, s);
-    case 2: return launch_stream<BITS, AFMT, MT, 2, 1>(p, grid, s);
-    case 4: return launch_stream<BITS, AFMT, MT, 4, 1>(p, grid, s);
-    default: return launch_stream<BITS, AFMT, MT, 8, 1>(p, grid, s);
+    case 1: return launch_stream<BITS, AFMT, MT, 1, 1, WC>(p, grid, s);
+    case 2: return launch_stream<BITS, AFMT, MT, 2, 1, WC>(p, grid, s);
+    case 4: return launch_stream<BITS, AFMT, MT, 4, 1, WC>(p, grid, s);
+    default: return launch_stream<BITS, AFMT, MT, 8, 1, WC>(p, grid, s);
+  }
+}
+
+template <int BITS, int AFMT, int MT>
+static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, int wc, dim3 grid, hipStream_t s) {
+  switch (wc) {
+    case 1: return launch_stream_wc<BITS, AFMT, MT, 1>(p, kt, wk, grid, s);
+    case 2: return launch_stream_wc<BITS, AFMT, MT, 2>(p, kt, wk, grid, s);
+    default: return launch_stream_wc<BITS, AFMT, MT, 4>(p, kt, wk, grid, s);
   }
 }
 
@@ -933,9 +959,9 @@ static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStre
   if (pl.kind == 0) {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
     switch (pl.mt) {
-      case 1: e = launch_stream_mt<BITS, AFMT, 1>(p, pl.kt, pl.wk, grid, s); break;
-      case 2: e = launch_stream_mt<BITS, AFMT, 2>(p, pl.kt, pl.wk, grid, s); break;
-      default: e = launch_stream_mt<BITS, AFMT, 4>(p, pl.kt, pl.wk, grid, s); break;
+      case 1: e = launch_stream_mt<BITS, AFMT, 1>(p, pl.kt, pl.wk, pl.wc, grid, s); break;
+      case 2: e = launch_stream_mt<BITS, AFMT, 2>(p, pl.kt, pl.wk, pl.wc, grid, s); break;
+      default: e = launch_stream_mt<BITS, AFMT, 4>(p, pl.kt, pl.wk, pl.wc, grid, s); break;
     }
   } else {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
