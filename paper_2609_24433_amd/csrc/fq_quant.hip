@@ -4,17 +4,14 @@
 //
 // Work layout: a row of K channels is split into 16-channel chunks.  A workgroup of NT
 // threads (256, or 1024 when there are few rows) holds RPW = NT / TPR rows; thread tau
-// of a row owns chunks c*TPR + tau.
+// of a row owns chunks c*TPR + tau, so consecutive chunks sit in consecutive lanes.
 //   loads: every chunk of the thread is requested up front (coalesced 16-byte loads);
-//   pass 1: the optional per-channel multiplier and the butterfly stages h = 1..8 run in
-//           registers;
-//   pass 2 (b > 16): the row goes through LDS one segment of TPR chunks at a time (a
-//           segment holds whole b-blocks); each thread takes whole "columns" (channels
-//           col + 16*m of one block), runs stages h = 16..b/2 and writes the results back
-//           in place, then reloads its own chunk.  Segment-sized LDS keeps enough rows
-//           resident per compute unit that their loads overlap;
-//   the row absmax is reduced across the row's threads, and each thread quantizes,
-//   packs and stores its chunks in natural channel order.
+//   stages h = 1..8: the optional per-channel multiplier, then the butterfly inside each
+//           chunk, in registers;
+//   stages h = 16..b/2: lane exchanges (a b-block spans b/16 <= 16 lanes of one wave),
+//           no LDS;
+//   the row absmax is reduced over the row's lanes (DPP / swizzle) and waves (LDS), and
+//   each thread quantizes, packs and stores its chunks in natural channel order.
 // Every stage is the pair update (a, c) -> (a + c, a - c) in fp32 in ascending h, so the
 // result does not depend on where the data lives; no multiply-add is contracted.
 #include "fq_device.hpp"
@@ -141,15 +138,39 @@ __device__ __forceinline__ void store_chunk_bits(uint8_t *row_out, int chunk, co
   }
 }
 
+// Value of lane (l ^ M) of the wave, for M < 32: DPP quad permutations for 1 and 2, a
+// 16-lane row rotation by 8 for 8, the LDS crossbar's bit-mask swizzle (no memory) for 4
+// and 16.  Pure data movement: the butterfly sums stay bit-exact.
+template <int M>
+__device__ __forceinline__ float lane_xor(float v) {
+  const int x = __float_as_int(v);
+  int r;
+  if constexpr (M == 1) r = __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);       // quad_perm 1,0,3,2
+  else if constexpr (M == 2) r = __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);  // quad_perm 2,3,0,1
+  else if constexpr (M == 8) r = __builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, false); // row_ror:8
+  else r = __builtin_amdgcn_ds_swizzle(x, (M << 10) | 0x1F);                                // xor M in 32 lanes
+  return __int_as_float(r);
+}
+
+// Butterfly stage h = 16 M across lanes: chunk j pairs with chunk j ^ M, held by lane ^ M.
+// The lower chunk keeps a + c, the upper one a - c, as fma(+-1, own, partner): one
+// rounding of the exact sum or difference, the same as the add or subtract.
+template <int M, int CPT>
+__device__ __forceinline__ void lane_stage(float (&v)[CPT][16], int tau) {
+  const float sgn = (tau & M) ? -1.0f : 1.0f;
+#pragma unroll
+  for (int c = 0; c < CPT; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[c][i] = __builtin_fmaf(sgn, v[c][i], lane_xor<M>(v[c][i]));
+}
+
 // NT threads per workgroup; a row is handled by TPR = 2^tpr_log2 consecutive threads,
 // each owning CPT chunks (chunk c * TPR + tau).
 template <typename Tin, int LOG2B, int CPT, int NT>
 __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   constexpr int B = 1 << LOG2B;
-  constexpr int B1 = B < 16 ? B : 16;              // stages done in pass 1
-  constexpr int MPU = B > 16 ? B / 16 : 1;         // elements per pass-2 unit
+  constexpr int B1 = B < 16 ? B : 16;              // stages done inside a chunk
   constexpr int NWAVES = NT / kWave;
-  extern __shared__ float smem[];
   __shared__ float red[NWAVES];
 
   const int tid = threadIdx.x;
@@ -197,73 +218,32 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
     butterfly<16, B1>(v1[c]);
   }
 
+  // ---- stages h = 16 .. b/2: a b-block is b/16 consecutive chunks, held by consecutive
+  // lanes of one wave (TPR >= b/16 and a multiple of it), so the partner of chunk j in
+  // stage h is lane ^ (h/16) and every stage is a lane exchange, no LDS round trip ----
+  if constexpr (B >= 32) lane_stage<1, CPT>(v1, tau);
+  if constexpr (B >= 64) lane_stage<2, CPT>(v1, tau);
+  if constexpr (B >= 128) lane_stage<4, CPT>(v1, tau);
+  if constexpr (B >= 256) lane_stage<8, CPT>(v1, tau);
+
+  // ---- row absmax: own chunks, then the row's lanes, then the row's waves ---------------
   float amax = 0.0f;
-  if constexpr (B > 16) {
-    // ---- pass 2, one segment at a time: round c covers chunks [c*TPR, (c+1)*TPR), which
-    // hold whole b-blocks.  The segment goes through LDS with 16 floats of padding after
-    // every block (the 16-lane groups of a wave read different blocks), each thread runs
-    // stages h = 16 .. b/2 over whole columns (channels col + 16*m of one block), writes
-    // them back in place and reloads its own chunk.
-    const int SEG = TPR * 16;
-    const int SEGP = SEG + 16 * (SEG / B);
-    float *srow = smem + (int64_t)row_local * SEGP;
-    constexpr int UPR = 256 / B;  // pass-2 units per thread per round
 #pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int j = c * TPR + tau;
-      if (c > 0) __syncthreads();  // the previous round's reloads are done
-      if (j < nchunks) {
-        float4 *d = reinterpret_cast<float4 *>(srow + tau * 16 + 16 * (tau * 16 / B));
+  for (int c = 0; c < CPT; ++c) {
+    const int j = c * TPR + tau;
+    if (j < nchunks) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          d[i] = make_float4(v1[c][4 * i], v1[c][4 * i + 1], v1[c][4 * i + 2], v1[c][4 * i + 3]);
-      }
-      __syncthreads();
-      const int nunits = (min(SEG, K - c * SEG) / B) * 16;
-#pragma unroll
-      for (int i = 0; i < UPR; ++i) {
-        const int u = i * TPR + tau;
-        if (u < nunits) {
-          const int base = (u >> 4) * (B + 16) + (u & 15);
-          float v2[MPU];
-#pragma unroll
-          for (int m = 0; m < MPU; ++m) v2[m] = srow[base + 16 * m];
-          butterfly<MPU, MPU>(v2);
-#pragma unroll
-          for (int m = 0; m < MPU; ++m) {
-            amax = fmaxf(amax, fabsf(v2[m]));
-            srow[base + 16 * m] = v2[m];
-          }
-        }
-      }
-      __syncthreads();
-      if (j < nchunks) {
-        const float4 *d = reinterpret_cast<const float4 *>(srow + tau * 16 + 16 * (tau * 16 / B));
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float4 t = d[i];
-          v1[c][4 * i] = t.x;
-          v1[c][4 * i + 1] = t.y;
-          v1[c][4 * i + 2] = t.z;
-          v1[c][4 * i + 3] = t.w;
-        }
-      }
-    }
-  } else {
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      const int j = c * TPR + tau;
-      if (j < nchunks) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(v1[c][i]));
-      }
+      for (int i = 0; i < 16; ++i) amax = fmaxf(amax, fabsf(v1[c][i]));
     }
   }
-
-  // ---- row absmax across the row's threads -------------------------------------------
   {
     const int lim = TPR < kWave ? TPR : kWave;
-    for (int off = lim >> 1; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off, kWave));
+    if (lim > 1) amax = fmaxf(amax, lane_xor<1>(amax));
+    if (lim > 2) amax = fmaxf(amax, lane_xor<2>(amax));
+    if (lim > 4) amax = fmaxf(amax, lane_xor<4>(amax));
+    if (lim > 8) amax = fmaxf(amax, lane_xor<8>(amax));
+    if (lim > 16) amax = fmaxf(amax, lane_xor<16>(amax));
+    if (lim > 32) amax = fmaxf(amax, __shfl_xor(amax, 32, kWave));
     if (TPR > kWave) {
       if ((tid & (kWave - 1)) == 0) red[tid / kWave] = amax;
       __syncthreads();
@@ -375,8 +355,8 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
   const int rpw = q.nt >> q.tpr_log2;
   int log2b = 0;
   while ((1 << log2b) < b) ++log2b;
-  const int seg = 16 << q.tpr_log2;  // channels per pass-2 round
-  const size_t smem = b > 16 ? (size_t)rpw * (seg + 16 * (seg / b)) * sizeof(float) : 0;
+  const size_t smem = 0;
+  if ((16 << q.tpr_log2) < b) return hipErrorInvalidValue;  // a block must lie in one wave's lanes
   const int64_t grid64 = (M + rpw - 1) / rpw;
   if (grid64 > 0x7FFFFFFF) return hipErrorInvalidValue;
   QuantParams p;
