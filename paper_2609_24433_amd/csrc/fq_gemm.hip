@@ -819,26 +819,22 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
   const int ktot = (int)(K / kTileK);
   if (M <= 64) {
     // Weight streaming.  A workgroup stages its activation slice (all M rows, the slice's
-    // k steps) in LDS once for its wave columns of 16 channels; wave groups of kt steps
-    // split the slice and add up in LDS.  Shapes measured at M = 50: K of at most 16 steps
-    // is one slice over 4 groups (no split-K epilogue kernel); up to 32 steps, slices of
-    // 8 (4 groups of 2); longer K, slices of 16 (2 groups of 8).  Then the fewest wave
-    // columns that keep the grid within one workgroup per compute unit, which spreads a
-    // narrow projection's weight stream over as many compute units as possible.
+    // k steps) in LDS once for its wave columns of 16 channels; 4 wave groups of kt steps
+    // split the slice and add up in LDS.  A slice holds as many k steps as LDS allows
+    // (32 of nibble codes, 16 of int8 codes: 128 KB for 64 rows), so K up to 4096 (W4A4)
+    // needs no split-K epilogue kernel.  Then the fewest wave columns that keep the grid
+    // within one workgroup per compute unit, which spreads a narrow projection's weight
+    // stream over more compute units.  These shapes measured fastest at M = 50.
     pl.kind = 0;
     pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
     if (ktot < 4) {
       pl.wk = 1;
       pl.kt = ktot >= 2 ? 2 : 1;
-    } else if (ktot <= 16) {
-      pl.wk = 4;
-      pl.kt = ktot <= 4 ? 1 : (ktot <= 8 ? 2 : 4);
-    } else if (ktot <= 32) {
-      pl.wk = 4;
-      pl.kt = 2;
     } else {
-      pl.wk = 2;
-      pl.kt = 8;
+      const int cap = bits == 4 ? 32 : 16;
+      const int per = ktot < cap ? ktot : cap;  // k steps per slice
+      pl.wk = 4;
+      pl.kt = per <= 4 ? 1 : (per <= 8 ? 2 : (per <= 16 ? 4 : 8));
     }
     if (tune.splits > 0) {
       int per = (ktot + tune.splits - 1) / tune.splits;  // k steps per slice
