@@ -253,10 +253,10 @@ fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_pa
                     ws_bytes, stream);
 }
 
-// fq_linear workspace: [codes (kernel-native int8)][delta][split-K partials]
+// fq_linear workspace: [codes (nibbles for W4A4, int8 for W8A8)][delta][split-K partials]
 size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
   if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
-  return align256((size_t)M * (size_t)K) + align256((size_t)M * 4) +
+  return align256((size_t)M * (size_t)K * (size_t)bits / 8) + align256((size_t)M * 4) +
          fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
 }
 
@@ -271,7 +271,7 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, in
   s = check_gemm(x_bf16, w_scale, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K);
   if (s != FQ_OK) return s;
   if (M == 0 || N == 0) return ok();
-  const size_t codes_bytes = align256((size_t)M * (size_t)K);
+  const size_t codes_bytes = align256((size_t)M * (size_t)K * (size_t)bits / 8);
   const size_t delta_bytes = align256((size_t)M * 4);
   const size_t need = fq_linear_workspace_bytes(M, N, K, bits);
   if (!ws || ws_bytes < need)
@@ -281,11 +281,10 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, in
   float *delta = reinterpret_cast<float *>(codes + codes_bytes);
   void *gws = codes + codes_bytes + delta_bytes;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  // W4A4 codes between the two kernels: nibbles for the streaming GEMM (small M: halves its
-  // LDS slice), widened int8 in the GEMM's interleaved order for the tiled one (no
-  // activation widening in its inner loop).
-  const bool nibble = bits == 4 && fq::plan_gemm(M, N, K, bits).kind == 0;
-  const int fmt = bits == 8 ? fq::kOutInt8 : (nibble ? fq::kOutNibble : fq::kOutPerm8);
+  // W4A4 codes between the two kernels are canonical nibbles (half the bytes of int8, the
+  // same per-step cost in the GEMMs, which widen them in registers); W8A8 codes are int8.
+  const bool nibble = bits == 4;
+  const int fmt = nibble ? fq::kOutNibble : fq::kOutInt8;
   const int64_t lda = nibble ? K / 2 : K;
   hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, M, (int)K, b, bits, clip_ratio,
                                        inv_sqrt_pow2(b), codes, lda, delta, fmt, st);

@@ -997,7 +997,7 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStrea
   p.ksteps = pl.ksteps;
   p.partial = pl.splits > 1 ? reinterpret_cast<int32_t *>(ws) : nullptr;
   if (g.bits == 4)
-    return g.a_fmt == kANibble ? launch_gemm_t<4, kANibble>(p, pl, s) : launch_gemm_t<4, kAInt8>(p, pl, s);
+    return g.a_fmt == kANibble ? launch_gemm_t<4, kANibble>(p, pl, s) : hipErrorInvalidValue;
   return launch_gemm_t<8, kAInt8>(p, pl, s);
 }
 

@@ -10,11 +10,10 @@ namespace fq {
 // Output layouts of the prologue.
 constexpr int kOutNibble = 0;  // canonical signed-INT4: channel 2i low nibble of byte i
 constexpr int kOutInt8 = 1;    // canonical int8, one byte per channel
-constexpr int kOutPerm8 = 2;   // int8, channels of each group of 8 stored as 0 2 4 6 1 3 5 7
 
 // Activation operand formats of the GEMM.
 constexpr int kANibble = 0;  // canonical nibbles (widened in the kernel)
-constexpr int kAInt8 = 1;    // canonical int8 (W8A8) or kOutPerm8 order (W4A4)
+constexpr int kAInt8 = 1;    // canonical int8 (W8A8)
 
 hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const float *chan_mult,
                              int64_t M, int K, int b, int bits, float clip_ratio, float cb,

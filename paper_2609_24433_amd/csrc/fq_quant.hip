@@ -122,18 +122,6 @@ __device__ __forceinline__ void store_chunk_bits(uint8_t *row_out, int chunk, co
       const uint32_t hi = __builtin_amdgcn_perm((uint32_t)c[4 * i + 3], (uint32_t)c[4 * i + 2], 0x04000c0cu);
       w[i] = lo | hi;
     }
-    if (out_fmt == kOutPerm8) {
-      // per group of 8 channels: bytes c0 c2 c4 c6 c1 c3 c5 c7 (the order in which the
-      // GEMM widens nibble-packed weights)
-      uint32_t p0 = __builtin_amdgcn_perm(w[1], w[0], 0x06040200u);
-      uint32_t p1 = __builtin_amdgcn_perm(w[1], w[0], 0x07050301u);
-      uint32_t p2 = __builtin_amdgcn_perm(w[3], w[2], 0x06040200u);
-      uint32_t p3 = __builtin_amdgcn_perm(w[3], w[2], 0x07050301u);
-      w[0] = p0;
-      w[1] = p1;
-      w[2] = p2;
-      w[3] = p3;
-    }
     *reinterpret_cast<uint4 *>(row_out + (int64_t)chunk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
