@@ -119,8 +119,9 @@ size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
 
 /* The whole runtime projection for one consumer (Alg. 1 runtime; eqs. (5), (8)):
  * prologue on x, integer GEMM against w_packed, rescale + bias, bf16 out.
- * Same arguments and contracts as fq_fwht_quant followed by fq_gemm_w{4a4,8a8}; the
- * intermediate codes live in `ws` in a kernel-native layout. */
+ * Same arguments and contracts as fq_fwht_quant followed by fq_gemm_w{4a4,8a8}, and the
+ * same output bit for bit; the intermediate codes (canonical layout) and scales live
+ * in `ws`. */
 fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
                     int64_t K, int64_t N, int b, int bits, float clip_ratio, const void *w_packed,
                     const float *w_scale, const float *bias, void *y_bf16, int64_t ldy, void *ws,
