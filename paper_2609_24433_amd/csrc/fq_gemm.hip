@@ -16,10 +16,11 @@
 // therefore fetches a whole tile with one fully coalesced 16/32-byte load per lane.
 //
 // Two GEMM kernels:
-//   gemm_stream (M <= 64): streams the weights once; a workgroup owns 64 output
-//     channels and a slice of K (optionally split again between two wave groups that
+//   gemm_stream (M <= 64): streams the weights once; a workgroup owns 16, 32 or 64
+//     output channels and a slice of K (split again between up to 4 wave groups that
 //     add up in LDS); the activation slice is staged to LDS in one batch.
-//   gemm_tile (M > 64): 128 x 128 output tiles fed through a ring of LDS stages.
+//   gemm_tile (M > 64): 128 x 128 output tiles fed through a ring of LDS stages, with a
+//     register-level software pipeline and an optional load-issuing fifth wave.
 // When K is split across workgroups, each slice writes its raw INT32 tile to a
 // partial buffer and a small epilogue kernel adds the slices (exact) and rescales;
 // the kernel boundary orders the two, so no atomics or cache-wide fences are needed.
