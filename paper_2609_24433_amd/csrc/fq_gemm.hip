@@ -379,6 +379,56 @@ __device__ __forceinline__ int slice_swizzle(int row) {
   return (row / RP) & MASK;
 }
 
+// Activation slice -> LDS with direct loads, swizzled 16-byte chunks.  Wave w fills the
+// KBs [w IA, (w+1) IA), whole rows of the slice.  The swizzle of row kb RPK + lr splits
+// into swz(kb RPK) ^ swz(lr), so a lane's offset is fixed up to one XOR with a
+// wave-uniform value and the row pointer advances by a uniform stride.  Rows past M read
+// the KB's first row and (KFULL false) chunks past the end of K read chunk 0: both reach
+// only dropped results.  A KB holding only rows past M is not loaded.
+template <int AROW, int IA, int SLICE_KB, bool KFULL>
+__device__ __forceinline__ void stage_slice(const uint8_t *abase, int64_t lda, int M, int wave, int lane,
+                                            int valid_cols, uint8_t *lds) {
+  constexpr int CPR = AROW / 16;  // 16-byte chunks per row
+  if constexpr (CPR >= 64) {
+    // a KB is 1/KPR of one row: row uniform, lane chunk h 64 + (lane ^ swz(row))
+    constexpr int KPR = CPR / 64;
+    constexpr int RPW = IA / KPR;  // rows per wave
+    static_assert(IA % KPR == 0, "a wave loads whole rows");
+    const int row0 = wave * RPW;
+    const uint8_t *rp = abase + (int64_t)row0 * lda;
+#pragma unroll
+    for (int rr = 0; rr < RPW; ++rr, rp += lda) {
+      const int row = row0 + rr;
+      if (row * KPR >= SLICE_KB || row >= M) break;
+      const int x = lane ^ slice_swizzle<AROW>(row);
+#pragma unroll
+      for (int h = 0; h < KPR; ++h) {
+        int col = h * 64 + x;
+        if (!KFULL && col >= valid_cols) col = 0;
+        load_to_lds16(rp + (uint32_t)(col * 16), lds + (row * KPR + h) * 1024);
+      }
+    }
+  } else {
+    // a KB holds RPK whole rows: lane -> row lr = lane / CPR, chunk pos = lane % CPR
+    constexpr int RPK = 64 / CPR;
+    const int lr = lane / CPR, pos = lane % CPR;
+    const int px = pos ^ slice_swizzle<AROW>(lr);
+    const int kb0 = wave * IA;
+    const uint8_t *rp = abase + (int64_t)kb0 * RPK * lda;
+    const uint32_t lro = (uint32_t)(lr * lda);
+#pragma unroll
+    for (int i = 0; i < IA; ++i, rp += RPK * lda) {
+      const int kb = kb0 + i;
+      const int row = kb * RPK;  // first row of the KB
+      if (kb >= SLICE_KB || row >= M) break;
+      int col = px ^ slice_swizzle<AROW>(row);
+      if (!KFULL && col >= valid_cols) col = 0;
+      const uint32_t ro = row + RPK <= M || lr < M - row ? lro : 0u;
+      load_to_lds16(rp + (ro + (uint32_t)(col * 16)), lds + kb * 1024);
+    }
+  }
+}
+
 template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
 __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p) {
   using F = Fmt<BITS, AFMT>;
@@ -396,7 +446,7 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar index math
   const int wn = wave % WC, kg = wave / WC;
   const int nblk = blockIdx.x;
   const int split = blockIdx.y;
@@ -408,37 +458,48 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
   const int ntile = nblk * WC + wn;
   const bool n_ok = ntile * 16 < p.N;
 
-  // 1. all weight tiles of this wave in flight
+  // 1. all weight tiles of this wave in flight.  Loads are unconditional (a step past the
+  // end of K re-reads the last tile, never used) so that no branch sits between them.
   uint4 wreg[KT][LU4];
-  const uint8_t *wbase = p.w + ((int64_t)min(ntile, p.N / 16 - 1) * ktot + ks_begin) * F::tb + lane * F::lb;
+  const uint8_t *wtile = p.w + (int64_t)min(ntile, p.N / 16 - 1) * ktot * F::tb + lane * F::lb;
+  if (nk == KT) {
 #pragma unroll
-  for (int kt = 0; kt < KT; ++kt)
+    for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
-    for (int u = 0; u < LU4; ++u)
-      wreg[kt][u] = (kt < nk) ? reinterpret_cast<const uint4 *>(wbase + (int64_t)kt * F::tb)[u]
-                              : make_uint4(0, 0, 0, 0);
-
-  // 2. activation slice -> LDS, direct loads, swizzled chunks.  Rows past M read row M-1
-  // and chunks past the end of K read chunk 0: both only reach results that are dropped.
-  const uint8_t *abase = p.a + (int64_t)slice_begin * F::arow;
-  const int valid_cols = min(WK * KT, ktot - slice_begin) * (F::arow / 16);
+      for (int u = 0; u < LU4; ++u)
+        wreg[kt][u] = reinterpret_cast<const uint4 *>(wtile + (int64_t)(ks_begin + kt) * F::tb)[u];
+  } else {
 #pragma unroll
-  for (int i = 0; i < IA; ++i) {
-    const int kb = wave * IA + i;  // KB of the slice this instruction fills
-    // a KB holding only rows past M is not loaded: those rows reach no stored output
-    if (kb < SLICE_KB && (kb * 64) / CPR < p.M) {
-      const int slot = kb * 64 + lane;
-      const int row = slot / CPR, pos = slot % CPR;
-      int col = pos ^ slice_swizzle<AROW>(row);
-      if (col >= valid_cols) col = 0;
-      const int grow = min(row, p.M - 1);
-      load_to_lds16(abase + (int64_t)grow * p.lda + col * 16, lds + kb * 1024);
-    }
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int u = 0; u < LU4; ++u)
+        wreg[kt][u] = reinterpret_cast<const uint4 *>(wtile + (int64_t)min(ks_begin + kt, ktot - 1) * F::tb)[u];
   }
 
+  // 2. activation slice -> LDS (see stage_slice)
+  {
+    const uint8_t *abase = p.a + (int64_t)slice_begin * F::arow;
+    const int valid_cols = min(WK * KT, ktot - slice_begin) * (F::arow / 16);
+    if (valid_cols == CPR)
+      stage_slice<AROW, IA, SLICE_KB, true>(abase, p.lda, p.M, wave, lane, valid_cols, lds);
+    else
+      stage_slice<AROW, IA, SLICE_KB, false>(abase, p.lda, p.M, wave, lane, valid_cols, lds);
+  }
+
+  // rescale factors of the row tiles this wave group finishes (i = kg mod WK)
   float dt[MT][4];
   EpiParams ep[1];
-  if (nsplit == 1) load_epi<MT, 1>(p, 0, ntile * 16, lane, dt, ep);
+  if (nsplit == 1) {
+    const int g = lane >> 4, cl = lane & 15;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+      if (i % WK == kg)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) dt[i][r] = p.delta[min(16 * i + 4 * g + r, p.M - 1)];
+    const int n = min(ntile * 16 + cl, p.N - 1);
+    ep[0].sw = p.w_scale[n];
+    ep[0].bj = p.bias ? p.bias[n] : 0.0f;
+  }
 
   wait_vmcnt<0>();
   lds_barrier();
@@ -490,31 +551,35 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
     }
   }
 
-  // 4. wave groups add up in LDS, then the 64-channel tile leaves through the LDS stage
+  // 4. every wave group leaves its tiles in LDS; wave group kg adds up row tiles
+  // i = kg mod WK (exact integer sums) and stages them; the tile leaves through the stage
   __syncthreads();  // the activation slice is no longer read
+  uint8_t *stage = lds + (WK > 1 ? (size_t)WK * WC * MT * 64 * 16 : 0);
   if constexpr (WK > 1) {
     v4i *red = reinterpret_cast<v4i *>(lds);
-    if (kg > 0) {
 #pragma unroll
-      for (int i = 0; i < MT; ++i) red[(((kg - 1) * WC + wn) * MT + i) * 64 + lane] = acc[i][0];
-    }
+    for (int i = 0; i < MT; ++i) red[((kg * WC + wn) * MT + i) * 64 + lane] = acc[i][0];
     __syncthreads();
-    if (kg == 0) {
 #pragma unroll
-      for (int g2 = 1; g2 < WK; ++g2)
+    for (int i = 0; i < MT; ++i)
+      if (i % WK == kg) {
+        v4i t = red[(wn * MT + i) * 64 + lane];
 #pragma unroll
-        for (int i = 0; i < MT; ++i) acc[i][0] += red[(((g2 - 1) * WC + wn) * MT + i) * 64 + lane];
+        for (int g2 = 1; g2 < WK; ++g2) t += red[((g2 * WC + wn) * MT + i) * 64 + lane];
+        acc[i][0] = t;
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+    if (i % WK == kg) {
+      const v4i t[1][1] = {{acc[i][0]}};
+      const float d[1][4] = {{dt[i][0], dt[i][1], dt[i][2], dt[i][3]}};
+      if (p.acc_out && nsplit == 1 && n_ok) store_acc_out<1, 1, F::shift>(p, t, 16 * i, ntile * 16, lane);
+      if (nsplit == 1)
+        stage_tiles<1, 1, F::shift, true>(stage, NCOL, t, 16 * i, wn * 16, lane, d, ep);
+      else
+        stage_tiles<1, 1, F::shift, false>(stage, NCOL, t, 16 * i, wn * 16, lane, d, ep);
     }
-    __syncthreads();
-  }
-  uint8_t *stage = lds + (size_t)(WK - 1) * WC * MT * 64 * 16;
-  if (kg == 0) {
-    if (p.acc_out && nsplit == 1 && n_ok) store_acc_out<MT, 1, F::shift>(p, acc, 0, ntile * 16, lane);
-    if (nsplit == 1)
-      stage_tiles<MT, 1, F::shift, true>(stage, NCOL, acc, 0, wn * 16, lane, dt, ep);
-    else
-      stage_tiles<MT, 1, F::shift, false>(stage, NCOL, acc, 0, wn * 16, lane, dt, ep);
-  }
   __syncthreads();
   if (nsplit == 1)
     store_staged<true>(stage, ROWS, NCOL, 0, nblk * NCOL, p, 0, NTHREADS);
@@ -525,7 +590,8 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
 template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
 static size_t stream_lds_bytes() {
   const size_t slice = (size_t)MT * 16 * (WK * KT * Fmt<BITS, AFMT>::arow);
-  const size_t out = (size_t)(WK - 1) * WC * MT * 64 * 16 + (size_t)MT * 16 * (16 * WC * 4 + 16);
+  const size_t red = WK > 1 ? (size_t)WK * WC * MT * 64 * 16 : 0;
+  const size_t out = red + (size_t)MT * 16 * (16 * WC * 4 + 16);
   return slice > out ? slice : out;
 }
 
