@@ -17,8 +17,9 @@
 //
 // Two GEMM kernels:
 //   gemm_stream (M <= 64): streams the weights once; a workgroup owns 16, 32 or 64
-//     output channels and a slice of K (split again between up to 4 wave groups that
-//     add up in LDS); the activation slice is staged to LDS in one batch.
+//     output channels, a block of rows (all M, or 16 when the grid would be small) and
+//     a slice of K (split again between up to 4 wave groups that add up in LDS); the
+//     activation slice is staged to LDS in one batch.
 //   gemm_tile (M > 64): 128 x 128 output tiles fed through a ring of LDS stages, with a
 //     register-level software pipeline and an optional load-issuing fifth wave.
 // When K is split across workgroups, each slice writes its raw INT32 tile to a
@@ -360,8 +361,8 @@ __device__ __forceinline__ void wait_ring(int later) {
 // ---------------- streaming kernel (M <= 64) ----------------
 //
 // Workgroup = WC x WK waves (WC, WK = 1, 2 or 4): 16 WC output channels (one 16-channel
-// tile per wave column) x a K slice of WK * KT k steps; wave group kg takes KT consecutive
-// steps.  Fewer wave columns spread a narrow projection's weights over more compute units.
+// tile per wave column) x MT 16-row tiles (row block blockIdx.z) x a K slice of WK * KT
+// k steps; wave group kg takes KT consecutive steps.  Fewer wave columns spread a narrow projection's weights over more compute units.
 // Every wave first issues the loads of all KT of its weight tiles into registers; the
 // activation slice (MT * 16 rows) then goes to LDS with direct-to-LDS loads, all in
 // flight at once.  The slice's 16-byte chunks are XOR-swizzled inside each row so that
@@ -457,6 +458,8 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
   const int nk = max(0, min(KT, ktot - ks_begin));
   const int ntile = nblk * WC + wn;
   const bool n_ok = ntile * 16 < p.N;
+  const int m0 = blockIdx.z * ROWS;      // first row of this workgroup's row block
+  const int mz = min(ROWS, p.M - m0);    // its rows (>= 1)
 
   // 1. all weight tiles of this wave in flight.  Loads are unconditional (a step past the
   // end of K re-reads the last tile, never used) so that no branch sits between them.
@@ -478,12 +481,12 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
 
   // 2. activation slice -> LDS (see stage_slice)
   {
-    const uint8_t *abase = p.a + (int64_t)slice_begin * F::arow;
+    const uint8_t *abase = p.a + (int64_t)m0 * p.lda + (int64_t)slice_begin * F::arow;
     const int valid_cols = min(WK * KT, ktot - slice_begin) * (F::arow / 16);
     if (valid_cols == CPR)
-      stage_slice<AROW, IA, SLICE_KB, true>(abase, p.lda, p.M, wave, lane, valid_cols, lds);
+      stage_slice<AROW, IA, SLICE_KB, true>(abase, p.lda, mz, wave, lane, valid_cols, lds);
     else
-      stage_slice<AROW, IA, SLICE_KB, false>(abase, p.lda, p.M, wave, lane, valid_cols, lds);
+      stage_slice<AROW, IA, SLICE_KB, false>(abase, p.lda, mz, wave, lane, valid_cols, lds);
   }
 
   // rescale factors of the row tiles this wave group finishes (i = kg mod WK)
@@ -495,7 +498,7 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
     for (int i = 0; i < MT; ++i)
       if (i % WK == kg)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dt[i][r] = p.delta[min(16 * i + 4 * g + r, p.M - 1)];
+        for (int r = 0; r < 4; ++r) dt[i][r] = p.delta[min(m0 + 16 * i + 4 * g + r, p.M - 1)];
     const int n = min(ntile * 16 + cl, p.N - 1);
     ep[0].sw = p.w_scale[n];
     ep[0].bj = p.bias ? p.bias[n] : 0.0f;
@@ -574,7 +577,7 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
     if (i % WK == kg) {
       const v4i t[1][1] = {{acc[i][0]}};
       const float d[1][4] = {{dt[i][0], dt[i][1], dt[i][2], dt[i][3]}};
-      if (p.acc_out && nsplit == 1 && n_ok) store_acc_out<1, 1, F::shift>(p, t, 16 * i, ntile * 16, lane);
+      if (p.acc_out && nsplit == 1 && n_ok) store_acc_out<1, 1, F::shift>(p, t, m0 + 16 * i, ntile * 16, lane);
       if (nsplit == 1)
         stage_tiles<1, 1, F::shift, true>(stage, NCOL, t, 16 * i, wn * 16, lane, d, ep);
       else
@@ -582,9 +585,9 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
     }
   __syncthreads();
   if (nsplit == 1)
-    store_staged<true>(stage, ROWS, NCOL, 0, nblk * NCOL, p, 0, NTHREADS);
+    store_staged<true>(stage, ROWS, NCOL, m0, nblk * NCOL, p, 0, NTHREADS);
   else
-    store_staged<false>(stage, ROWS, NCOL, 0, nblk * NCOL, p, split, NTHREADS);
+    store_staged<false>(stage, ROWS, NCOL, m0, nblk * NCOL, p, split, NTHREADS);
 }
 
 template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
@@ -860,6 +863,7 @@ struct Tune {
   int wk = 0, kt = 0, wc = 0;
   int stages = 0;
   int loader = -1;
+  int rb = 0;
 };
 static Tune read_tune() {
   Tune t;
@@ -877,6 +881,8 @@ static Tune read_tune() {
   if (c) t.wc = atoi(c + 3);
   const char *l = strstr(e, "loader=");
   if (l) t.loader = atoi(l + 7);
+  const char *r = strstr(e, "rb=");
+  if (r) t.rb = atoi(r + 3);
   return t;
 }
 
@@ -885,8 +891,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
   GemmPlan pl{};
   const int ktot = (int)(K / kTileK);
   if (M <= 64) {
-    // Weight streaming.  A workgroup stages its activation slice (all M rows, the slice's
-    // k steps) in LDS once for its wave columns of 16 channels; 4 wave groups of kt steps
+    // Weight streaming.  A workgroup stages its activation slice (the rows of its row
+    // block, the slice's k steps) in LDS once for its wave columns of 16 channels; 4 wave groups of kt steps
     // split the slice and add up in LDS.  A slice holds as many k steps as LDS allows
     // (32 of nibble codes, 16 of int8 codes: 128 KB for 64 rows), so K up to 4096 (W4A4)
     // needs no split-K epilogue kernel.  Then the fewest wave columns that keep the grid
@@ -921,6 +927,22 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       }
     if (tune.wc > 0) pl.wc = tune.wc;
     pl.tiles = (N + 16 * pl.wc - 1) / (16 * pl.wc);
+    // A grid that fills at most half the compute units also splits the rows: one 16-row
+    // tile per workgroup, so each workgroup widens a quarter of the activation codes
+    // (M = 50) and four times as many compute units share the weight stream.  Sibling
+    // row blocks read the same weights; when the tile count is a multiple of 8 they run
+    // on one XCD (workgroups go round-robin over the 8 XCDs) and its L2 serves the repeats.
+    pl.rb = 1;
+    if (tune.rb <= 0 && M > 16 && pl.tiles * pl.splits <= 128) {
+      pl.mt = 1;
+      pl.rb = (int)((M + 15) / 16);
+    }
+    if (tune.rb > 1) {
+      const int t16 = (int)((M + 15) / 16);
+      const int per = (t16 + tune.rb - 1) / tune.rb;  // 16-row tiles per row block
+      pl.mt = per <= 1 ? 1 : (per <= 2 ? 2 : 4);
+      pl.rb = (int)((M + 16 * pl.mt - 1) / (16 * pl.mt));
+    }
   } else {
     pl.kind = 1;
     pl.bm = 128;
@@ -1020,7 +1042,7 @@ template <int BITS, int AFMT>
 static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStream_t s) {
   hipError_t e;
   if (pl.kind == 0) {
-    dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
+    dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits, (unsigned)pl.rb);
     switch (pl.mt) {
       case 1: e = launch_stream_mt<BITS, AFMT, 1>(p, pl.kt, pl.wk, pl.wc, grid, s); break;
       case 2: e = launch_stream_mt<BITS, AFMT, 2>(p, pl.kt, pl.wk, pl.wc, grid, s); break;

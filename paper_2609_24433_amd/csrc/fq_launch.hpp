@@ -31,6 +31,7 @@ struct GemmPlan {
   int mt;       // streaming: 16-row tiles covering M
   int kt, wk;   // streaming: k steps per wave, wave groups along K per workgroup
   int wc;       // streaming: 16-channel wave columns per workgroup
+  int rb;       // streaming: row blocks of 16 mt rows (the grid's z dimension)
   int bm, bn;   // tiled: workgroup tile
   int stages;   // tiled: depth of the LDS load ring
   int loader;   // tiled: 1 = a fifth wave issues the ring loads
