@@ -184,6 +184,9 @@ __device__ __forceinline__ v4i w_operand(const uint8_t *tile, int l, int c) {
 
 __device__ __forceinline__ void lds_fence() { asm volatile("" ::: "memory"); }
 
+// Instruction-scheduling wall: the compiler moves nothing across it.
+__device__ __forceinline__ void sched_wall() { __builtin_amdgcn_sched_barrier(0); }
+
 // Workgroup barrier that waits only for this wave's LDS accesses.  __syncthreads() also
 // waits for every outstanding global load (vmcnt(0)), which would drain a prefetch ring.
 __device__ __forceinline__ void lds_barrier() {
@@ -461,25 +464,7 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
   const int m0 = blockIdx.z * ROWS;      // first row of this workgroup's row block
   const int mz = min(ROWS, p.M - m0);    // its rows (>= 1)
 
-  // 1. all weight tiles of this wave in flight.  Loads are unconditional (a step past the
-  // end of K re-reads the last tile, never used) so that no branch sits between them.
-  uint4 wreg[KT][LU4];
-  const uint8_t *wtile = p.w + (int64_t)min(ntile, p.N / 16 - 1) * ktot * F::tb + lane * F::lb;
-  if (nk == KT) {
-#pragma unroll
-    for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-      for (int u = 0; u < LU4; ++u)
-        wreg[kt][u] = reinterpret_cast<const uint4 *>(wtile + (int64_t)(ks_begin + kt) * F::tb)[u];
-  } else {
-#pragma unroll
-    for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-      for (int u = 0; u < LU4; ++u)
-        wreg[kt][u] = reinterpret_cast<const uint4 *>(wtile + (int64_t)min(ks_begin + kt, ktot - 1) * F::tb)[u];
-  }
-
-  // 2. activation slice -> LDS (see stage_slice)
+  // 1. activation slice -> LDS (see stage_slice)
   {
     const uint8_t *abase = p.a + (int64_t)m0 * p.lda + (int64_t)slice_begin * F::arow;
     const int valid_cols = min(WK * KT, ktot - slice_begin) * (F::arow / 16);
@@ -504,7 +489,30 @@ __global__ __launch_bounds__(64 * WC * WK) void gemm_stream_kernel(GemmParams p)
     ep[0].bj = p.bias ? p.bias[n] : 0.0f;
   }
 
-  wait_vmcnt<0>();
+  // 2. then all weight tiles of this wave, in k order.  Vector loads complete in issue
+  // order, so once everything but the weights has landed the slice is in LDS, and the
+  // MFMAs of step kt start when tile kt arrives, while later tiles are still streaming.
+  // Loads are unconditional (a step past the end of K re-reads the last tile, never
+  // used) so that no branch sits between them.
+  sched_wall();
+  uint4 wreg[KT][LU4];
+  const uint8_t *wtile = p.w + (int64_t)min(ntile, p.N / 16 - 1) * ktot * F::tb + lane * F::lb;
+  if (nk == KT) {
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int u = 0; u < LU4; ++u)
+        wreg[kt][u] = reinterpret_cast<const uint4 *>(wtile + (int64_t)(ks_begin + kt) * F::tb)[u];
+  } else {
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int u = 0; u < LU4; ++u)
+        wreg[kt][u] = reinterpret_cast<const uint4 *>(wtile + (int64_t)min(ks_begin + kt, ktot - 1) * F::tb)[u];
+  }
+
+  sched_wall();
+  wait_vmcnt<KT * LU4>();
   lds_barrier();
 
   // 3. MFMA over the wave's k steps, activation operands one step ahead in registers
