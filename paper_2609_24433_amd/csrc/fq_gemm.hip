@@ -291,44 +291,38 @@ __device__ __forceinline__ void load_epi(const GemmParams &p, int m_base, int n_
 
 // ---------------- split-K epilogue ----------------
 // Adds the K slices of the raw INT32 partials (exact, fixed order), divides out the
-// widening scale and applies the eq. (8) rescale; 8 output columns per thread.
+// widening scale and applies the eq. (8) rescale; 4 output columns per thread.  The loads
+// of up to 8 slices and of the rescale factors are all issued before the first add, so a
+// thread waits for one round trip rather than one per slice.
 template <int SHIFT>
 __global__ __launch_bounds__(256) void splitk_epilogue_kernel(GemmParams p, int slices) {
-  const int cpr = p.N / 8;
+  const int cpr = p.N / 4;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)p.M * cpr) return;
-  const int m = (int)(idx / cpr), n = (int)(idx % cpr) * 8;
-  int a[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int z = 0; z < slices; ++z) {
-    const int4 *src = reinterpret_cast<const int4 *>(p.partial + ((int64_t)z * p.M + m) * p.N + n);
-    const int4 u = src[0], v = src[1];
-    a[0] += u.x; a[1] += u.y; a[2] += u.z; a[3] += u.w;
-    a[4] += v.x; a[5] += v.y; a[6] += v.z; a[7] += v.w;
-  }
-#pragma unroll
-  for (int i = 0; i < 8; ++i) a[i] >>= SHIFT;
-  if (p.acc_out) {
-    int4 *d = reinterpret_cast<int4 *>(p.acc_out + (int64_t)m * p.N + n);
-    d[0] = make_int4(a[0], a[1], a[2], a[3]);
-    d[1] = make_int4(a[4], a[5], a[6], a[7]);
-  }
+  const int m = (int)(idx / cpr), n = (int)(idx % cpr) * 4;
   const float dt = p.delta[m];
-  const float4 s0 = *reinterpret_cast<const float4 *>(p.w_scale + n);
-  const float4 s1 = *reinterpret_cast<const float4 *>(p.w_scale + n + 4);
-  const float sw[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-  float bj[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  if (p.bias) {
-    const float4 b0 = *reinterpret_cast<const float4 *>(p.bias + n);
-    const float4 b1 = *reinterpret_cast<const float4 *>(p.bias + n + 4);
-    bj[0] = b0.x; bj[1] = b0.y; bj[2] = b0.z; bj[3] = b0.w;
-    bj[4] = b1.x; bj[5] = b1.y; bj[6] = b1.z; bj[7] = b1.w;
-  }
-  uint32_t o[4];
+  const float4 sw = *reinterpret_cast<const float4 *>(p.w_scale + n);
+  const float4 bj = p.bias ? *reinterpret_cast<const float4 *>(p.bias + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+  const int4 *src = reinterpret_cast<const int4 *>(p.partial + (int64_t)m * p.N + n);
+  const int64_t zs = (int64_t)p.M * p.N / 4;  // int4 stride between slices
+  int a[4] = {0, 0, 0, 0};
+  for (int z0 = 0; z0 < slices; z0 += 8) {
+    int4 v[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    o[i] = f32_to_bf16(rescale(a[2 * i], sw[2 * i], dt, bj[2 * i])) |
-           (f32_to_bf16(rescale(a[2 * i + 1], sw[2 * i + 1], dt, bj[2 * i + 1])) << 16);
-  *reinterpret_cast<uint4 *>(p.y + (int64_t)m * p.ldy + n) = make_uint4(o[0], o[1], o[2], o[3]);
+    for (int z = 0; z < 8; ++z)
+      if (z0 + z < slices) v[z] = src[(z0 + z) * zs];
+#pragma unroll
+    for (int z = 0; z < 8; ++z)
+      if (z0 + z < slices) {
+        a[0] += v[z].x; a[1] += v[z].y; a[2] += v[z].z; a[3] += v[z].w;
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) a[i] >>= SHIFT;
+  if (p.acc_out) *reinterpret_cast<int4 *>(p.acc_out + (int64_t)m * p.N + n) = make_int4(a[0], a[1], a[2], a[3]);
+  const uint32_t o0 = f32_to_bf16(rescale(a[0], sw.x, dt, bj.x)) | (f32_to_bf16(rescale(a[1], sw.y, dt, bj.y)) << 16);
+  const uint32_t o1 = f32_to_bf16(rescale(a[2], sw.z, dt, bj.z)) | (f32_to_bf16(rescale(a[3], sw.w, dt, bj.w)) << 16);
+  *reinterpret_cast<uint2 *>(p.y + (int64_t)m * p.ldy + n) = make_uint2(o0, o1);
 }
 
 // 16 bytes per lane from global memory straight into LDS; a wave fills the contiguous
@@ -1069,7 +1063,7 @@ static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStre
       e = pl.stages == 4 ? launch_tile<BITS, AFMT, 4, 0>(p, grid, s) : launch_tile<BITS, AFMT, 3, 0>(p, grid, s);
   }
   if (e != hipSuccess || pl.splits == 1) return e;
-  const int64_t threads = (int64_t)p.M * (p.N / 8);
+  const int64_t threads = (int64_t)p.M * (p.N / 4);
   const unsigned blocks = (unsigned)((threads + 255) / 256);
   hipLaunchKernelGGL((splitk_epilogue_kernel<Fmt<BITS, AFMT>::shift>), dim3(blocks), dim3(256), 0, s, p,
                      pl.splits);
