@@ -96,10 +96,11 @@ def measured_traffic(site):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("sources_sha256") != sources_digest() or t.get("site") != site:
+    r = t.get("sites", {}).get(site)
+    if t.get("sources_sha256") != sources_digest() or r is None:
         return None
-    fetch = t["fetch_kib_per_call"] * 1024 * t["copy_bytes_read"] / (t["copy_fetch_kib"] * 1024)
-    write = t["write_kib_per_call"] * 1024 * t["copy_bytes_written"] / (t["copy_write_kib"] * 1024)
+    fetch = r["fetch_kib_per_call"] * 1024 * t["copy_bytes_read"] / (t["copy_fetch_kib"] * 1024)
+    write = r["write_kib_per_call"] * 1024 * t["copy_bytes_written"] / (t["copy_write_kib"] * 1024)
     return int(round(fetch + write))
 
 
