@@ -34,8 +34,8 @@ def _lib():
         lib = ctypes.CDLL(_build.LIB)
         i64, i32, f32 = ctypes.c_int64, ctypes.c_int, ctypes.c_float
         vp = ctypes.c_void_p
-        lib.fqo_fwht_quant_bf16.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp, vp, vp]
-        lib.fqo_fwht_quant_f32.argtypes = [vp, i64, vp, i64, i64, i64, i32, f32, vp, vp, vp]
+        lib.fqo_fwht_quant_bf16.argtypes = [vp, i64, vp, vp, i64, i64, i64, i32, f32, vp, vp, vp]
+        lib.fqo_fwht_quant_f32.argtypes = [vp, i64, vp, vp, i64, i64, i64, i32, f32, vp, vp, vp]
         lib.fqo_pack_int4.argtypes = [vp, i64, i64, vp]
         lib.fqo_gemm_i64.argtypes = [vp, vp, i64, i64, i64, vp]
         lib.fqo_dequant.argtypes = [vp, vp, vp, vp, i64, i64, vp]
@@ -90,11 +90,13 @@ def bf16_bits(x) -> np.ndarray:
 
 
 def fwht_quant(x, b: int, bits: int, clip_ratio: float = 1.0,
-               chan_mult: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+               chan_mult: Optional[np.ndarray] = None,
+               post_mult: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
     """Runtime prologue on tokens (Alg. 1 runtime; eq. (5)).
 
     x: bf16 torch tensor [M, K] or uint16 bit array, or float32 array [M, K].
-    chan_mult: optional fp32 [K] multiplier applied before the rotation.
+    chan_mult: optional fp32 [K] multiplier applied before the rotation (fold-before S^-1).
+    post_mult: optional fp32 [K] multiplier applied after it (fold-after P^-1, Sec. III-B).
     Returns (codes int8 [M, K] unpacked, delta float32 [M]).
     """
     lib = _lib()
@@ -105,13 +107,14 @@ def fwht_quant(x, b: int, bits: int, clip_ratio: float = 1.0,
     delta = np.zeros(M, dtype=np.float32)
     scratch = np.zeros(max(1, max_threads()) * max(K, 1), dtype=np.float32)
     cm = None if chan_mult is None else np.ascontiguousarray(chan_mult, dtype=np.float32)
+    pm = None if post_mult is None else np.ascontiguousarray(post_mult, dtype=np.float32)
     if x.dtype == np.uint16:
         xx = np.ascontiguousarray(x)
-        rc = lib.fqo_fwht_quant_bf16(_ptr(xx), K, _ptr(cm), M, K, b, bits, clip_ratio,
+        rc = lib.fqo_fwht_quant_bf16(_ptr(xx), K, _ptr(cm), _ptr(pm), M, K, b, bits, clip_ratio,
                                      _ptr(codes), _ptr(delta), _ptr(scratch))
     elif x.dtype == np.float32:
         xx = np.ascontiguousarray(x)
-        rc = lib.fqo_fwht_quant_f32(_ptr(xx), K, _ptr(cm), M, K, b, bits, clip_ratio,
+        rc = lib.fqo_fwht_quant_f32(_ptr(xx), K, _ptr(cm), _ptr(pm), M, K, b, bits, clip_ratio,
                                     _ptr(codes), _ptr(delta), _ptr(scratch))
     else:
         raise TypeError(f"unsupported dtype {x.dtype}")
@@ -119,14 +122,15 @@ def fwht_quant(x, b: int, bits: int, clip_ratio: float = 1.0,
     return codes, delta
 
 
-def quantize_weights(w: np.ndarray, b: int, bits: int,
-                     col_scale: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
-    """Offline fold + round-to-nearest (Alg. 1 offline; eq. (2) with T = R S^-1).
+def quantize_weights(w: np.ndarray, b: int, bits: int, col_scale: Optional[np.ndarray] = None,
+                     post_scale: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Offline fold + round-to-nearest (Alg. 1 offline; eq. (2) with T = P^-1 R S^-1).
 
-    Row j of the folded weight W S R^T is R (s . w_j); it is rounded with the same
-    per-row rule as a token at r = 1.  Returns (codes int8 [N, K], s_w float32 [N]).
+    Row j of the folded weight W S R^T P is p . R (s . w_j) (fold-before S, fold-after P,
+    Sec. III-B); it is rounded with the same per-row rule as a token at r = 1.
+    Returns (codes int8 [N, K], s_w float32 [N]).
     """
-    return fwht_quant(np.ascontiguousarray(w, dtype=np.float32), b, bits, 1.0, col_scale)
+    return fwht_quant(np.ascontiguousarray(w, dtype=np.float32), b, bits, 1.0, col_scale, post_scale)
 
 
 def pack_int4(codes: np.ndarray) -> np.ndarray:
@@ -165,9 +169,9 @@ def dequant(acc: np.ndarray, delta: np.ndarray, s_w: np.ndarray,
 
 def linear(x, w_codes: np.ndarray, s_w: np.ndarray, b: int, bits: int,
            clip_ratio: float = 1.0, smooth_inv: Optional[np.ndarray] = None,
-           bias: Optional[np.ndarray] = None):
+           bias: Optional[np.ndarray] = None, post_inv: Optional[np.ndarray] = None):
     """Whole runtime path of Alg. 1 for one consumer: returns (codes, delta, acc, y)."""
-    codes, delta = fwht_quant(x, b, bits, clip_ratio, smooth_inv)
+    codes, delta = fwht_quant(x, b, bits, clip_ratio, smooth_inv, post_inv)
     acc = gemm(codes, w_codes)
     y = dequant(acc, delta, s_w, bias)
     return codes, delta, acc, y

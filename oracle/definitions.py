@@ -5,9 +5,10 @@ and no reordering, so it can be checked against the paper by eye:
   * sylvester(b): H_b[i, j] = (-1)^popcount(i & j), the Sylvester +-1 matrix in
     natural order (Sec. III-C).
   * block_rotation(K, b): R = I_{K/b} (x) H_b / sqrt(b) (Sec. III-C).
-  * fold_weight(W, s, b): W~ = W S R^T, the fold-before consumer weight
-    (Sec. III-C, T = R S^-1 in eq. (3); eq. (2) with identity output transform).
-  * transform_tokens(X, s_inv, b): z_t = R S^-1 x_t.
+  * fold_weight(W, b, s, p): W~ = W S R^T P, the consumer weight of the fold presets
+    (Sec. III-B: fold-before (S^-1, I) gives W S R^T, fold-after (I, P^-1) gives
+    W R^T P; eq. (2)).
+  * transform_tokens(X, b, s_inv, p_inv): z_t = P^-1 R S^-1 x_t.
   * quantize_eq5(Z, bits, r): eq. (5) in float64 with the zero-token rule.
   * integer_output(qw, s_w, qa, delta, bias): eq. (8).
 """
@@ -38,22 +39,30 @@ def block_rotation(K: int, b: int) -> np.ndarray:
     return np.kron(np.eye(K // b), sylvester(b) / np.sqrt(b))
 
 
-def transform_tokens(X: np.ndarray, b: int, s_inv: Optional[np.ndarray] = None) -> np.ndarray:
-    """z_t = R S^-1 x_t for every row x_t of X (float64 [M, K])."""
+def transform_tokens(X: np.ndarray, b: int, s_inv: Optional[np.ndarray] = None,
+                     p_inv: Optional[np.ndarray] = None) -> np.ndarray:
+    """z_t = P^-1 R S^-1 x_t for every row x_t of X (float64 [M, K])."""
     X = np.asarray(X, dtype=np.float64)
     if s_inv is not None:
         X = X * np.asarray(s_inv, dtype=np.float64)[None, :]
     R = block_rotation(X.shape[1], b)
-    return X @ R.T
+    Z = X @ R.T
+    if p_inv is not None:
+        Z = Z * np.asarray(p_inv, dtype=np.float64)[None, :]
+    return Z
 
 
-def fold_weight(W: np.ndarray, b: int, s: Optional[np.ndarray] = None) -> np.ndarray:
-    """W~ = W S R^T (float64 [N, K])."""
+def fold_weight(W: np.ndarray, b: int, s: Optional[np.ndarray] = None,
+                p: Optional[np.ndarray] = None) -> np.ndarray:
+    """W~ = W S R^T P (float64 [N, K])."""
     W = np.asarray(W, dtype=np.float64)
     if s is not None:
         W = W * np.asarray(s, dtype=np.float64)[None, :]
     R = block_rotation(W.shape[1], b)
-    return W @ R.T
+    Wt = W @ R.T
+    if p is not None:
+        Wt = Wt * np.asarray(p, dtype=np.float64)[None, :]
+    return Wt
 
 
 def quantize_eq5(Z: np.ndarray, bits: int, r: float = 1.0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:

@@ -109,45 +109,52 @@ static int check_args(int64_t M, int64_t K, int64_t b, int bits, float r, int64_
     return FQO_OK;
 }
 
-/* One row: optional per-channel multiplier, blockwise FWHT, quantize. */
-static void transform_quantize_row(float *v, const float *chan_mult, int64_t K, int64_t b,
-                                   int bits, float r, float cb, int8_t *code, float *delta) {
+/* One row: optional per-channel multiplier before the rotation (fold-before S^-1,
+ * Sec. III-B), blockwise FWHT, optional per-channel multiplier after it (fold-after
+ * P^-1, Sec. III-B), quantize.  Each multiplier is one fp32 rounding per element. */
+static void transform_quantize_row(float *v, const float *chan_mult, const float *post_mult,
+                                   int64_t K, int64_t b, int bits, float r, float cb,
+                                   int8_t *code, float *delta) {
     if (chan_mult)
         for (int64_t c = 0; c < K; ++c) v[c] = v[c] * chan_mult[c];
     for (int64_t k0 = 0; k0 < K; k0 += b) fqo_fwht_block_f32(v + k0, b);
+    if (post_mult)
+        for (int64_t c = 0; c < K; ++c) v[c] = v[c] * post_mult[c];
     quantize_token(v, K, bits, r, cb, code, delta);
 }
 
 /* Activation prologue (Alg. 1 runtime, first two steps) on bf16 tokens.
  * x: [M, ldx] bf16 bit patterns; chan_mult: [K] or NULL (fold-before S^-1);
- * codes: [M, K] int8 (unpacked); delta: [M]; scratch: [nthreads * K] floats. */
-int fqo_fwht_quant_bf16(const uint16_t *x, int64_t ldx, const float *chan_mult, int64_t M,
-                        int64_t K, int64_t b, int bits, float r, int8_t *codes, float *delta,
-                        float *scratch) {
+ * post_mult: [K] or NULL (fold-after P^-1); codes: [M, K] int8 (unpacked);
+ * delta: [M]; scratch: [nthreads * K] floats. */
+int fqo_fwht_quant_bf16(const uint16_t *x, int64_t ldx, const float *chan_mult,
+                        const float *post_mult, int64_t M, int64_t K, int64_t b, int bits,
+                        float r, int8_t *codes, float *delta, float *scratch) {
     if (check_args(M, K, b, bits, r, ldx)) return FQO_BAD_ARG;
     const float cb = fqo_inv_sqrt_b(b);
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t t = 0; t < M; ++t) {
         float *v = scratch + (int64_t)omp_thread_slot() * K;
         for (int64_t c = 0; c < K; ++c) v[c] = bf16_bits_to_float(x[t * ldx + c]);
-        transform_quantize_row(v, chan_mult, K, b, bits, r, cb, codes + t * K, delta + t);
+        transform_quantize_row(v, chan_mult, post_mult, K, b, bits, r, cb, codes + t * K, delta + t);
     }
     return FQO_OK;
 }
 
-/* Same on fp32 rows.  With r = 1 and chan_mult = s (fold-before S), this is the
- * offline weight rounding: row j of W S R^T equals R (s . w_j) because H_b is
- * symmetric, and RTN with a per-output-channel scale (Sec. III-E/F, Alg. 1
- * offline) rounds it with the same per-row rule. */
-int fqo_fwht_quant_f32(const float *x, int64_t ldx, const float *chan_mult, int64_t M, int64_t K,
-                       int64_t b, int bits, float r, int8_t *codes, float *delta, float *scratch) {
+/* Same on fp32 rows.  With r = 1, chan_mult = s (fold-before S) and post_mult = p
+ * (fold-after P), this is the offline weight rounding: row j of W S R^T P equals
+ * p . R (s . w_j) because H_b is symmetric, and RTN with a per-output-channel scale
+ * (Sec. III-E/F, Alg. 1 offline) rounds it with the same per-row rule. */
+int fqo_fwht_quant_f32(const float *x, int64_t ldx, const float *chan_mult, const float *post_mult,
+                       int64_t M, int64_t K, int64_t b, int bits, float r, int8_t *codes,
+                       float *delta, float *scratch) {
     if (check_args(M, K, b, bits, r, ldx)) return FQO_BAD_ARG;
     const float cb = fqo_inv_sqrt_b(b);
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t t = 0; t < M; ++t) {
         float *v = scratch + (int64_t)omp_thread_slot() * K;
         memcpy(v, x + t * ldx, (size_t)K * sizeof(float));
-        transform_quantize_row(v, chan_mult, K, b, bits, r, cb, codes + t * K, delta + t);
+        transform_quantize_row(v, chan_mult, post_mult, K, b, bits, r, cb, codes + t * K, delta + t);
     }
     return FQO_OK;
 }

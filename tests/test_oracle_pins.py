@@ -224,6 +224,38 @@ def test_fold_before_multiplier():
     np.testing.assert_allclose(delta, dref, rtol=1e-6)
 
 
+def test_fold_after_multiplier():
+    # Sec. III-B fold-after: z = P^-1 R x, the per-channel multiply AFTER the rotation.
+    # Against the float64 definition; a multiply placed before the rotation, or on the
+    # wrong channel, moves most codes and fails.
+    x = synth.activations(8, 512, seed=33, outlier_frac=0.01, outlier_scale=30.0)
+    p_inv = synth.channel_vector(512, seed=34, low=0.25, high=4.0)
+    codes, delta = oracle.fwht_quant(x, 64, 4, 1.0, None, p_inv)
+    Z = D.transform_tokens(x.float().numpy(), 64, None, p_inv)
+    ref, dref, ratio = D.quantize_eq5(Z, 4)
+    ok = np.abs(np.abs(ratio - np.floor(ratio)) - 0.5) > 1e-4
+    np.testing.assert_array_equal(codes[ok], ref[ok])
+    np.testing.assert_allclose(delta, dref, rtol=1e-6)
+    wrong = D.transform_tokens(x.float().numpy() * p_inv, 64)  # the multiply before the rotation
+    wref, _, _ = D.quantize_eq5(wrong, 4)
+    assert (wref != codes).mean() > 0.3
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_fold_after_unit_and_power_of_two_scales(bits):
+    # P = I changes nothing; P^-1 = 2^k I scales delta by 2^k and keeps every code
+    # (one exact fp32 multiply, then Prop. 2 homogeneity), bit for bit.
+    x = synth.activations(12, 1024, seed=35, outlier_frac=0.01, outlier_scale=30.0)
+    c0, d0 = oracle.fwht_quant(x, 128, bits)
+    c1, d1 = oracle.fwht_quant(x, 128, bits, 1.0, None, np.ones(1024, np.float32))
+    np.testing.assert_array_equal(c1, c0)
+    np.testing.assert_array_equal(d1, d0)
+    for k in (-3, 5):
+        c2, d2 = oracle.fwht_quant(x, 128, bits, 1.0, None, np.full(1024, 2.0 ** k, np.float32))
+        np.testing.assert_array_equal(c2, c0)
+        np.testing.assert_array_equal(d2, d0 * np.float32(2.0 ** k))
+
+
 # --- eq. (2) / Sec. III-C fold, and the offline weight rounding ---------------------------------
 
 @pytest.mark.parametrize("b", [1, 8, 64, 128])
@@ -234,6 +266,34 @@ def test_fold_identity_float64(b):
     Wt = D.fold_weight(W, b, s)
     Z = D.transform_tokens(X, b, 1.0 / s)
     np.testing.assert_allclose(Z @ Wt.T, X @ W.T, rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("b", [8, 64, 128])
+def test_fold_after_identity_float64(b):
+    # Prop. 1 with T = P^-1 R: (W R^T P)(P^-1 R x) = W x.
+    W = synth.weights(48, 256, seed=43).astype(np.float64)
+    X = synth.activations(10, 256, seed=44, outlier_frac=0.02, outlier_scale=30.0).double().numpy()
+    pv = synth.channel_vector(256, seed=45, low=0.5, high=2.0).astype(np.float64)
+    Wt = D.fold_weight(W, b, None, pv)
+    Z = D.transform_tokens(X, b, None, 1.0 / pv)
+    np.testing.assert_allclose(Z @ Wt.T, X @ W.T, rtol=1e-10, atol=1e-12)
+    # the dense R S R^T of a fold-before scale is not diagonal: the presets differ
+    Rb = D.block_rotation(256, b)
+    dense = Rb @ np.diag(pv) @ Rb.T
+    assert np.abs(dense - np.diag(np.diag(dense))).max() > 1e-3
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_weight_rounding_fold_after(bits):
+    W = synth.weights(64, 512, seed=52)
+    pv = synth.channel_vector(512, seed=53, low=0.5, high=1.5)
+    codes, s_w = oracle.quantize_weights(W, 128, bits, None, pv)
+    Wt = D.fold_weight(W, 128, None, pv)  # W R^T P in float64
+    err = np.abs(Wt - s_w[:, None].astype(np.float64) * codes)
+    assert np.all(err <= s_w[:, None] * 0.5 * (1 + 1e-5))
+    q = 2 ** (bits - 1) - 1
+    assert np.all(np.abs(codes).max(axis=1) == q)
+    np.testing.assert_allclose(s_w, np.abs(Wt).max(axis=1) / q, rtol=1e-6)
 
 
 @pytest.mark.parametrize("bits", [4, 8])
