@@ -2,12 +2,15 @@
  * fq.h -- C ABI of the FoldQuantVLA runtime quantized projection on AMD MI355X (gfx950).
  *
  * The projection (Sec. III-E/F, Alg. 1 runtime) computes, for tokens x_t:
- *   z_t   = R S^-1 x_t,  R = I_{K/b} (x) H_b / sqrt(b)   (block Hadamard, Sec. III-C)
+ *   z_t   = P^-1 R S^-1 x_t,  R = I_{K/b} (x) H_b / sqrt(b)   (block Hadamard, Sec. III-C)
  *   qA_t, delta_t = per-token symmetric quantization of z_t       (eq. (5))
  *   c_jt  = sum_c qW_jc qA_ct   (integer accumulation, INT32)     (eq. (8))
  *   y_jt  = s_j delta_t c_jt + b_j                                 (eq. (8))
- * against weights folded and rounded offline: W~ = W S R^T rounded per output
- * channel to signed INT4 / INT8 codes qW with scales s (Alg. 1 offline).
+ * against weights folded and rounded offline: W~ = W S R^T P rounded per output
+ * channel to signed INT4 / INT8 codes qW with scales s (Alg. 1 offline).  S and P are
+ * the positive diagonal scales of the two fold presets of Sec. III-B: fold-before
+ * (S calibrated in the original coordinates, P = I) and fold-after (S = I, P calibrated
+ * after the rotation); either may be the identity (NULL).
  *
  * Conventions shared by every entry point:
  *   - Every buffer argument is a DEVICE pointer owned by the caller, except where a
@@ -26,7 +29,9 @@
  *
  * Numerical contract of the prologue (so that codes are reproducible bit for bit):
  *   the transform is an fp32 butterfly on the UNNORMALIZED Sylvester matrix with
- *   stages h = 1, 2, ..., b/2, pairs (a, c) -> (a + c, a - c); A_t = max_c |u_tc|
+ *   stages h = 1, 2, ..., b/2, pairs (a, c) -> (a + c, a - c), with the optional
+ *   S^-1 multiply (one fp32 rounding) before it and the optional P^-1 multiply (one
+ *   fp32 rounding) after it; A_t = max_c |u_tc|
  *   over the whole row; inv = q / (r * A_t) (one correctly rounded fp32 division);
  *   code = clamp(rne(u * inv), -q, q); delta_t = ((r * A_t) * c_b) / q with c_b
  *   the float nearest 1/sqrt(b); a zero row gives codes 0 and delta 0.  No fused
@@ -54,27 +59,31 @@ typedef enum {
 
 /* Runtime prologue, Alg. 1 runtime steps 1-2 (Sec. III-C transform, eq. (5)).
  *   x_bf16     [M, ldx] bf16 tokens (only the first K columns are read).
- *   smooth_inv [K] fp32 fold-before multiplier S^-1 (Sec. III-C), or NULL for S = I;
+ *   smooth_inv [K] fp32 fold-before multiplier S^-1 (Sec. III-B/C), or NULL for S = I;
  *              multiplied into x once, in fp32, before the rotation.
+ *   post_inv   [K] fp32 fold-after multiplier P^-1 (Sec. III-B), or NULL for P = I;
+ *              multiplied into the rotated row once, in fp32, before the row absmax.
  *   b          Hadamard block size; bits: 4 or 8 (q = 7 or 127); clip_ratio: r in eq. (5).
  *   a_codes    output codes, canonical layout: bits = 8 -> int8 [M, K];
  *              bits = 4 -> uint8 [M, K/2], byte i of a row = channel 2i in the low
  *              nibble, channel 2i+1 in the high nibble (two's complement).
  *   delta      output fp32 [M] per-token scales (0 for a zero token). */
-fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
-                        int64_t K, int b, int bits, float clip_ratio, void *a_codes, float *delta,
-                        void *stream);
+fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv,
+                        const float *post_inv, int64_t M, int64_t K, int b, int bits,
+                        float clip_ratio, void *a_codes, float *delta, void *stream);
 
 /* Offline weight fold and round-to-nearest, Alg. 1 offline (eq. (2), Sec. III-C/F).
  *   w          [N, ldw] fp32 weights of one consumer (row j = output channel j).
  *   col_scale  [K] fp32 S (fold-before smoothing, times a folded norm gain, eq. (4)),
  *              or NULL; multiplied into each row once, in fp32, before the rotation.
- *   Row j of W S R^T is R (s . w_j) because H_b is symmetric, so each row is rounded
- *   with the prologue's contract at r = 1: w_codes int8 [N, K] in [-q, q] and
+ *   post_scale [K] fp32 P (fold-after scale, Sec. III-B), or NULL; multiplied into
+ *              each rotated row once, in fp32, before the row absmax.
+ *   Row j of W S R^T P is p . R (s . w_j) because H_b is symmetric, so each row is
+ *   rounded with the prologue's contract at r = 1: w_codes int8 [N, K] in [-q, q] and
  *   w_scale fp32 [N] (the per-output-channel s_j). */
-fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scale, int64_t N,
-                              int64_t K, int b, int bits, int8_t *w_codes, float *w_scale,
-                              void *stream);
+fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scale,
+                              const float *post_scale, int64_t N, int64_t K, int b, int bits,
+                              int8_t *w_codes, float *w_scale, void *stream);
 
 /* Bytes of the packed, kernel-native weight layout for an [N, K] matrix. */
 size_t fq_packed_weight_bytes(int64_t N, int64_t K, int bits);
@@ -122,10 +131,10 @@ size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
  * Same arguments and contracts as fq_fwht_quant followed by fq_gemm_w{4a4,8a8}, and the
  * same output bit for bit; the intermediate codes (canonical layout) and scales live
  * in `ws`. */
-fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
-                    int64_t K, int64_t N, int b, int bits, float clip_ratio, const void *w_packed,
-                    const float *w_scale, const float *bias, void *y_bf16, int64_t ldy, void *ws,
-                    size_t ws_bytes, void *stream);
+fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, const float *post_inv,
+                    int64_t M, int64_t K, int64_t N, int b, int bits, float clip_ratio,
+                    const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,
+                    int64_t ldy, void *ws, size_t ws_bytes, void *stream);
 
 /* Static description of a status code, and the thread-local message of the last failure. */
 const char *fq_status_string(fq_status s);

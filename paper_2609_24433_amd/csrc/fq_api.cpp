@@ -79,12 +79,14 @@ fq_status check_prologue_shape(int64_t ldx, int ld_mult, int64_t M, int64_t K, i
   return FQ_OK;
 }
 
-fq_status check_prologue(const void *x, int64_t ldx, int ld_mult, const float *smooth, int64_t M,
-                         int64_t K, int b, int bits, float r, const void *codes, const float *delta) {
+fq_status check_prologue(const void *x, int64_t ldx, int ld_mult, const float *smooth,
+                         const float *post, int64_t M, int64_t K, int b, int bits, float r,
+                         const void *codes, const float *delta) {
   fq_status s = check_prologue_shape(ldx, ld_mult, M, K, b, bits, r);
   if (s != FQ_OK || M == 0) return s;
   if (!x || !codes || !delta) return fail(FQ_ERR_NULL, "input, codes and scales must be non-NULL");
-  if (!aligned16(x) || !aligned16(codes) || !aligned16(delta) || (smooth && !aligned16(smooth)))
+  if (!aligned16(x) || !aligned16(codes) || !aligned16(delta) || (smooth && !aligned16(smooth)) ||
+      (post && !aligned16(post)))
     return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
   return FQ_OK;
 }
@@ -167,28 +169,28 @@ const char *fq_status_string(fq_status s) {
 
 const char *fq_last_error(void) { return g_err; }
 
-fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
-                        int64_t K, int b, int bits, float clip_ratio, void *a_codes, float *delta,
-                        void *stream) {
-  fq_status s = check_prologue(x_bf16, ldx, 8, smooth_inv, M, K, b, bits, clip_ratio, a_codes, delta);
+fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv,
+                        const float *post_inv, int64_t M, int64_t K, int b, int bits,
+                        float clip_ratio, void *a_codes, float *delta, void *stream) {
+  fq_status s = check_prologue(x_bf16, ldx, 8, smooth_inv, post_inv, M, K, b, bits, clip_ratio, a_codes, delta);
   if (s != FQ_OK) return s;
   if (M == 0) return ok();
   const int fmt = bits == 4 ? fq::kOutNibble : fq::kOutInt8;
   const int64_t ldc = bits == 4 ? K / 2 : K;
-  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, M, (int)K, b, bits, clip_ratio,
-                                       inv_sqrt_pow2(b), static_cast<uint8_t *>(a_codes), ldc, delta,
-                                       fmt, static_cast<hipStream_t>(stream));
+  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, post_inv, M, (int)K, b, bits,
+                                       clip_ratio, inv_sqrt_pow2(b), static_cast<uint8_t *>(a_codes), ldc,
+                                       delta, fmt, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
   return ok();
 }
 
-fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scale, int64_t N,
-                              int64_t K, int b, int bits, int8_t *w_codes, float *w_scale,
-                              void *stream) {
-  fq_status s = check_prologue(w, ldw, 4, col_scale, N, K, b, bits, 1.0f, w_codes, w_scale);
+fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scale,
+                              const float *post_scale, int64_t N, int64_t K, int b, int bits,
+                              int8_t *w_codes, float *w_scale, void *stream) {
+  fq_status s = check_prologue(w, ldw, 4, col_scale, post_scale, N, K, b, bits, 1.0f, w_codes, w_scale);
   if (s != FQ_OK) return s;
   if (N == 0) return ok();
-  hipError_t e = fq::launch_fwht_quant(w, true, ldw, col_scale, N, (int)K, b, bits, 1.0f,
+  hipError_t e = fq::launch_fwht_quant(w, true, ldw, col_scale, post_scale, N, (int)K, b, bits, 1.0f,
                                        inv_sqrt_pow2(b), reinterpret_cast<uint8_t *>(w_codes), K,
                                        w_scale, fq::kOutInt8, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "quantize_weights launch");
@@ -260,14 +262,15 @@ size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
          fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
 }
 
-fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, int64_t M,
-                    int64_t K, int64_t N, int b, int bits, float clip_ratio, const void *w_packed,
-                    const float *w_scale, const float *bias, void *y_bf16, int64_t ldy, void *ws,
-                    size_t ws_bytes, void *stream) {
+fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, const float *post_inv,
+                    int64_t M, int64_t K, int64_t N, int b, int bits, float clip_ratio,
+                    const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,
+                    int64_t ldy, void *ws, size_t ws_bytes, void *stream) {
   // validate both stages before enqueueing either
   fq_status s = check_prologue_shape(ldx, 8, M, K, b, bits, clip_ratio);
   if (s != FQ_OK) return s;
   if (M > 0 && smooth_inv && !aligned16(smooth_inv)) return fail(FQ_ERR_ALIGN, "smooth_inv must be 16-byte aligned");
+  if (M > 0 && post_inv && !aligned16(post_inv)) return fail(FQ_ERR_ALIGN, "post_inv must be 16-byte aligned");
   s = check_gemm(x_bf16, w_scale, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K);
   if (s != FQ_OK) return s;
   if (M == 0 || N == 0) return ok();
@@ -286,8 +289,8 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, in
   const bool nibble = bits == 4;
   const int fmt = nibble ? fq::kOutNibble : fq::kOutInt8;
   const int64_t lda = nibble ? K / 2 : K;
-  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, M, (int)K, b, bits, clip_ratio,
-                                       inv_sqrt_pow2(b), codes, lda, delta, fmt, st);
+  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, post_inv, M, (int)K, b, bits,
+                                       clip_ratio, inv_sqrt_pow2(b), codes, lda, delta, fmt, st);
   if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
   return gemm_common(codes, nibble ? fq::kANibble : fq::kAInt8, lda, delta, w_packed, w_scale, bias, y_bf16,
                      ldy, nullptr, M, N, K, bits, gws, ws_bytes - codes_bytes - delta_bytes, st);

@@ -161,6 +161,7 @@ struct GemmParams {
   int M, N, K;
   int ksteps;        // k steps of 128 per K slice
   int32_t *partial;  // [slices][M][N] raw accumulators when K is split
+  int order;         // tiled: bit 0 = tile ids run down the rows first; bit 1 = no XCD grouping
 };
 
 template <int BITS, int AFMT>
@@ -624,8 +625,8 @@ __device__ __forceinline__ int a_swizzle(int row) {
   return AFMT == kANibble ? ((row >> 1) & 3) : ((row >> 1) & 7);
 }
 
-// Logical tile order that keeps consecutive tiles (same activation rows) on one XCD:
-// the hardware hands workgroup p to XCD p % 8.
+// Optional logical tile order that keeps consecutive tiles (same activation rows) on one
+// XCD: the hardware hands workgroup p to XCD p % 8.
 __device__ __forceinline__ int xcd_remap(int p, int total) {
   if ((total & 7) != 0) return p;
   return (p & 7) * (total >> 3) + (p >> 3);
@@ -657,11 +658,13 @@ __global__ __launch_bounds__(256 + 64 * LW) void gemm_tile_kernel(GemmParams p) 
   const int ntiles_n = (p.N + BN - 1) / BN;
   const int ntiles_m = (p.M + BM - 1) / BM;
   const int total = ntiles_n * ntiles_m * gridDim.y;
-  const int logical = xcd_remap(blockIdx.x + blockIdx.y * gridDim.x, total);
+  const int lin = blockIdx.x + blockIdx.y * gridDim.x;
+  const int logical = (p.order & 2) ? lin : xcd_remap(lin, total);
   const int tile_id = logical % (ntiles_n * ntiles_m);
   const int split = logical / (ntiles_n * ntiles_m);
   const int nsplit = gridDim.y;
-  const int tn = tile_id % ntiles_n, tm = tile_id / ntiles_n;
+  const int tn = (p.order & 1) ? tile_id / ntiles_m : tile_id % ntiles_n;
+  const int tm = (p.order & 1) ? tile_id % ntiles_m : tile_id / ntiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
   const int ktot = p.K / kTileK;
   const int ks_begin = split * p.ksteps;
@@ -866,6 +869,7 @@ struct Tune {
   int stages = 0;
   int loader = -1;
   int rb = 0;
+  int order = -1;
 };
 static Tune read_tune() {
   Tune t;
@@ -885,6 +889,8 @@ static Tune read_tune() {
   if (l) t.loader = atoi(l + 7);
   const char *r = strstr(e, "rb=");
   if (r) t.rb = atoi(r + 3);
+  const char *o = strstr(e, "order=");
+  if (o) t.order = atoi(o + 6);
   return t;
 }
 
@@ -964,6 +970,10 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     pl.stages = lone && bits == 4 ? 4 : 3;
     if (tune.stages > 0) pl.stages = tune.stages;
     if (tune.loader >= 0) pl.loader = tune.loader;
+    // Tile ids in workgroup order, rows of tiles along N (measured 2-4% faster at M = 816
+    // than grouping consecutive tiles on one XCD or running down the rows first).
+    pl.order = 2;
+    if (tune.order >= 0) pl.order = tune.order & 3;
   }
   pl.partial_bytes = pl.splits > 1 ? align256((size_t)pl.splits * M * N * 4) : 0;
   return pl;
@@ -1087,6 +1097,7 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStrea
   p.K = (int)g.K;
   p.ksteps = pl.ksteps;
   p.partial = pl.splits > 1 ? reinterpret_cast<int32_t *>(ws) : nullptr;
+  p.order = pl.order;
   if (g.bits == 4)
     return g.a_fmt == kANibble ? launch_gemm_t<4, kANibble>(p, pl, s) : hipErrorInvalidValue;
   return launch_gemm_t<8, kAInt8>(p, pl, s);

@@ -16,7 +16,7 @@ constexpr int kANibble = 0;  // canonical nibbles (widened in the kernel)
 constexpr int kAInt8 = 1;    // canonical int8 (W8A8)
 
 hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const float *chan_mult,
-                             int64_t M, int K, int b, int bits, float clip_ratio, float cb,
+                             const float *post_mult, int64_t M, int K, int b, int bits, float clip_ratio, float cb,
                              uint8_t *codes, int64_t ld_codes, float *delta, int out_fmt,
                              hipStream_t s);
 
@@ -35,6 +35,7 @@ struct GemmPlan {
   int bm, bn;   // tiled: workgroup tile
   int stages;   // tiled: depth of the LDS load ring
   int loader;   // tiled: 1 = a fifth wave issues the ring loads
+  int order;    // tiled: tile order (bit 0: down the rows first; bit 1: no XCD grouping)
   int splits;   // K slices (each slice: ksteps k steps); > 1 adds an epilogue kernel
   int ksteps;   // 128-wide k steps per slice
   int64_t tiles;        // output tiles along the grid's x dimension

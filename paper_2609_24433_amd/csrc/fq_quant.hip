@@ -22,7 +22,8 @@ namespace fq {
 struct QuantParams {
   const void *x;
   int64_t ldx;  // elements
-  const float *chan_mult;
+  const float *chan_mult;  // fold-before S^-1, before the rotation (or NULL)
+  const float *post_mult;  // fold-after P^-1, after the rotation (or NULL)
   int64_t M;
   int K;
   int bits;
@@ -176,7 +177,7 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
 
   // ---- all loads first (branch-free: out-of-range chunks read chunk 0) ----------------
   Chunk<Tin> raw[CPT];
-  float4 cm[CPT][4];
+  float4 cm[CPT][4], pm[CPT][4];
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
     const int j = c * TPR + tau;
@@ -186,6 +187,11 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
       const float4 *m4 = reinterpret_cast<const float4 *>(p.chan_mult + jc * 16);
 #pragma unroll
       for (int i = 0; i < 4; ++i) cm[c][i] = m4[i];
+    }
+    if (p.post_mult) {
+      const float4 *m4 = reinterpret_cast<const float4 *>(p.post_mult + jc * 16);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pm[c][i] = m4[i];
     }
   }
 
@@ -213,6 +219,19 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   if constexpr (B >= 64) lane_stage<2, CPT>(v1, tau);
   if constexpr (B >= 128) lane_stage<4, CPT>(v1, tau);
   if constexpr (B >= 256) lane_stage<8, CPT>(v1, tau);
+
+  // ---- optional fold-after multiplier (Sec. III-B), one fp32 rounding per element -------
+  if (p.post_mult) {
+#pragma unroll
+    for (int c = 0; c < CPT; ++c)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v1[c][4 * i] = v1[c][4 * i] * pm[c][i].x;
+        v1[c][4 * i + 1] = v1[c][4 * i + 1] * pm[c][i].y;
+        v1[c][4 * i + 2] = v1[c][4 * i + 2] * pm[c][i].z;
+        v1[c][4 * i + 3] = v1[c][4 * i + 3] * pm[c][i].w;
+      }
+  }
 
   // ---- row absmax: own chunks, then the row's lanes, then the row's waves ---------------
   float amax = 0.0f;
@@ -335,7 +354,7 @@ static hipError_t launch_t(const QuantParams &p, int log2b, const QuantShape &q,
 }
 
 hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const float *chan_mult,
-                             int64_t M, int K, int b, int bits, float clip_ratio, float cb,
+                             const float *post_mult, int64_t M, int K, int b, int bits, float clip_ratio, float cb,
                              uint8_t *codes, int64_t ld_codes, float *delta, int out_fmt,
                              hipStream_t s) {
   if (M <= 0) return hipSuccess;
@@ -351,6 +370,7 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
   p.x = x;
   p.ldx = ldx;
   p.chan_mult = chan_mult;
+  p.post_mult = post_mult;
   p.M = M;
   p.K = K;
   p.bits = bits;

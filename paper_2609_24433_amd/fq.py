@@ -37,13 +37,13 @@ def _load() -> ctypes.CDLL:
     lib = ctypes.CDLL(LIB_PATH)
     vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     sig = {
-        "fq_fwht_quant": [vp, i64, vp, i64, i64, i32, i32, f32, vp, vp, vp],
-        "fq_quantize_weights": [vp, i64, vp, i64, i64, i32, i32, vp, vp, vp],
+        "fq_fwht_quant": [vp, i64, vp, vp, i64, i64, i32, i32, f32, vp, vp, vp],
+        "fq_quantize_weights": [vp, i64, vp, vp, i64, i64, i32, i32, vp, vp, vp],
         "fq_pack_weights": [vp, i64, i64, i32, vp, vp],
         "fq_unpack_weights": [vp, i64, i64, i32, vp, vp],
         "fq_gemm_w4a4": [vp, vp, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
         "fq_gemm_w8a8": [vp, vp, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
-        "fq_linear": [vp, i64, vp, i64, i64, i64, i32, i32, f32, vp, vp, vp, vp, i64, vp, sz, vp],
+        "fq_linear": [vp, i64, vp, vp, i64, i64, i64, i32, i32, f32, vp, vp, vp, vp, i64, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -81,8 +81,9 @@ def _stream(stream: Optional[torch.cuda.Stream] = None):
 
 # ---------------------------------------------------------------- raw C-ABI calls (pointers)
 
-def fwht_quant_raw(x_ptr, ldx, smooth_ptr, M, K, b, bits, clip_ratio, codes_ptr, delta_ptr, stream_ptr):
-    _check(LIB.fq_fwht_quant(x_ptr, ldx, smooth_ptr, M, K, b, bits, clip_ratio, codes_ptr, delta_ptr,
+def fwht_quant_raw(x_ptr, ldx, smooth_ptr, M, K, b, bits, clip_ratio, codes_ptr, delta_ptr, stream_ptr,
+                   post_ptr=None):
+    _check(LIB.fq_fwht_quant(x_ptr, ldx, smooth_ptr, post_ptr, M, K, b, bits, clip_ratio, codes_ptr, delta_ptr,
                              stream_ptr))
 
 
@@ -94,26 +95,29 @@ def code_bytes(K: int, bits: int) -> int:
 
 def fwht_quant(x: torch.Tensor, b: int, bits: int, clip_ratio: float = 1.0,
                smooth_inv: Optional[torch.Tensor] = None, out_codes: Optional[torch.Tensor] = None,
-               out_delta: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Prologue: x bf16 [M, K] (row stride x.stride(0)) -> (codes uint8 [M, K*bits/8], delta fp32 [M])."""
+               out_delta: Optional[torch.Tensor] = None,
+               post_inv: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Prologue: x bf16 [M, K] (row stride x.stride(0)) -> (codes uint8 [M, K*bits/8], delta fp32 [M]).
+    smooth_inv: fold-before S^-1 (before the rotation); post_inv: fold-after P^-1 (after it)."""
     M, K = x.shape
     assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
     codes = out_codes if out_codes is not None else torch.empty((M, code_bytes(K, bits)), dtype=torch.uint8, device=x.device)
     delta = out_delta if out_delta is not None else torch.empty((M,), dtype=torch.float32, device=x.device)
-    _check(LIB.fq_fwht_quant(_p(x), x.stride(0) if M else K, _p(smooth_inv), M, K, b, bits, clip_ratio, _p(codes),
-                             _p(delta), _stream()))
+    _check(LIB.fq_fwht_quant(_p(x), x.stride(0) if M else K, _p(smooth_inv), _p(post_inv), M, K, b, bits,
+                             clip_ratio, _p(codes), _p(delta), _stream()))
     return codes, delta
 
 
-def quantize_weights(w: torch.Tensor, b: int, bits: int,
-                     col_scale: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Offline fold + RTN: w fp32 [N, K] -> (codes int8 [N, K], scales fp32 [N])."""
+def quantize_weights(w: torch.Tensor, b: int, bits: int, col_scale: Optional[torch.Tensor] = None,
+                     post_scale: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Offline fold + RTN: w fp32 [N, K] -> (codes int8 [N, K], scales fp32 [N]).
+    col_scale: fold-before S (before the rotation); post_scale: fold-after P (after it)."""
     N, K = w.shape
     assert w.dtype == torch.float32 and w.stride(1) == 1
     codes = torch.empty((N, K), dtype=torch.int8, device=w.device)
     scale = torch.empty((N,), dtype=torch.float32, device=w.device)
-    _check(LIB.fq_quantize_weights(_p(w), w.stride(0), _p(col_scale), N, K, b, bits, _p(codes), _p(scale),
-                                   _stream()))
+    _check(LIB.fq_quantize_weights(_p(w), w.stride(0), _p(col_scale), _p(post_scale), N, K, b, bits, _p(codes),
+                                   _p(scale), _stream()))
     return codes, scale
 
 
@@ -166,15 +170,16 @@ def gemm(a_codes: torch.Tensor, delta: torch.Tensor, w_packed: torch.Tensor, w_s
 def linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: int, b: int, bits: int,
            clip_ratio: float = 1.0, smooth_inv: Optional[torch.Tensor] = None,
            bias: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
-           out: Optional[torch.Tensor] = None) -> torch.Tensor:
+           out: Optional[torch.Tensor] = None, post_inv: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Fused projection: bf16 x [M, K] -> bf16 y [M, N]."""
     M, K = x.shape
     assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
     if ws is None:
         ws = workspace(linear_workspace_bytes(M, N, K, bits), x.device)
-    _check(LIB.fq_linear(_p(x), x.stride(0) if M else K, _p(smooth_inv), M, K, N, b, bits, clip_ratio, _p(w_packed),
-                         _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N, _p(ws), ws.numel(), _stream()))
+    _check(LIB.fq_linear(_p(x), x.stride(0) if M else K, _p(smooth_inv), _p(post_inv), M, K, N, b, bits, clip_ratio,
+                         _p(w_packed), _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N, _p(ws), ws.numel(),
+                         _stream()))
     return y
 
 
@@ -182,14 +187,15 @@ class QuantLinear:
     """One consumer projection: folded, rounded and packed weights kept resident on the device."""
 
     def __init__(self, w: torch.Tensor, b: int, bits: int, col_scale: Optional[torch.Tensor] = None,
-                 bias: Optional[torch.Tensor] = None):
+                 bias: Optional[torch.Tensor] = None, post_scale: Optional[torch.Tensor] = None):
         self.N, self.K = w.shape
         self.b, self.bits = b, bits
-        codes, self.w_scale = quantize_weights(w, b, bits, col_scale)
+        codes, self.w_scale = quantize_weights(w, b, bits, col_scale, post_scale)
         self.w_packed = pack_weights(codes, bits)
         self.bias = bias
 
     def __call__(self, x: torch.Tensor, clip_ratio: float = 1.0, smooth_inv: Optional[torch.Tensor] = None,
-                 ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+                 ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                 post_inv: Optional[torch.Tensor] = None) -> torch.Tensor:
         return linear(x, self.w_packed, self.w_scale, self.N, self.b, self.bits, clip_ratio, smooth_inv,
-                      self.bias, ws, out)
+                      self.bias, ws, out, post_inv)

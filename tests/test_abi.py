@@ -49,8 +49,9 @@ def test_sizes():
         assert fq.gemm_workspace_bytes(M, 2048, 16384, 4) % 256 == 0
 
 
-def call_quant(x=FAKE, ldx=1024, smooth=NULL, M=4, K=1024, b=64, bits=4, r=1.0, codes=FAKE, delta=FAKE):
-    return fq.LIB.fq_fwht_quant(x, ldx, smooth, M, K, b, bits, r, codes, delta, None)
+def call_quant(x=FAKE, ldx=1024, smooth=NULL, M=4, K=1024, b=64, bits=4, r=1.0, codes=FAKE, delta=FAKE,
+               post=NULL):
+    return fq.LIB.fq_fwht_quant(x, ldx, smooth, post, M, K, b, bits, r, codes, delta, None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -60,7 +61,7 @@ def call_quant(x=FAKE, ldx=1024, smooth=NULL, M=4, K=1024, b=64, bits=4, r=1.0, 
     (dict(b=3), 3), (dict(b=512), 3), (dict(b=0), 3), (dict(bits=2), 3), (dict(bits=16), 3),
     (dict(r=0.0), 3), (dict(r=1.5), 3), (dict(r=float("nan")), 3),
     (dict(x=MISALIGNED), 4), (dict(codes=MISALIGNED), 4), (dict(ldx=1028), 4),
-    (dict(smooth=MISALIGNED), 4),
+    (dict(smooth=MISALIGNED), 4), (dict(post=MISALIGNED), 4),
 ])
 def test_fwht_quant_rejects(kw, status):
     assert call_quant(**kw) == status
@@ -74,8 +75,8 @@ def test_fwht_quant_k_not_multiple_of_b():
 def test_zero_rows_are_noops():
     assert call_quant(M=0, x=NULL, codes=NULL, delta=NULL) == 0
     assert fq.LIB.fq_gemm_w4a4(NULL, NULL, NULL, NULL, NULL, NULL, 16, NULL, 0, 16, 128, NULL, 0, None) == 0
-    assert fq.LIB.fq_linear(NULL, 1024, NULL, 0, 1024, 256, 64, 4, 1.0, NULL, NULL, NULL, NULL, 256, NULL, 0,
-                            None) == 0
+    assert fq.LIB.fq_linear(NULL, 1024, NULL, NULL, 0, 1024, 256, 64, 4, 1.0, NULL, NULL, NULL, NULL, 256, NULL,
+                            0, None) == 0
 
 
 def call_gemm(bits=4, a=FAKE, delta=FAKE, w=FAKE, sw=FAKE, bias=NULL, y=FAKE, ldy=256, acc=NULL,
@@ -98,15 +99,15 @@ def test_gemm_rejects(bits, kw, status):
 
 
 def call_linear(x=FAKE, ldx=1024, M=50, K=1024, N=256, b=64, bits=4, r=1.0, w=FAKE, sw=FAKE, bias=NULL,
-                y=FAKE, ldy=256, ws=FAKE, ws_bytes=1 << 30, smooth=NULL):
-    return fq.LIB.fq_linear(x, ldx, smooth, M, K, N, b, bits, r, w, sw, bias, y, ldy, ws, ws_bytes, None)
+                y=FAKE, ldy=256, ws=FAKE, ws_bytes=1 << 30, smooth=NULL, post=NULL):
+    return fq.LIB.fq_linear(x, ldx, smooth, post, M, K, N, b, bits, r, w, sw, bias, y, ldy, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(x=NULL), 1), (dict(w=NULL), 1), (dict(y=NULL), 1), (dict(sw=NULL), 1),
     (dict(ldx=512), 2), (dict(ldy=100), 2), (dict(b=5), 3), (dict(bits=6), 3), (dict(N=40, ldy=40), 3),
     (dict(r=-1.0), 3), (dict(ws=NULL, ws_bytes=0), 5), (dict(ws_bytes=100), 5), (dict(ws=MISALIGNED), 4),
-    (dict(smooth=MISALIGNED), 4),
+    (dict(smooth=MISALIGNED), 4), (dict(post=MISALIGNED), 4),
 ])
 def test_linear_rejects(kw, status):
     assert call_linear(**kw) == status
@@ -126,7 +127,8 @@ def test_pack_rejects(fn):
 
 def test_quantize_weights_rejects():
     f = fq.LIB.fq_quantize_weights
-    assert f(NULL, 128, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 1
-    assert f(FAKE, 130, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 4
-    assert f(FAKE, 64, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 2
-    assert f(FAKE, 128, NULL, 16, 128, 64, 7, FAKE, FAKE, None) == 3
+    assert f(NULL, 128, NULL, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 1
+    assert f(FAKE, 130, NULL, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 4
+    assert f(FAKE, 64, NULL, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 2
+    assert f(FAKE, 128, NULL, NULL, 16, 128, 64, 7, FAKE, FAKE, None) == 3
+    assert f(FAKE, 128, NULL, MISALIGNED, 16, 128, 64, 4, FAKE, FAKE, None) == 4

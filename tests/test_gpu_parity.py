@@ -89,6 +89,26 @@ def test_fwht_quant_fold_before_multiplier(b, bits):
     np.testing.assert_array_equal(delta.cpu().numpy(), d_ref)
 
 
+@pytest.mark.parametrize("b,bits,M,K", [(64, 4, 33, 2048), (128, 8, 33, 2048), (256, 4, 5, 16384),
+                                         (128, 4, 50, 4096), (16, 8, 70, 384)])
+def test_fwht_quant_fold_after_multiplier(b, bits, M, K):
+    # Sec. III-B fold-after: P^-1 after the rotation, bit-exact (alone and with S^-1 before it)
+    flush(f"fwht_quant post b={b} bits={bits} M={M} K={K}")
+    x = synth.activations(M, K, seed=79, outlier_frac=0.01, outlier_scale=30.0)
+    p_inv = synth.channel_vector(K, seed=80, low=0.2, high=3.0)
+    s_inv = synth.channel_vector(K, seed=81, low=0.5, high=2.0)
+    pd, sd = torch.from_numpy(p_inv).to(DEV), torch.from_numpy(s_inv).to(DEV)
+    codes, delta = fq().fwht_quant(x.to(DEV), b, bits, 1.0, post_inv=pd)
+    codes2, delta2 = fq().fwht_quant(x.to(DEV), b, bits, 0.9, sd, post_inv=pd)
+    torch.cuda.synchronize()
+    c_ref, d_ref = oracle.fwht_quant(x, b, bits, 1.0, None, p_inv)
+    np.testing.assert_array_equal(codes.cpu().numpy(), canonical_codes(c_ref, bits))
+    np.testing.assert_array_equal(delta.cpu().numpy(), d_ref)
+    c_ref2, d_ref2 = oracle.fwht_quant(x, b, bits, 0.9, s_inv, p_inv)
+    np.testing.assert_array_equal(codes2.cpu().numpy(), canonical_codes(c_ref2, bits))
+    np.testing.assert_array_equal(delta2.cpu().numpy(), d_ref2)
+
+
 # ------------------------------------------------------------------ offline weights
 
 @pytest.mark.parametrize("N,K,b,bits,scaled", [(64, 1024, 64, 4, False), (48, 2048, 128, 8, True),
@@ -103,6 +123,19 @@ def test_quantize_weights_bit_exact(N, K, b, bits, scaled):
                                          None if cs is None else torch.from_numpy(cs).to(DEV))
     torch.cuda.synchronize()
     c_ref, s_ref = oracle.quantize_weights(w, b, bits, cs)
+    np.testing.assert_array_equal(codes.cpu().numpy(), c_ref)
+    np.testing.assert_array_equal(scale.cpu().numpy(), s_ref)
+
+
+@pytest.mark.parametrize("N,K,b,bits", [(64, 1024, 64, 4), (48, 2048, 128, 8), (32, 16384, 256, 4)])
+def test_quantize_weights_fold_after_bit_exact(N, K, b, bits):
+    flush(f"quantize_weights post N={N} K={K} b={b} bits={bits}")
+    w = synth.weights(N, K, seed=N + K + 1)
+    w[2] = 0.0
+    pv = synth.channel_vector(K, seed=6, low=0.5, high=1.5)
+    codes, scale = fq().quantize_weights(torch.from_numpy(w).to(DEV), b, bits, None, torch.from_numpy(pv).to(DEV))
+    torch.cuda.synchronize()
+    c_ref, s_ref = oracle.quantize_weights(w, b, bits, None, pv)
     np.testing.assert_array_equal(codes.cpu().numpy(), c_ref)
     np.testing.assert_array_equal(scale.cpu().numpy(), s_ref)
 
@@ -219,4 +252,25 @@ def test_linear_clip_and_smoothing():
     torch.cuda.synchronize()
     wc, s_w = oracle.quantize_weights(w, b, bits, s)
     _, _, _, y_ref = oracle.linear(x, wc, s_w, b, bits, clip_ratio=0.9, smooth_inv=s_inv)
+    assert_bf16_close(y, y_ref)
+
+
+@pytest.mark.parametrize("M,K,N,bits", [(50, 1024, 1536, 4), (24, 2048, 512, 8), (200, 2048, 384, 4)])
+def test_linear_fold_after(M, K, N, bits):
+    """Fold-after preset end to end: weights W R^T P rounded on the GPU, tokens P^-1 R x."""
+    flush(f"linear fold-after M={M} K={K} N={N} bits={bits}")
+    f = fq()
+    b = 128
+    x = synth.activations(M, K, seed=12, outlier_frac=0.01, outlier_scale=30.0)
+    w = synth.weights(N, K, seed=13)
+    pv = synth.channel_vector(K, seed=14, low=0.5, high=2.0)
+    p_inv = (1.0 / pv).astype(np.float32)
+    lin = f.QuantLinear(torch.from_numpy(w).to(DEV), b, bits, post_scale=torch.from_numpy(pv).to(DEV))
+    ws = f.workspace(f.linear_workspace_bytes(M, N, K, bits), DEV)
+    y = lin(x.to(DEV), ws=ws, post_inv=torch.from_numpy(p_inv).to(DEV))
+    torch.cuda.synchronize()
+    wc, s_w = oracle.quantize_weights(w, b, bits, None, pv)
+    np.testing.assert_array_equal(lin.w_scale.cpu().numpy(), s_w)
+    np.testing.assert_array_equal(f.unpack_weights(lin.w_packed, N, K, bits).cpu().numpy(), wc)
+    _, _, _, y_ref = oracle.linear(x, wc, s_w, b, bits, post_inv=p_inv)
     assert_bf16_close(y, y_ref)
