@@ -39,6 +39,7 @@ def _lib():
         lib.fqo_pack_int4.argtypes = [vp, i64, i64, vp]
         lib.fqo_gemm_i64.argtypes = [vp, vp, i64, i64, i64, vp]
         lib.fqo_dequant.argtypes = [vp, vp, vp, vp, i64, i64, vp]
+        lib.fqo_w4a16.argtypes = [vp, i64, vp, vp, vp, i64, i64, i64, vp, vp]
         lib.fqo_fwht_block_f32.argtypes = [vp, i64]
         lib.fqo_fwht_block_f32.restype = None
         lib.fqo_inv_sqrt_b.argtypes = [i64]
@@ -47,7 +48,7 @@ def _lib():
         lib.fqo_set_threads.argtypes = [i32]
         lib.fqo_set_threads.restype = None
         for name in ("fqo_fwht_quant_bf16", "fqo_fwht_quant_f32", "fqo_pack_int4", "fqo_gemm_i64",
-                     "fqo_dequant"):
+                     "fqo_dequant", "fqo_w4a16"):
             getattr(lib, name).restype = i32
         _LIB = lib
     return _LIB
@@ -165,6 +166,27 @@ def dequant(acc: np.ndarray, delta: np.ndarray, s_w: np.ndarray,
     bb = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
     _check(_lib().fqo_dequant(_ptr(acc), _ptr(d), _ptr(s), _ptr(bb), M, N, _ptr(y)), "dequant")
     return y
+
+
+def w4a16(x, w_codes: np.ndarray, s_w: np.ndarray,
+          bias: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Weight-only INT4 projection (Sec. III-A, the adaptive layer-norm modulation path):
+    bf16 tokens x [M, K] (torch tensor or uint16 bits) times INT4 weight codes [N, K] with
+    per-output-channel scales.  Returns (acc, y) in float64: acc = x q^T, y = s_w acc + bias."""
+    lib = _lib()
+    if not isinstance(x, np.ndarray):
+        x = bf16_bits(x)
+    xx = np.ascontiguousarray(x, dtype=np.uint16)
+    M, K = xx.shape
+    qw = np.ascontiguousarray(w_codes, dtype=np.int8)
+    N, K2 = qw.shape
+    assert K == K2
+    acc = np.zeros((M, N), dtype=np.float64)
+    y = np.zeros((M, N), dtype=np.float64)
+    s = np.ascontiguousarray(s_w, dtype=np.float32)
+    bb = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    _check(lib.fqo_w4a16(_ptr(xx), K, _ptr(qw), _ptr(s), _ptr(bb), M, N, K, _ptr(acc), _ptr(y)), "w4a16")
+    return acc, y
 
 
 def linear(x, w_codes: np.ndarray, s_w: np.ndarray, b: int, bits: int,

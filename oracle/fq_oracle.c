@@ -198,3 +198,25 @@ int fqo_dequant(const int64_t *acc, const float *delta, const float *s_w, const 
         }
     return FQO_OK;
 }
+
+/* Weight-only INT4 projection: the paper keeps GR00T's adaptive layer-norm modulation
+ * at floating-point activations times INT4 weights (Sec. III-A).  The weights are
+ * rounded per output channel (codes q, scales s); the activations stay bf16 and are
+ * not quantized.  acc[t, j] = sum_c x[t, c] * q[j, c] and y[t, j] = s_j acc[t, j] + b_j,
+ * both in double (every product of a bf16 and a small integer is exact in double). */
+int fqo_w4a16(const uint16_t *x, int64_t ldx, const int8_t *qw, const float *s_w,
+              const float *bias, int64_t M, int64_t N, int64_t K, double *acc, double *y) {
+    if (M < 0 || N < 0 || K < 1 || ldx < K) return FQO_BAD_ARG;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < M; ++t)
+        for (int64_t j = 0; j < N; ++j) {
+            double a = 0.0;
+            for (int64_t c = 0; c < K; ++c)
+                a += (double)bf16_bits_to_float(x[t * ldx + c]) * (double)qw[j * K + c];
+            acc[t * N + j] = a;
+            double v = (double)s_w[j] * a;
+            if (bias) v += (double)bias[j];
+            y[t * N + j] = v;
+        }
+    return FQO_OK;
+}

@@ -373,3 +373,26 @@ def test_quantized_projection_tracks_float_projection(bits):
     ref = x.double().numpy() @ W.astype(np.float64).T
     cos = (y * ref).sum() / np.linalg.norm(y) / np.linalg.norm(ref)
     assert cos > (0.97 if bits == 4 else 0.9995)
+
+
+# --- weight-only INT4 projection (Sec. III-A, adaptive layer-norm modulation) ------------------
+
+def test_w4a16_matches_numpy_float64_and_special_cases():
+    x = synth.activations(7, 256, seed=70, outlier_frac=0.02, outlier_scale=30.0)
+    W = synth.weights(48, 256, seed=71)
+    q, s_w = oracle.quantize_weights(W, 1, 4)  # per-output-channel RTN, no rotation
+    bias = synth.channel_vector(48, seed=72, low=-0.5, high=0.5)
+    acc, y = oracle.w4a16(x, q, s_w, bias)
+    xf = x.float().numpy().astype(np.float64)
+    np.testing.assert_allclose(acc, xf @ q.astype(np.float64).T, rtol=1e-12, atol=1e-9)
+    np.testing.assert_allclose(y, acc * s_w.astype(np.float64) + bias, rtol=1e-12, atol=1e-12)
+    # one-hot tokens read single weight columns exactly; a zero token gives the bias
+    e = torch.zeros(3, 256, dtype=torch.bfloat16)
+    e[0, 5] = 1.0
+    e[1, 200] = -2.0
+    acc1, y1 = oracle.w4a16(e, q, s_w, bias)
+    np.testing.assert_array_equal(acc1[0], q[:, 5].astype(np.float64))
+    np.testing.assert_array_equal(acc1[1], -2.0 * q[:, 200].astype(np.float64))
+    np.testing.assert_array_equal(y1[2], bias.astype(np.float64))
+    # the weights' integer codes stay on the -7..7 grid of eq. (5) at b = 1
+    assert np.abs(q).max() == 7
