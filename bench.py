@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0    # MI355X dense INT8 MFMA, TOPS (no INT4 MFMA on gfx950)
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s (the W4A16 path)
 
 
 def parse():
@@ -260,6 +261,10 @@ def measure_points(torch, fq, synth, dev, log_fn):
             ws = fq.workspace(fq.linear_workspace_bytes(M, N, K, bits), dev)
             call = lambda i: fq.linear(x, wp[i % copies], lin.w_scale, N, b, bits, ws=ws, out=y)
             nbytes = linear_bytes(M, N, K, bits)
+        elif kind == "w4a16":
+            ws = fq.workspace(fq.w4a16_workspace_bytes(M, N, K), dev)
+            call = lambda i: fq.gemm_w4a16(x, wp[i % copies], lin.w_scale, N, ws=ws, out=y)
+            nbytes = linear_bytes(M, N, K, 4)
         else:
             ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
             call = lambda i: fq.gemm(codes, delta, wp[i % copies], lin.w_scale, N, K, bits, ws=ws, out=y)
@@ -268,7 +273,7 @@ def measure_points(torch, fq, synth, dev, log_fn):
         us = time_graph(torch, g, max(1, 200 // copies)) / copies * 1e6
         ops = 2.0 * M * N * K
         t_hbm = nbytes / HBM_PEAK_GBS / 1e3
-        t_mfma = ops / INT8_PEAK_TOPS / 1e6
+        t_mfma = ops / (BF16_PEAK_TFLOPS if kind == "w4a16" else INT8_PEAK_TOPS) / 1e6
         rec = {"name": name, "kind": kind, "M": M, "K": K, "N": N, "b": b, "bits": bits,
                "us": round(us, 3), "TOPS": round(ops / us / 1e6, 2), "GBps": round(nbytes / us / 1e3, 1),
                "bound": "hbm" if t_hbm >= t_mfma else "mfma",
@@ -286,6 +291,10 @@ def measure_points(torch, fq, synth, dev, log_fn):
     run_point("down_w4a4_m816_gemm", 816, 16384, 2048, 128, 4, "gemm")
     run_point("down_w8a8_m816_linear", 816, 16384, 2048, 128, 8, "linear")
     run_point("down_w4a4_m4096_gemm", 4096, 16384, 2048, 128, 4, "gemm")
+    # weight-only INT4 (adaptive layer-norm modulation path): b = 1, no rotation
+    run_point("adaln_w4a16_m1", 1, 1024, 6144, 1, 4, "w4a16")
+    run_point("down_w4a16_m1", 1, 16384, 2048, 1, 4, "w4a16")
+    run_point("down_w4a16_m16", 16, 16384, 2048, 1, 4, "w4a16")
     return out
 
 

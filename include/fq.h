@@ -122,6 +122,24 @@ fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_pa
                        int32_t *acc_out, int64_t M, int64_t N, int64_t K, void *ws,
                        size_t ws_bytes, void *stream);
 
+/* Weight-only INT4 projection (W4A16): the paper runs GR00T's adaptive layer-norm
+ * modulation with floating-point activations and INT4 weights (Sec. III-A).
+ *   x_bf16    [M, ldx] bf16 activations, not quantized (ldx >= K, multiple of 8).
+ *   w_packed  INT4 weights from fq_pack_weights(bits = 4), rounded per output channel,
+ *             typically with fq_quantize_weights at b = 1 (no rotation); w_scale fp32 [N].
+ *   y_bf16    [M, ldy] bf16: y = bf16_rne(fp32(sum_c x_tc q_jc) * w_scale[j] + bias[j]).
+ *   acc_out   fp32 [M, N] sums before the scale, or NULL (for verification).
+ *   ws        scratch of fq_gemm_w4a16_workspace_bytes(M, N, K) bytes (fp32 partial sums
+ *             of a split K; 0 bytes and NULL allowed when K is not split).
+ * The sums are floating point on the bf16 matrix cores (every product of a bf16 and a
+ * code is exact in fp32; the additions round), so they agree with an exact sum within
+ * (K - 1) 2^-24 sum_c |x_tc q_jc|, not bit for bit.  Same shape limits as the other
+ * entry points. */
+size_t fq_gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
+fq_status fq_gemm_w4a16(const void *x_bf16, int64_t ldx, const void *w_packed, const float *w_scale,
+                        const float *bias, void *y_bf16, int64_t ldy, float *acc_out, int64_t M,
+                        int64_t N, int64_t K, void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace bytes fq_linear needs: the intermediate activation codes and scales, and the
  * split-K partial sums.  Scratch with no initialization requirement. */
 size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);

@@ -255,6 +255,42 @@ fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_pa
                     ws_bytes, stream);
 }
 
+size_t fq_gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || K < 128) return 0;
+  return fq::plan_w4a16(M, N, K).partial_bytes;
+}
+
+fq_status fq_gemm_w4a16(const void *x_bf16, int64_t ldx, const void *w_packed, const float *w_scale,
+                        const float *bias, void *y_bf16, int64_t ldy, float *acc_out, int64_t M,
+                        int64_t N, int64_t K, void *ws, size_t ws_bytes, void *stream) {
+  fq_status s = check_gemm(x_bf16, w_scale, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K);
+  if (s != FQ_OK) return s;
+  if (ldx < K) return fail(FQ_ERR_SHAPE, "leading dimension %lld < K=%lld", (long long)ldx, (long long)K);
+  if (ldx % 8) return fail(FQ_ERR_ALIGN, "leading dimension %lld is not a multiple of 8", (long long)ldx);
+  if (M == 0 || N == 0) return ok();
+  if (acc_out && !aligned16(acc_out)) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  const fq::W16Plan pl = fq::plan_w4a16(M, N, K);
+  if (pl.partial_bytes > 0 && (!ws || ws_bytes < pl.partial_bytes))
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", pl.partial_bytes,
+                ws ? ws_bytes : (size_t)0);
+  if (pl.partial_bytes > 0 && !aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  fq::W16Args g;
+  g.x = x_bf16;
+  g.ldx = ldx;
+  g.w = static_cast<const uint8_t *>(w_packed);
+  g.w_scale = w_scale;
+  g.bias = bias;
+  g.y = static_cast<uint16_t *>(y_bf16);
+  g.ldy = ldy;
+  g.acc_out = acc_out;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  hipError_t e = fq::launch_w4a16(g, pl, ws, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "w4a16 launch");
+  return ok();
+}
+
 // fq_linear workspace: [codes (nibbles for W4A4, int8 for W8A8)][delta][split-K partials]
 size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
   if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;

@@ -1103,4 +1103,235 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStrea
   return launch_gemm_t<8, kAInt8>(p, pl, s);
 }
 
+// ----------------------------------------------------------------------------------------
+// Weight-only INT4 projection (W4A16): bf16 activations times the packed INT4 weight
+// tiles, y = bf16_rne(s_j sum_c x_tc q_jc + b_j), the sum in fp32 on the bf16 matrix cores
+// (v_mfma_f32_16x16x32_bf16).  The paper runs GR00T's adaptive layer-norm modulation this
+// way (Sec. III-A).  Same streaming design as the W4A4 kernel: a workgroup owns one
+// 16-channel weight tile column, a block of MT 16-row tiles and a K slice split between 4
+// wave groups; the bf16 activation slice goes to LDS first (swizzled direct-to-LDS
+// loads), the weight tiles follow in k order, and each k step's MFMAs start when its tile
+// lands.  A weight nibble becomes a bf16 exactly: sign-extending bit-field extract,
+// int -> fp32 (|code| <= 8), the fp32's upper half.  MFMA c of a 128-wide k step takes,
+// from lane group g, channels 32 g + 8 c + [0, 8): the lane's own weight bytes 4c..4c+3 and
+// the matching 16 bytes of the activation row, so both operands use one k order.
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+struct W16Params {
+  const uint8_t *x;      // bf16 [M, ldx]
+  int64_t ldx;           // elements
+  const uint8_t *w;      // packed INT4 tiles
+  const float *w_scale;  // [N]
+  const float *bias;     // [N] or NULL
+  uint16_t *y;           // bf16 [M, ldy]
+  int64_t ldy;
+  float *acc_out;        // fp32 [M, N] or NULL
+  float *partial;        // fp32 [splits][M][N] when K is split
+  int M, N, K;
+};
+
+// 8 nibble codes (channels 2i in the low, 2i + 1 in the high nibble of byte i) -> 8 bf16
+// in channel order.
+__device__ __forceinline__ bf16x8 nibbles_to_bf16(uint32_t w) {
+  uint32_t r[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float e = (float)((int32_t)(w << (28 - 8 * i)) >> 28);
+    const float o = (float)((int32_t)(w << (24 - 8 * i)) >> 28);
+    r[i] = __builtin_amdgcn_perm(__float_as_uint(o), __float_as_uint(e), 0x07060302u);
+  }
+  const uint4 v = make_uint4(r[0], r[1], r[2], r[3]);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int MT, int KT>
+__global__ __launch_bounds__(256) void w4a16_stream_kernel(W16Params p) {
+  constexpr int WK = 4;
+  constexpr int AROW = WK * KT * 256;  // bf16 bytes per row of the slice (128 channels per step)
+  constexpr int ROWS = MT * 16;
+  constexpr int CPR = AROW / 16;
+  constexpr int SLICE_KB = ROWS * AROW / 1024;
+  constexpr int IA = SLICE_KB / WK;
+  static_assert(ROWS * AROW % (1024 * WK) == 0, "slice must split into whole KBs per wave");
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int kg = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ntile = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
+  const int m0 = blockIdx.z * ROWS;
+  const int mz = min(ROWS, p.M - m0);
+  const int ktot = p.K / kTileK;
+  const int slice_begin = split * WK * KT;
+  const int ks_begin = slice_begin + kg * KT;
+  const int nk = max(0, min(KT, ktot - ks_begin));
+
+  // 1. bf16 activation slice -> LDS
+  {
+    const uint8_t *abase = p.x + ((int64_t)m0 * p.ldx + (int64_t)slice_begin * kTileK) * 2;
+    const int valid_cols = min(WK * KT, ktot - slice_begin) * (kTileK * 2 / 16);
+    if (valid_cols == CPR)
+      stage_slice<AROW, IA, SLICE_KB, true>(abase, p.ldx * 2, mz, kg, lane, valid_cols, lds);
+    else
+      stage_slice<AROW, IA, SLICE_KB, false>(abase, p.ldx * 2, mz, kg, lane, valid_cols, lds);
+  }
+  // 2. this wave's weight tiles, in k order, unconditionally (clamped past the end of K)
+  sched_wall();
+  uint4 wreg[KT];
+  const uint8_t *wtile = p.w + (int64_t)ntile * ktot * tile_bytes(4) + lane * lane_bytes(4);
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt)
+    wreg[kt] = *reinterpret_cast<const uint4 *>(wtile + (int64_t)min(ks_begin + kt, ktot - 1) * tile_bytes(4));
+  sched_wall();
+  wait_vmcnt<KT>();
+  lds_barrier();
+
+  // 3. MFMAs: per k step, 4 chunks of 32 channels, MT row tiles each
+  v4f acc[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) acc[i] = v4f{0.f, 0.f, 0.f, 0.f};
+  const int r16 = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt) {
+    if (kt < nk) {
+      const uint32_t wd[4] = {wreg[kt].x, wreg[kt].y, wreg[kt].z, wreg[kt].w};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const bf16x8 b = nibbles_to_bf16(wd[c]);
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+          const int row = i * 16 + r16;
+          const int chunk = (kg * KT + kt) * 16 + 4 * g + c;
+          const uint4 av = *reinterpret_cast<const uint4 *>(lds + row * AROW + ((chunk ^ slice_swizzle<AROW>(row)) * 16));
+          acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), b, acc[i], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // 4. wave groups add up through LDS (fixed order); group kg finishes row tiles kg mod 4
+  __syncthreads();  // the slice is no longer read
+  v4f *red = reinterpret_cast<v4f *>(lds);
+#pragma unroll
+  for (int i = 0; i < MT; ++i) red[(kg * MT + i) * 64 + lane] = acc[i];
+  __syncthreads();
+  const int n = ntile * 16 + r16;
+  const float sw = p.w_scale[n];
+  const float bj = p.bias ? p.bias[n] : 0.0f;
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    if (i % WK != kg) continue;
+    v4f t = red[i * 64 + lane];
+#pragma unroll
+    for (int g2 = 1; g2 < WK; ++g2) t += red[(g2 * MT + i) * 64 + lane];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + i * 16 + 4 * g + r;
+      if (m >= p.M) continue;
+      if (nsplit > 1) {
+        p.partial[((int64_t)split * p.M + m) * p.N + n] = t[r];
+      } else {
+        if (p.acc_out) p.acc_out[(int64_t)m * p.N + n] = t[r];
+        p.y[(int64_t)m * p.ldy + n] = (uint16_t)f32_to_bf16(t[r] * sw + bj);
+      }
+    }
+  }
+}
+
+// Adds the fp32 K slices in fixed order and applies the scale and bias; 4 columns per thread.
+__global__ __launch_bounds__(256) void w4a16_splitk_epilogue_kernel(W16Params p, int slices) {
+  const int cpr = p.N / 4;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)p.M * cpr) return;
+  const int m = (int)(idx / cpr), n = (int)(idx % cpr) * 4;
+  const float4 sw = *reinterpret_cast<const float4 *>(p.w_scale + n);
+  const float4 bj = p.bias ? *reinterpret_cast<const float4 *>(p.bias + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+  const float4 *src = reinterpret_cast<const float4 *>(p.partial + (int64_t)m * p.N + n);
+  const int64_t zs = (int64_t)p.M * p.N / 4;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int z0 = 0; z0 < slices; z0 += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int z = 0; z < 8; ++z)
+      if (z0 + z < slices) v[z] = src[(z0 + z) * zs];
+#pragma unroll
+    for (int z = 0; z < 8; ++z)
+      if (z0 + z < slices) {
+        a.x += v[z].x; a.y += v[z].y; a.z += v[z].z; a.w += v[z].w;
+      }
+  }
+  if (p.acc_out) *reinterpret_cast<float4 *>(p.acc_out + (int64_t)m * p.N + n) = a;
+  const uint32_t o0 = f32_to_bf16(a.x * sw.x + bj.x) | (f32_to_bf16(a.y * sw.y + bj.y) << 16);
+  const uint32_t o1 = f32_to_bf16(a.z * sw.z + bj.z) | (f32_to_bf16(a.w * sw.w + bj.w) << 16);
+  *reinterpret_cast<uint2 *>(p.y + (int64_t)m * p.ldy + n) = make_uint2(o0, o1);
+}
+
+W16Plan plan_w4a16(int64_t M, int64_t N, int64_t K) {
+  W16Plan pl{};
+  const int ktot = (int)(K / kTileK);
+  pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  const int smax = 32 / pl.mt;  // k steps per slice that fit 128 KB of LDS for 16 mt rows
+  const int per = ktot < smax ? ktot : smax;
+  pl.kt = per <= 4 ? 1 : (per <= 8 ? 2 : (per <= 16 ? 4 : 8));
+  pl.splits = (ktot + 4 * pl.kt - 1) / (4 * pl.kt);
+  pl.tiles = N / 16;
+  pl.rb = (int)((M + 16 * pl.mt - 1) / (16 * pl.mt));
+  pl.partial_bytes = pl.splits > 1 ? align256((size_t)pl.splits * M * N * 4) : 0;
+  return pl;
+}
+
+template <int MT, int KT>
+static hipError_t launch_w16(const W16Params &p, dim3 grid, hipStream_t s) {
+  constexpr size_t slice = (size_t)MT * 16 * 4 * KT * 256;
+  constexpr size_t red = (size_t)4 * MT * 64 * 16;
+  constexpr size_t lds = slice > red ? slice : red;
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  static bool attr = false;
+  hipError_t e = allow_lds(&w4a16_stream_kernel<MT, KT>, lds, attr);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((w4a16_stream_kernel<MT, KT>), grid, dim3(256), lds, s, p);
+  return hipGetLastError();
+}
+
+template <int MT>
+static hipError_t launch_w16_kt(const W16Params &p, int kt, dim3 grid, hipStream_t s) {
+  switch (kt) {
+    case 1: return launch_w16<MT, 1>(p, grid, s);
+    case 2: return launch_w16<MT, 2>(p, grid, s);
+    case 4: if constexpr (MT <= 2) return launch_w16<MT, 4>(p, grid, s); else return hipErrorInvalidValue;
+    default: if constexpr (MT == 1) return launch_w16<MT, 8>(p, grid, s); else return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_w4a16(const W16Args &g, const W16Plan &pl, void *ws, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  W16Params p;
+  p.x = static_cast<const uint8_t *>(g.x);
+  p.ldx = g.ldx;
+  p.w = g.w;
+  p.w_scale = g.w_scale;
+  p.bias = g.bias;
+  p.y = g.y;
+  p.ldy = g.ldy;
+  p.acc_out = g.acc_out;
+  p.partial = pl.splits > 1 ? reinterpret_cast<float *>(ws) : nullptr;
+  p.M = (int)g.M;
+  p.N = (int)g.N;
+  p.K = (int)g.K;
+  const dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits, (unsigned)pl.rb);
+  hipError_t e;
+  switch (pl.mt) {
+    case 1: e = launch_w16_kt<1>(p, pl.kt, grid, s); break;
+    case 2: e = launch_w16_kt<2>(p, pl.kt, grid, s); break;
+    default: e = launch_w16_kt<4>(p, pl.kt, grid, s); break;
+  }
+  if (e != hipSuccess || pl.splits == 1) return e;
+  const int64_t threads = (int64_t)p.M * (p.N / 4);
+  hipLaunchKernelGGL(w4a16_splitk_epilogue_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, p,
+                     pl.splits);
+  return hipGetLastError();
+}
+
 }  // namespace fq

@@ -63,4 +63,25 @@ struct GemmArgs {
 // ws: at least gemm_plan_workspace(pl) bytes of scratch (no initialization needed)
 hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s);
 
+// Weight-only INT4 (bf16 activations) projection.
+struct W16Plan {
+  int mt, kt;           // 16-row tiles per workgroup, k steps per wave group (4 groups)
+  int splits, rb;       // K slices, row blocks
+  int64_t tiles;        // 16-channel weight tiles
+  size_t partial_bytes; // fp32 partials [splits][M][N] when K is split
+};
+struct W16Args {
+  const void *x;        // bf16 [M, ldx]
+  int64_t ldx;
+  const uint8_t *w;
+  const float *w_scale;
+  const float *bias;
+  uint16_t *y;
+  int64_t ldy;
+  float *acc_out;
+  int64_t M, N, K;
+};
+W16Plan plan_w4a16(int64_t M, int64_t N, int64_t K);
+hipError_t launch_w4a16(const W16Args &g, const W16Plan &pl, void *ws, hipStream_t s);
+
 }  // namespace fq

@@ -21,7 +21,8 @@ _STATUS = {1: "FQ_ERR_NULL", 2: "FQ_ERR_SHAPE", 3: "FQ_ERR_UNSUPPORTED", 4: "FQ_
 
 EXPORTED = ["fq_fwht_quant", "fq_quantize_weights", "fq_packed_weight_bytes", "fq_pack_weights",
             "fq_unpack_weights", "fq_gemm_workspace_bytes", "fq_gemm_w4a4", "fq_gemm_w8a8",
-            "fq_linear_workspace_bytes", "fq_linear", "fq_status_string", "fq_last_error"]
+            "fq_linear_workspace_bytes", "fq_linear", "fq_gemm_w4a16_workspace_bytes", "fq_gemm_w4a16",
+            "fq_status_string", "fq_last_error"]
 
 
 class FQError(RuntimeError):
@@ -44,6 +45,7 @@ def _load() -> ctypes.CDLL:
         "fq_gemm_w4a4": [vp, vp, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
         "fq_gemm_w8a8": [vp, vp, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
         "fq_linear": [vp, i64, vp, vp, i64, i64, i64, i32, i32, f32, vp, vp, vp, vp, i64, vp, sz, vp],
+        "fq_gemm_w4a16": [vp, i64, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -51,7 +53,8 @@ def _load() -> ctypes.CDLL:
         fn.restype = ctypes.c_int
     for name, args in {"fq_packed_weight_bytes": [i64, i64, i32],
                        "fq_gemm_workspace_bytes": [i64, i64, i64, i32],
-                       "fq_linear_workspace_bytes": [i64, i64, i64, i32]}.items():
+                       "fq_linear_workspace_bytes": [i64, i64, i64, i32],
+                       "fq_gemm_w4a16_workspace_bytes": [i64, i64, i64]}.items():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = sz
@@ -181,6 +184,26 @@ def linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: in
                          _p(w_packed), _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N, _p(ws), ws.numel(),
                          _stream()))
     return y
+
+
+def w4a16_workspace_bytes(M: int, N: int, K: int) -> int:
+    return int(LIB.fq_gemm_w4a16_workspace_bytes(M, N, K))
+
+
+def gemm_w4a16(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: int,
+               bias: Optional[torch.Tensor] = None, want_acc: bool = False, ws: Optional[torch.Tensor] = None,
+               out: Optional[torch.Tensor] = None):
+    """Weight-only INT4 projection: bf16 x [M, K] times packed INT4 weights -> bf16 y [M, N]
+    (and the fp32 sums if want_acc)."""
+    M, K = x.shape
+    assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
+    y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    acc = torch.empty((M, N), dtype=torch.float32, device=x.device) if want_acc else None
+    if ws is None:
+        ws = workspace(w4a16_workspace_bytes(M, N, K), x.device)
+    _check(LIB.fq_gemm_w4a16(_p(x), x.stride(0) if M else K, _p(w_packed), _p(w_scale), _p(bias), _p(y),
+                             y.stride(0) if M else N, _p(acc), M, N, K, _p(ws), ws.numel(), _stream()))
+    return (y, acc) if want_acc else y
 
 
 class QuantLinear:

@@ -132,3 +132,26 @@ def test_quantize_weights_rejects():
     assert f(FAKE, 64, NULL, NULL, 16, 128, 64, 4, FAKE, FAKE, None) == 2
     assert f(FAKE, 128, NULL, NULL, 16, 128, 64, 7, FAKE, FAKE, None) == 3
     assert f(FAKE, 128, NULL, MISALIGNED, 16, 128, 64, 4, FAKE, FAKE, None) == 4
+
+
+def call_w4a16(x=FAKE, ldx=1024, w=FAKE, sw=FAKE, bias=NULL, y=FAKE, ldy=256, acc=NULL, M=1, N=256, K=1024,
+               ws=FAKE, ws_bytes=1 << 30):
+    return fq.LIB.fq_gemm_w4a16(x, ldx, w, sw, bias, y, ldy, acc, M, N, K, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=NULL), 1), (dict(w=NULL), 1), (dict(sw=NULL), 1), (dict(y=NULL), 1),
+    (dict(M=-1), 2), (dict(ldx=512), 2), (dict(ldy=128), 2),
+    (dict(N=250, ldy=256), 3), (dict(K=1000, ldx=1000), 3), (dict(K=0), 3),
+    (dict(x=MISALIGNED), 4), (dict(acc=MISALIGNED), 4), (dict(ldx=1028), 4), (dict(bias=MISALIGNED), 4),
+    (dict(ws=NULL, ws_bytes=0, K=16384, ldx=16384), 5), (dict(ws_bytes=8, K=16384, ldx=16384), 5),
+])
+def test_w4a16_rejects(kw, status):
+    assert call_w4a16(**kw) == status
+
+
+def test_w4a16_workspace_sizes():
+    assert fq.w4a16_workspace_bytes(1, 2048, 1024) == 0          # one K slice: no partials
+    assert fq.w4a16_workspace_bytes(1, 2048, 16384) >= 4 * 1 * 2048 * 4
+    assert fq.w4a16_workspace_bytes(0, 2048, 16384) == 0
+    assert call_w4a16(M=0, x=NULL, w=NULL, sw=NULL, y=NULL) == 0
