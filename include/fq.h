@@ -8,7 +8,7 @@
  *   y_jt  = s_j delta_t c_jt + b_j                                 (eq. (8))
  * against weights folded and rounded offline: W~ = W S R^T P rounded per output
  * channel to signed INT4 / INT8 codes qW with scales s (Alg. 1 offline).  S and P are
- * the positive diagonal scales of the two fold presets of Sec. III-B: fold-before
+ * the positive diagonal scales of the two fold presets of Sec. III-C: fold-before
  * (S calibrated in the original coordinates, P = I) and fold-after (S = I, P calibrated
  * after the rotation); either may be the identity (NULL).
  *
@@ -59,9 +59,9 @@ typedef enum {
 
 /* Runtime prologue, Alg. 1 runtime steps 1-2 (Sec. III-C transform, eq. (5)).
  *   x_bf16     [M, ldx] bf16 tokens (only the first K columns are read).
- *   smooth_inv [K] fp32 fold-before multiplier S^-1 (Sec. III-B/C), or NULL for S = I;
+ *   smooth_inv [K] fp32 fold-before multiplier S^-1 (Sec. III-C), or NULL for S = I;
  *              multiplied into x once, in fp32, before the rotation.
- *   post_inv   [K] fp32 fold-after multiplier P^-1 (Sec. III-B), or NULL for P = I;
+ *   post_inv   [K] fp32 fold-after multiplier P^-1 (Sec. III-C), or NULL for P = I;
  *              multiplied into the rotated row once, in fp32, before the row absmax.
  *   b          Hadamard block size; bits: 4 or 8 (q = 7 or 127); clip_ratio: r in eq. (5).
  *   a_codes    output codes, canonical layout: bits = 8 -> int8 [M, K];
@@ -76,7 +76,7 @@ fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv
  *   w          [N, ldw] fp32 weights of one consumer (row j = output channel j).
  *   col_scale  [K] fp32 S (fold-before smoothing, times a folded norm gain, eq. (4)),
  *              or NULL; multiplied into each row once, in fp32, before the rotation.
- *   post_scale [K] fp32 P (fold-after scale, Sec. III-B), or NULL; multiplied into
+ *   post_scale [K] fp32 P (fold-after scale, Sec. III-C), or NULL; multiplied into
  *              each rotated row once, in fp32, before the row absmax.
  *   Row j of W S R^T P is p . R (s . w_j) because H_b is symmetric, so each row is
  *   rounded with the prologue's contract at r = 1: w_codes int8 [N, K] in [-q, q] and

@@ -97,7 +97,7 @@ def fwht_quant(x, b: int, bits: int, clip_ratio: float = 1.0,
 
     x: bf16 torch tensor [M, K] or uint16 bit array, or float32 array [M, K].
     chan_mult: optional fp32 [K] multiplier applied before the rotation (fold-before S^-1).
-    post_mult: optional fp32 [K] multiplier applied after it (fold-after P^-1, Sec. III-B).
+    post_mult: optional fp32 [K] multiplier applied after it (fold-after P^-1, Sec. III-C).
     Returns (codes int8 [M, K] unpacked, delta float32 [M]).
     """
     lib = _lib()
@@ -128,7 +128,7 @@ def quantize_weights(w: np.ndarray, b: int, bits: int, col_scale: Optional[np.nd
     """Offline fold + round-to-nearest (Alg. 1 offline; eq. (2) with T = P^-1 R S^-1).
 
     Row j of the folded weight W S R^T P is p . R (s . w_j) (fold-before S, fold-after P,
-    Sec. III-B); it is rounded with the same per-row rule as a token at r = 1.
+    Sec. III-C); it is rounded with the same per-row rule as a token at r = 1.
     Returns (codes int8 [N, K], s_w float32 [N]).
     """
     return fwht_quant(np.ascontiguousarray(w, dtype=np.float32), b, bits, 1.0, col_scale, post_scale)

@@ -6,7 +6,7 @@ and no reordering, so it can be checked against the paper by eye:
     natural order (Sec. III-C).
   * block_rotation(K, b): R = I_{K/b} (x) H_b / sqrt(b) (Sec. III-C).
   * fold_weight(W, b, s, p): W~ = W S R^T P, the consumer weight of the fold presets
-    (Sec. III-B: fold-before (S^-1, I) gives W S R^T, fold-after (I, P^-1) gives
+    (Sec. III-C: fold-before (S^-1, I) gives W S R^T, fold-after (I, P^-1) gives
     W R^T P; eq. (2)).
   * transform_tokens(X, b, s_inv, p_inv): z_t = P^-1 R S^-1 x_t.
   * quantize_eq5(Z, bits, r): eq. (5) in float64 with the zero-token rule.

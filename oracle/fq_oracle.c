@@ -110,8 +110,8 @@ static int check_args(int64_t M, int64_t K, int64_t b, int bits, float r, int64_
 }
 
 /* One row: optional per-channel multiplier before the rotation (fold-before S^-1,
- * Sec. III-B), blockwise FWHT, optional per-channel multiplier after it (fold-after
- * P^-1, Sec. III-B), quantize.  Each multiplier is one fp32 rounding per element. */
+ * Sec. III-C), blockwise FWHT, optional per-channel multiplier after it (fold-after
+ * P^-1, Sec. III-C), quantize.  Each multiplier is one fp32 rounding per element. */
 static void transform_quantize_row(float *v, const float *chan_mult, const float *post_mult,
                                    int64_t K, int64_t b, int bits, float r, float cb,
                                    int8_t *code, float *delta) {

@@ -220,7 +220,7 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   if constexpr (B >= 128) lane_stage<4, CPT>(v1, tau);
   if constexpr (B >= 256) lane_stage<8, CPT>(v1, tau);
 
-  // ---- optional fold-after multiplier (Sec. III-B), one fp32 rounding per element -------
+  // ---- optional fold-after multiplier (Sec. III-C), one fp32 rounding per element -------
   if (p.post_mult) {
 #pragma unroll
     for (int c = 0; c < CPT; ++c)

@@ -92,7 +92,7 @@ def test_fwht_quant_fold_before_multiplier(b, bits):
 @pytest.mark.parametrize("b,bits,M,K", [(64, 4, 33, 2048), (128, 8, 33, 2048), (256, 4, 5, 16384),
                                          (128, 4, 50, 4096), (16, 8, 70, 384)])
 def test_fwht_quant_fold_after_multiplier(b, bits, M, K):
-    # Sec. III-B fold-after: P^-1 after the rotation, bit-exact (alone and with S^-1 before it)
+    # Sec. III-C fold-after: P^-1 after the rotation, bit-exact (alone and with S^-1 before it)
     flush(f"fwht_quant post b={b} bits={bits} M={M} K={K}")
     x = synth.activations(M, K, seed=79, outlier_frac=0.01, outlier_scale=30.0)
     p_inv = synth.channel_vector(K, seed=80, low=0.2, high=3.0)

@@ -225,7 +225,7 @@ def test_fold_before_multiplier():
 
 
 def test_fold_after_multiplier():
-    # Sec. III-B fold-after: z = P^-1 R x, the per-channel multiply AFTER the rotation.
+    # Sec. III-C fold-after: z = P^-1 R x, the per-channel multiply AFTER the rotation.
     # Against the float64 definition; a multiply placed before the rotation, or on the
     # wrong channel, moves most codes and fails.
     x = synth.activations(8, 512, seed=33, outlier_frac=0.01, outlier_scale=30.0)
