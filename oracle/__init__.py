@@ -40,6 +40,8 @@ def _lib():
         lib.fqo_gemm_i64.argtypes = [vp, vp, i64, i64, i64, vp]
         lib.fqo_dequant.argtypes = [vp, vp, vp, vp, i64, i64, vp]
         lib.fqo_w4a16.argtypes = [vp, i64, vp, vp, vp, i64, i64, i64, vp, vp]
+        lib.fqo_rotate_quant_bf16.argtypes = [vp, i64, vp, vp, vp, vp, i64, i64, i64, i32, f32, vp, vp, vp]
+        lib.fqo_rotate_quant_f32.argtypes = [vp, i64, vp, vp, vp, vp, i64, i64, i64, i32, f32, vp, vp, vp]
         lib.fqo_fwht_block_f32.argtypes = [vp, i64]
         lib.fqo_fwht_block_f32.restype = None
         lib.fqo_inv_sqrt_b.argtypes = [i64]
@@ -48,7 +50,7 @@ def _lib():
         lib.fqo_set_threads.argtypes = [i32]
         lib.fqo_set_threads.restype = None
         for name in ("fqo_fwht_quant_bf16", "fqo_fwht_quant_f32", "fqo_pack_int4", "fqo_gemm_i64",
-                     "fqo_dequant", "fqo_w4a16"):
+                     "fqo_dequant", "fqo_w4a16", "fqo_rotate_quant_bf16", "fqo_rotate_quant_f32"):
             getattr(lib, name).restype = i32
         _LIB = lib
     return _LIB
@@ -132,6 +134,46 @@ def quantize_weights(w: np.ndarray, b: int, bits: int, col_scale: Optional[np.nd
     Returns (codes int8 [N, K], s_w float32 [N]).
     """
     return fwht_quant(np.ascontiguousarray(w, dtype=np.float32), b, bits, 1.0, col_scale, post_scale)
+
+
+def rotate_quant(x, perm: Optional[np.ndarray], blocks: np.ndarray, b: int, bits: int,
+                 clip_ratio: float = 1.0, chan_mult: Optional[np.ndarray] = None,
+                 post_mult: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Prologue with the stored composite rotation of Sec. III-C in place of the block
+    Hadamard: gather by `perm` (int32 [K], output position c takes input channel perm[c];
+    None = identity), per-block orthogonal matrices `blocks` fp32 [K/b, b, b] applied as an
+    fma chain in ascending j, then eq. (5) with nothing deferred to delta.
+    x: bf16 torch tensor / uint16 bits, or float32 rows (the weight side).
+    Returns (codes int8 [M, K], delta float32 [M])."""
+    lib = _lib()
+    if not isinstance(x, np.ndarray):
+        x = bf16_bits(x)
+    M, K = x.shape
+    codes = np.zeros((M, K), dtype=np.int8)
+    delta = np.zeros(M, dtype=np.float32)
+    scratch = np.zeros(max(1, max_threads()) * 3 * max(K, 1), dtype=np.float32)
+    pm_ = None if perm is None else np.ascontiguousarray(perm, dtype=np.int32)
+    bl = np.ascontiguousarray(blocks, dtype=np.float32)
+    assert bl.shape == (K // b, b, b)
+    cm = None if chan_mult is None else np.ascontiguousarray(chan_mult, dtype=np.float32)
+    po = None if post_mult is None else np.ascontiguousarray(post_mult, dtype=np.float32)
+    xx = np.ascontiguousarray(x)
+    fn = lib.fqo_rotate_quant_bf16 if xx.dtype == np.uint16 else lib.fqo_rotate_quant_f32
+    if xx.dtype not in (np.uint16, np.float32):
+        raise TypeError(f"unsupported dtype {xx.dtype}")
+    rc = fn(_ptr(xx), K, _ptr(pm_), _ptr(bl), _ptr(cm), _ptr(po), M, K, b, bits, clip_ratio,
+            _ptr(codes), _ptr(delta), _ptr(scratch))
+    _check(rc, "rotate_quant")
+    return codes, delta
+
+
+def quantize_weights_rotated(w: np.ndarray, perm: Optional[np.ndarray], blocks: np.ndarray, b: int,
+                             bits: int, col_scale: Optional[np.ndarray] = None,
+                             post_scale: Optional[np.ndarray] = None) -> Tuple[np.ndarray, np.ndarray]:
+    """Offline fold + RTN for the composite rotation R = B P: row j of W S R^T P_out is
+    p . R (s . w_j), rounded with the token rule at r = 1."""
+    return rotate_quant(np.ascontiguousarray(w, dtype=np.float32), perm, blocks, b, bits, 1.0,
+                        col_scale, post_scale)
 
 
 def pack_int4(codes: np.ndarray) -> np.ndarray:

@@ -9,6 +9,8 @@ and no reordering, so it can be checked against the paper by eye:
     (Sec. III-C: fold-before (S^-1, I) gives W S R^T, fold-after (I, P^-1) gives
     W R^T P; eq. (2)).
   * transform_tokens(X, b, s_inv, p_inv): z_t = P^-1 R S^-1 x_t.
+  * composite_rotation(perm, blocks): R = B P, the stored composite rotation of
+    Sec. III-C (channel permutation P, block-diagonal B of per-block matrices).
   * quantize_eq5(Z, bits, r): eq. (5) in float64 with the zero-token rule.
   * integer_output(qw, s_w, qa, delta, bias): eq. (8).
 """
@@ -63,6 +65,17 @@ def fold_weight(W: np.ndarray, b: int, s: Optional[np.ndarray] = None,
     if p is not None:
         Wt = Wt * np.asarray(p, dtype=np.float64)[None, :]
     return Wt
+
+
+def composite_rotation(perm: Optional[np.ndarray], blocks: np.ndarray) -> np.ndarray:
+    """R = B P (float64 [K, K]): (P v)_c = v_perm[c], B = diag(Q_0, Q_1, ...)."""
+    nb, b, _ = blocks.shape
+    K = nb * b
+    P = np.eye(K)[np.arange(K) if perm is None else np.asarray(perm)]
+    B = np.zeros((K, K))
+    for k in range(nb):
+        B[k * b:(k + 1) * b, k * b:(k + 1) * b] = blocks[k]
+    return B @ P
 
 
 def quantize_eq5(Z: np.ndarray, bits: int, r: float = 1.0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:

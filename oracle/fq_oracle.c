@@ -220,3 +220,66 @@ int fqo_w4a16(const uint16_t *x, int64_t ldx, const int8_t *qw, const float *s_w
         }
     return FQO_OK;
 }
+
+/* Stored composite rotation (Sec. III-C, the action expert's optional transform): a
+ * channel permutation followed by per-block orthogonal b x b matrices, R = B P, in place
+ * of the block Hadamard.  The paper fixes neither the permutation ("zigzag") nor how the
+ * block matrices are made ("SVD-Hadamard"); both are inputs here.  Per token:
+ *   v_c = fl(x_c * s^-1_c)                (optional fold-before, original channel order)
+ *   w_c = v_perm[c]                       (gather; perm = NULL is the identity)
+ *   u_{kb+i} = fma chain over j = 0..b-1 ascending of Q_k[i][j] * w_{kb+j}, from +0
+ *   u_c = fl(u_c * p^-1_c)                (optional fold-after)
+ * then eq. (5) with c_b = 1 (the blocks are orthonormal, nothing is deferred to delta).
+ * blocks: [K/b][b][b] fp32, Q_k row-major.  scratch: [nthreads * 2K] floats. */
+static void rotate_quantize_row(const float *x, const int32_t *perm, const float *blocks,
+                                const float *chan_mult, const float *post_mult, int64_t K,
+                                int64_t b, int bits, float r, int8_t *code, float *delta,
+                                float *v, float *u) {
+    for (int64_t c = 0; c < K; ++c) v[c] = chan_mult ? x[c] * chan_mult[c] : x[c];
+    for (int64_t k0 = 0; k0 < K; k0 += b) {
+        const float *Q = blocks + k0 * b;  /* block k0 / b: b * b entries */
+        for (int64_t i = 0; i < b; ++i) {
+            float acc = 0.0f;
+            for (int64_t j = 0; j < b; ++j) {
+                const int64_t src = perm ? (int64_t)perm[k0 + j] : k0 + j;
+                acc = fmaf(Q[i * b + j], v[src], acc);
+            }
+            u[k0 + i] = post_mult ? acc * post_mult[k0 + i] : acc;
+        }
+    }
+    quantize_token(u, K, bits, r, 1.0f, code, delta);
+}
+
+static int check_perm(const int32_t *perm, int64_t K) {
+    if (!perm) return FQO_OK;
+    for (int64_t c = 0; c < K; ++c)
+        if (perm[c] < 0 || perm[c] >= K) return FQO_BAD_ARG;
+    return FQO_OK;
+}
+
+int fqo_rotate_quant_bf16(const uint16_t *x, int64_t ldx, const int32_t *perm, const float *blocks,
+                          const float *chan_mult, const float *post_mult, int64_t M, int64_t K,
+                          int64_t b, int bits, float r, int8_t *codes, float *delta, float *scratch) {
+    if (check_args(M, K, b, bits, r, ldx) || check_perm(perm, K) || !blocks) return FQO_BAD_ARG;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < M; ++t) {
+        float *row = scratch + (int64_t)omp_thread_slot() * 3 * K;
+        for (int64_t c = 0; c < K; ++c) row[c] = bf16_bits_to_float(x[t * ldx + c]);
+        rotate_quantize_row(row, perm, blocks, chan_mult, post_mult, K, b, bits, r, codes + t * K,
+                            delta + t, row + K, row + 2 * K);
+    }
+    return FQO_OK;
+}
+
+int fqo_rotate_quant_f32(const float *x, int64_t ldx, const int32_t *perm, const float *blocks,
+                         const float *chan_mult, const float *post_mult, int64_t M, int64_t K,
+                         int64_t b, int bits, float r, int8_t *codes, float *delta, float *scratch) {
+    if (check_args(M, K, b, bits, r, ldx) || check_perm(perm, K) || !blocks) return FQO_BAD_ARG;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t t = 0; t < M; ++t) {
+        float *row = scratch + (int64_t)omp_thread_slot() * 3 * K;
+        rotate_quantize_row(x + t * ldx, perm, blocks, chan_mult, post_mult, K, b, bits, r,
+                            codes + t * K, delta + t, row + K, row + 2 * K);
+    }
+    return FQO_OK;
+}

@@ -396,3 +396,73 @@ def test_w4a16_matches_numpy_float64_and_special_cases():
     np.testing.assert_array_equal(y1[2], bias.astype(np.float64))
     # the weights' integer codes stay on the -7..7 grid of eq. (5) at b = 1
     assert np.abs(q).max() == 7
+
+
+# --- Sec. III-C stored composite rotation (permutation + per-block matrices) ------------------
+
+def _orthogonal_blocks(nb, b, seed, dtype=np.float32):
+    rng = np.random.default_rng(seed)
+    qs = [np.linalg.qr(rng.standard_normal((b, b)))[0] for _ in range(nb)]
+    return np.stack(qs).astype(dtype)
+
+
+@pytest.mark.parametrize("b,bits", [(64, 4), (128, 8), (32, 4)])
+def test_composite_matches_float64_definition(b, bits):
+    K = 512
+    x = synth.activations(10, K, seed=90, outlier_frac=0.01, outlier_scale=30.0)
+    perm = np.random.default_rng(91).permutation(K).astype(np.int32)
+    blocks = _orthogonal_blocks(K // b, b, 92)
+    codes, delta = oracle.rotate_quant(x, perm, blocks, b, bits)
+    R = D.composite_rotation(perm, blocks.astype(np.float64))
+    Z = x.float().numpy().astype(np.float64) @ R.T
+    ref, dref, ratio = D.quantize_eq5(Z, bits)
+    ok = np.abs(np.abs(ratio - np.floor(ratio)) - 0.5) > 1e-4
+    np.testing.assert_array_equal(codes[ok], ref[ok])
+    np.testing.assert_allclose(delta, dref, rtol=1e-5)
+    # the gather direction matters: the inverse permutation moves most codes
+    Zw = x.float().numpy().astype(np.float64) @ D.composite_rotation(np.argsort(perm), blocks.astype(np.float64)).T
+    wref, _, _ = D.quantize_eq5(Zw, bits)
+    assert (wref != codes).mean() > 0.3
+
+
+@pytest.mark.parametrize("b", [16, 64, 128])
+def test_composite_with_hadamard_blocks_gives_fwht_codes(b):
+    # integer tokens and the +-1 Sylvester blocks: every fma is exact, so the dense chain and
+    # the butterfly reach the same numbers and the same codes (delta differs by c_b)
+    K = 1024
+    rng = np.random.default_rng(93)
+    xi = rng.integers(-40, 41, size=(8, K)).astype(np.float32)
+    x = torch.from_numpy(xi).to(torch.bfloat16)
+    blocks = np.stack([D.sylvester(b)] * (K // b)).astype(np.float32)
+    for bits in (4, 8):
+        c1, d1 = oracle.rotate_quant(x, None, blocks, b, bits)
+        c0, d0 = oracle.fwht_quant(x, b, bits)
+        np.testing.assert_array_equal(c1, c0)
+        np.testing.assert_allclose(d1 * oracle.inv_sqrt_b(b), d0, rtol=2e-7)
+
+
+@pytest.mark.parametrize("bits", [4, 8])
+def test_composite_identity_blocks_is_permuted_rtn(bits):
+    K, b = 256, 64
+    x = synth.activations(6, K, seed=94, dist="student_t3")
+    perm = np.random.default_rng(95).permutation(K).astype(np.int32)
+    eye = np.stack([np.eye(b, dtype=np.float32)] * (K // b))
+    c1, d1 = oracle.rotate_quant(x, perm, eye, b, bits)
+    c0, d0 = oracle.fwht_quant(x[:, torch.from_numpy(perm.astype(np.int64))].contiguous(), 1, bits)
+    np.testing.assert_array_equal(c1, c0)
+    np.testing.assert_array_equal(d1, d0)
+
+
+def test_composite_fold_identity_and_weight_rounding():
+    K, b, N = 256, 64, 40
+    perm = np.random.default_rng(96).permutation(K).astype(np.int32)
+    R64 = D.composite_rotation(perm, _orthogonal_blocks(K // b, b, 97, np.float64))
+    W = synth.weights(N, K, seed=98).astype(np.float64)
+    X = synth.activations(9, K, seed=99).double().numpy()
+    np.testing.assert_allclose((X @ R64.T) @ (W @ R64.T).T, X @ W.T, rtol=1e-9, atol=1e-12)
+    blocks = _orthogonal_blocks(K // b, b, 97)
+    R = D.composite_rotation(perm, blocks.astype(np.float64))
+    codes, s_w = oracle.quantize_weights_rotated(W.astype(np.float32), perm, blocks, b, 4)
+    Wt = W.astype(np.float32).astype(np.float64) @ R.T
+    err = np.abs(Wt - s_w[:, None].astype(np.float64) * codes)
+    assert np.all(err <= s_w[:, None] * 0.5 * (1 + 1e-4))
