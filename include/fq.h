@@ -85,6 +85,35 @@ fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scal
                               const float *post_scale, int64_t N, int64_t K, int b, int bits,
                               int8_t *w_codes, float *w_scale, void *stream);
 
+/* Prologue with the stored composite rotation (Sec. III-C: the action expert's optional
+ * transform, a channel permutation followed by per-block SVD-Hadamard matrices) in place
+ * of the block Hadamard: z_t = P^-1 B Pi S^-1 x_t with
+ *   perm       int32 [K] or NULL (identity): output position c takes input channel perm[c]
+ *              (entries outside [0, K) are clamped, giving wrong codes but no fault);
+ *   blocks     fp32 [K/b, b, b], block k's matrix Q_k row-major, applied to positions
+ *              [k b, (k+1) b); orthonormal blocks keep the scale (nothing deferred to delta);
+ *   b          a power of two, 1 <= b <= 128 (a block's matrix is held in LDS).
+ * Contract: after the optional S^-1 multiply and the gather, output i of block k is the
+ * fp32 fused multiply-add chain over j = 0..b-1 ascending of Q_k[i][j] * w_{kb+j},
+ * starting from +0; then the optional P^-1 multiply; then eq. (5) exactly as
+ * fq_fwht_quant with c_b = 1.  Codes in the canonical layout, as fq_fwht_quant.
+ *   ws         scratch of fq_rotate_quant_workspace_bytes(M, K) bytes (the fp32 rotated
+ *              rows); no initialization needed. */
+size_t fq_rotate_quant_workspace_bytes(int64_t M, int64_t K);
+fq_status fq_rotate_quant(const void *x_bf16, int64_t ldx, const int32_t *perm, const float *blocks,
+                          const float *smooth_inv, const float *post_inv, int64_t M, int64_t K, int b,
+                          int bits, float clip_ratio, void *a_codes, float *delta, void *ws,
+                          size_t ws_bytes, void *stream);
+
+/* Offline weight fold and round-to-nearest for the composite rotation: row j of
+ * W S R^T P with R = B Pi is rounded with fq_rotate_quant's contract at r = 1 (fp32 rows
+ * [N, ldw], ldw a multiple of 4); w_codes int8 [N, K], w_scale fp32 [N]; ws as above
+ * with M = N. */
+fq_status fq_quantize_weights_rotated(const float *w, int64_t ldw, const int32_t *perm, const float *blocks,
+                                      const float *col_scale, const float *post_scale, int64_t N, int64_t K,
+                                      int b, int bits, int8_t *w_codes, float *w_scale, void *ws,
+                                      size_t ws_bytes, void *stream);
+
 /* Bytes of the packed, kernel-native weight layout for an [N, K] matrix. */
 size_t fq_packed_weight_bytes(int64_t N, int64_t K, int bits);
 

@@ -150,6 +150,30 @@ fq_status gemm_entry(int bits, const void *a_codes, const float *delta, const vo
                      bits, ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
 
+fq_status rotate_common(const void *x, bool x_f32, int64_t ldx, const int32_t *perm, const float *blocks,
+                        const float *pre, const float *post, int64_t M, int64_t K, int b, int bits, float r,
+                        void *codes, int64_t ldc, float *delta, int fmt, void *ws, size_t ws_bytes,
+                        void *stream) {
+  fq_status s = check_prologue(x, ldx, x_f32 ? 4 : 8, pre, post, M, K, b, bits, r, codes, delta);
+  if (s != FQ_OK) return s;
+  if (b > 128) return fail(FQ_ERR_UNSUPPORTED, "b=%d: the composite rotation holds blocks of at most 128", b);
+  if (K > 32768) return fail(FQ_ERR_UNSUPPORTED, "K=%lld: the composite rotation handles K <= 32768", (long long)K);
+  if (M > 0x7FFFFFFF) return fail(FQ_ERR_UNSUPPORTED, "M=%lld too large", (long long)M);
+  if (M == 0) return ok();
+  if (!blocks) return fail(FQ_ERR_NULL, "blocks must be non-NULL");
+  if (!aligned16(blocks) || (perm && !aligned16(perm)))
+    return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  const size_t need = fq_rotate_quant_workspace_bytes(M, K);
+  if (!ws || ws_bytes < need)
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  hipError_t e = fq::launch_rotate_quant(x, x_f32, ldx, perm, blocks, pre, post, M, (int)K, b, bits, r,
+                                         static_cast<uint8_t *>(codes), ldc, delta, fmt,
+                                         static_cast<float *>(ws), static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "rotate_quant launch");
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -195,6 +219,30 @@ fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scal
                                        w_scale, fq::kOutInt8, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "quantize_weights launch");
   return ok();
+}
+
+size_t fq_rotate_quant_workspace_bytes(int64_t M, int64_t K) {
+  if (M <= 0 || K < 128) return 0;
+  return align256((size_t)M * (size_t)K * 4);
+}
+
+
+fq_status fq_rotate_quant(const void *x_bf16, int64_t ldx, const int32_t *perm, const float *blocks,
+                          const float *smooth_inv, const float *post_inv, int64_t M, int64_t K, int b,
+                          int bits, float clip_ratio, void *a_codes, float *delta, void *ws,
+                          size_t ws_bytes, void *stream) {
+  const bool nib = bits == 4;
+  return rotate_common(x_bf16, false, ldx, perm, blocks, smooth_inv, post_inv, M, K, b, bits, clip_ratio,
+                       a_codes, nib ? K / 2 : K, delta, nib ? fq::kOutNibble : fq::kOutInt8, ws, ws_bytes,
+                       stream);
+}
+
+fq_status fq_quantize_weights_rotated(const float *w, int64_t ldw, const int32_t *perm, const float *blocks,
+                                      const float *col_scale, const float *post_scale, int64_t N, int64_t K,
+                                      int b, int bits, int8_t *w_codes, float *w_scale, void *ws,
+                                      size_t ws_bytes, void *stream) {
+  return rotate_common(w, true, ldw, perm, blocks, col_scale, post_scale, N, K, b, bits, 1.0f, w_codes, K,
+                       w_scale, fq::kOutInt8, ws, ws_bytes, stream);
 }
 
 size_t fq_packed_weight_bytes(int64_t N, int64_t K, int bits) {

@@ -20,6 +20,13 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
                              uint8_t *codes, int64_t ld_codes, float *delta, int out_fmt,
                              hipStream_t s);
 
+// Composite-rotation prologue (permutation + per-block matrices, b <= 128) through the fp32
+// workspace z [M, K].
+hipError_t launch_rotate_quant(const void *x, bool x_is_f32, int64_t ldx, const int32_t *perm,
+                               const float *blocks, const float *chan_mult, const float *post_mult,
+                               int64_t M, int K, int b, int bits, float clip_ratio, uint8_t *codes,
+                               int64_t ld_codes, float *delta, int out_fmt, float *z, hipStream_t s);
+
 hipError_t launch_pack_weights(const int8_t *codes, int64_t N, int K, int bits, uint8_t *packed,
                                hipStream_t s);
 hipError_t launch_unpack_weights(const uint8_t *packed, int64_t N, int K, int bits, int8_t *codes,

@@ -385,4 +385,166 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
                   : launch_t<uint16_t>(p, log2b, q, smem, (int)grid64, s);
 }
 
+// ---------------------------------------------------------------------------------------
+// Stored composite rotation (Sec. III-C, the action expert's optional transform in place of
+// the block Hadamard): gather by a channel permutation, then per-block orthogonal b x b
+// matrices, as two kernels through an fp32 workspace z [M, K]:
+//   rot_transform_kernel: a workgroup holds one block's Q^T in LDS and runs 256/b rows per
+//     pass; output i of a row is the fma chain over j = 0..b-1 ascending of Q[i][j] * w_j
+//     from +0 (w_j = x[perm[kb + j]] times the optional fold-before multiplier of that
+//     input channel), times the optional fold-after multiplier;
+//   rot_quant_kernel: one workgroup per row: row absmax, eq. (5) with c_b = 1 (the
+//     blocks are orthonormal), canonical packing.
+// Permutation entries are clamped into [0, K): a bad permutation gives wrong codes, never
+// an out-of-bounds read.
+
+// rows per transform workgroup (the Q^T load is amortized over them): at least one pass
+template <int B>
+constexpr int rot_rows() { return 256 / B > 16 ? 256 / B : 16; }
+
+template <typename Tin, int B>
+__global__ __launch_bounds__(256) void rot_transform_kernel(const void *x, int64_t ldx, const int32_t *perm,
+                                                            const float *blocks, const float *chan_mult,
+                                                            const float *post_mult, int64_t M, int K,
+                                                            float *z) {
+  constexpr int RP = 256 / B;  // rows per pass
+  extern __shared__ __attribute__((aligned(16))) float rot_lds[];
+  float *qt = rot_lds;                                           // [B * B], Q^T
+  float(*vb)[B] = reinterpret_cast<float(*)[B]>(rot_lds + B * B);  // [RP][B], the pass's rows
+  const int tid = threadIdx.x;
+  const int kblk = blockIdx.x;
+  const int64_t row0 = (int64_t)blockIdx.y * rot_rows<B>();
+  const float *Q = blocks + (int64_t)kblk * B * B;
+  for (int e = tid; e < B * B; e += 256) qt[(e % B) * B + e / B] = Q[e];  // Q^T
+  const int rr = tid / B, i = tid % B;
+  const int c_out = kblk * B + i;
+  int src = perm ? perm[c_out] : c_out;
+  src = min(max(src, 0), K - 1);
+  const float cm = chan_mult ? chan_mult[src] : 1.0f;
+  const float pm = post_mult ? post_mult[c_out] : 1.0f;
+  for (int r0 = 0; r0 < rot_rows<B>(); r0 += RP) {
+    const int64_t row = row0 + r0 + rr;
+    const bool ok = row < M;
+    __syncthreads();  // Q^T is in place; the previous pass no longer reads vb
+    float v = 0.0f;
+    if (ok) {
+      if constexpr (sizeof(Tin) == 2)
+        v = bf16_lo(reinterpret_cast<const uint16_t *>(x)[row * ldx + src]);
+      else
+        v = reinterpret_cast<const float *>(x)[row * ldx + src];
+      if (chan_mult) v = v * cm;
+    }
+    vb[rr][i] = v;
+    __syncthreads();
+    float acc = 0.0f;
+#pragma unroll 8
+    for (int j = 0; j < B; ++j) acc = __builtin_fmaf(qt[j * B + i], vb[rr][j], acc);
+    if (post_mult) acc = acc * pm;
+    if (ok) z[row * K + c_out] = acc;
+  }
+}
+
+// One workgroup per row; thread t owns 16-channel chunks t, t + 256, ... (K <= 32768).
+__global__ __launch_bounds__(256) void rot_quant_kernel(const float *z, int64_t M, int K, int bits, float clip_ratio,
+                                                        uint8_t *codes, int64_t ld_codes, float *delta, int out_fmt) {
+  constexpr int CPT = 8;
+  __shared__ float red[4];
+  const int tid = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const int nchunks = K >> 4;
+  const float *zr = z + row * K;
+  float v[CPT][16];
+  float amax = 0.0f;
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) {
+    const int j = c * 256 + tid;
+    if (j < nchunks) {
+      const float4 *s4 = reinterpret_cast<const float4 *>(zr + j * 16);
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 t = s4[q4];
+        v[c][4 * q4] = t.x; v[c][4 * q4 + 1] = t.y; v[c][4 * q4 + 2] = t.z; v[c][4 * q4 + 3] = t.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 16; ++e) amax = fmaxf(amax, fabsf(v[c][e]));
+    }
+  }
+  amax = fmaxf(amax, lane_xor<1>(amax));
+  amax = fmaxf(amax, lane_xor<2>(amax));
+  amax = fmaxf(amax, lane_xor<4>(amax));
+  amax = fmaxf(amax, lane_xor<8>(amax));
+  amax = fmaxf(amax, lane_xor<16>(amax));
+  amax = fmaxf(amax, __shfl_xor(amax, 32, kWave));
+  if ((tid & 63) == 0) red[tid >> 6] = amax;
+  __syncthreads();
+  amax = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const int q = (1 << (bits - 1)) - 1;
+  const float qf = (float)q;
+  const bool zero = !(amax > 0.0f);
+  const float rA = clip_ratio * amax;
+  const float inv = zero ? 0.0f : qf / rA;
+  if (tid == 0) delta[row] = zero ? 0.0f : (rA * 1.0f) / qf;
+  uint8_t *row_out = codes + row * ld_codes;
+  const float lim = qf + 0.49f;
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) {
+    const int j = c * 256 + tid;
+    if (j < nchunks) {
+      int cc[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) cc[e] = quantize_bits(v[c][e], inv, lim);
+      store_chunk_bits(row_out, j, cc, out_fmt);
+    }
+  }
+}
+
+template <typename Tin, int B>
+static hipError_t launch_rot_b(const void *x, int64_t ldx, const int32_t *perm, const float *blocks,
+                               const float *chan_mult, const float *post_mult, int64_t M, int K, float *z,
+                               hipStream_t s) {
+  constexpr size_t lds = (size_t)(B * B + 256) * sizeof(float);
+  static bool attr = false;  // more than 64 KB of dynamic LDS must be requested once
+  if (lds > 65536 && !attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&rot_transform_kernel<Tin, B>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const dim3 grid((unsigned)(K / B), (unsigned)((M + rot_rows<B>() - 1) / rot_rows<B>()));
+  hipLaunchKernelGGL((rot_transform_kernel<Tin, B>), grid, dim3(256), lds, s, x, ldx, perm, blocks, chan_mult,
+                     post_mult, M, K, z);
+  return hipGetLastError();
+}
+
+template <typename Tin>
+static hipError_t launch_rot_t(const void *x, int64_t ldx, const int32_t *perm, const float *blocks,
+                               const float *chan_mult, const float *post_mult, int64_t M, int K, int b,
+                               float *z, hipStream_t s) {
+  switch (b) {
+    case 1: return launch_rot_b<Tin, 1>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    case 2: return launch_rot_b<Tin, 2>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    case 4: return launch_rot_b<Tin, 4>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    case 8: return launch_rot_b<Tin, 8>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    case 16: return launch_rot_b<Tin, 16>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    case 32: return launch_rot_b<Tin, 32>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    case 64: return launch_rot_b<Tin, 64>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    case 128: return launch_rot_b<Tin, 128>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, z, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_rotate_quant(const void *x, bool x_is_f32, int64_t ldx, const int32_t *perm,
+                               const float *blocks, const float *chan_mult, const float *post_mult,
+                               int64_t M, int K, int b, int bits, float clip_ratio, uint8_t *codes,
+                               int64_t ld_codes, float *delta, int out_fmt, float *z, hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  if (K > 256 * 8 * 16 || M > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipError_t e = x_is_f32 ? launch_rot_t<float>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, b, z, s)
+                          : launch_rot_t<uint16_t>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, b, z, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(rot_quant_kernel, dim3((unsigned)M), dim3(256), 0, s, z, M, K, bits, clip_ratio, codes,
+                     ld_codes, delta, out_fmt);
+  return hipGetLastError();
+}
+
 }  // namespace fq

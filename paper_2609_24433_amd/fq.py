@@ -22,6 +22,7 @@ _STATUS = {1: "FQ_ERR_NULL", 2: "FQ_ERR_SHAPE", 3: "FQ_ERR_UNSUPPORTED", 4: "FQ_
 EXPORTED = ["fq_fwht_quant", "fq_quantize_weights", "fq_packed_weight_bytes", "fq_pack_weights",
             "fq_unpack_weights", "fq_gemm_workspace_bytes", "fq_gemm_w4a4", "fq_gemm_w8a8",
             "fq_linear_workspace_bytes", "fq_linear", "fq_gemm_w4a16_workspace_bytes", "fq_gemm_w4a16",
+            "fq_rotate_quant_workspace_bytes", "fq_rotate_quant", "fq_quantize_weights_rotated",
             "fq_status_string", "fq_last_error"]
 
 
@@ -46,6 +47,8 @@ def _load() -> ctypes.CDLL:
         "fq_gemm_w8a8": [vp, vp, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
         "fq_linear": [vp, i64, vp, vp, i64, i64, i64, i32, i32, f32, vp, vp, vp, vp, i64, vp, sz, vp],
         "fq_gemm_w4a16": [vp, i64, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
+        "fq_rotate_quant": [vp, i64, vp, vp, vp, vp, i64, i64, i32, i32, f32, vp, vp, vp, sz, vp],
+        "fq_quantize_weights_rotated": [vp, i64, vp, vp, vp, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -54,7 +57,8 @@ def _load() -> ctypes.CDLL:
     for name, args in {"fq_packed_weight_bytes": [i64, i64, i32],
                        "fq_gemm_workspace_bytes": [i64, i64, i64, i32],
                        "fq_linear_workspace_bytes": [i64, i64, i64, i32],
-                       "fq_gemm_w4a16_workspace_bytes": [i64, i64, i64]}.items():
+                       "fq_gemm_w4a16_workspace_bytes": [i64, i64, i64],
+                       "fq_rotate_quant_workspace_bytes": [i64, i64]}.items():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = sz
@@ -184,6 +188,36 @@ def linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: in
                          _p(w_packed), _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N, _p(ws), ws.numel(),
                          _stream()))
     return y
+
+
+def rotate_quant(x: torch.Tensor, perm: Optional[torch.Tensor], blocks: torch.Tensor, b: int, bits: int,
+                 clip_ratio: float = 1.0, smooth_inv: Optional[torch.Tensor] = None,
+                 post_inv: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Prologue with the stored composite rotation (permutation int32 [K] or None, blocks fp32
+    [K/b, b, b]): x bf16 [M, K] -> (codes [M, K*bits/8], delta fp32 [M])."""
+    M, K = x.shape
+    assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
+    codes = torch.empty((M, code_bytes(K, bits)), dtype=torch.uint8, device=x.device)
+    delta = torch.empty((M,), dtype=torch.float32, device=x.device)
+    ws = workspace(int(LIB.fq_rotate_quant_workspace_bytes(M, K)), x.device)
+    _check(LIB.fq_rotate_quant(_p(x), x.stride(0) if M else K, _p(perm), _p(blocks), _p(smooth_inv), _p(post_inv),
+                               M, K, b, bits, clip_ratio, _p(codes), _p(delta), _p(ws), ws.numel(), _stream()))
+    return codes, delta
+
+
+def quantize_weights_rotated(w: torch.Tensor, perm: Optional[torch.Tensor], blocks: torch.Tensor, b: int,
+                             bits: int, col_scale: Optional[torch.Tensor] = None,
+                             post_scale: Optional[torch.Tensor] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Offline fold + RTN for the composite rotation: w fp32 [N, K] -> (codes int8 [N, K], scales fp32 [N])."""
+    N, K = w.shape
+    assert w.dtype == torch.float32 and w.stride(1) == 1
+    codes = torch.empty((N, K), dtype=torch.int8, device=w.device)
+    scale = torch.empty((N,), dtype=torch.float32, device=w.device)
+    ws = workspace(int(LIB.fq_rotate_quant_workspace_bytes(N, K)), w.device)
+    _check(LIB.fq_quantize_weights_rotated(_p(w), w.stride(0), _p(perm), _p(blocks), _p(col_scale),
+                                           _p(post_scale), N, K, b, bits, _p(codes), _p(scale), _p(ws),
+                                           ws.numel(), _stream()))
+    return codes, scale
 
 
 def w4a16_workspace_bytes(M: int, N: int, K: int) -> int:

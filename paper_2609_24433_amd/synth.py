@@ -72,6 +72,18 @@ def random_codes(M: int, K: int, bits: int, *, seed: int) -> np.ndarray:
     return rng.integers(-q, q + 1, size=(M, K), dtype=np.int8)
 
 
+def permutation(K: int, *, seed: int) -> np.ndarray:
+    """int32 [K]: a uniformly random permutation of 0..K-1."""
+    return np.random.default_rng(seed).permutation(K).astype(np.int32)
+
+
+def orthogonal_blocks(nb: int, b: int, *, seed: int) -> np.ndarray:
+    """fp32 [nb, b, b]: nb random orthogonal b x b matrices (Q factors of Gaussian draws), the
+    shape of a stored per-block rotation whose entries are dense and of mixed sign."""
+    rng = np.random.default_rng(seed)
+    return np.stack([np.linalg.qr(rng.standard_normal((b, b)))[0] for _ in range(nb)]).astype(np.float32)
+
+
 def random_scales(n: int, *, seed: int, low: float = 1e-3, high: float = 1e-1) -> np.ndarray:
     """fp32 [n] positive scales ~ U(low, high)."""
     rng = np.random.default_rng(seed)

@@ -155,3 +155,29 @@ def test_w4a16_workspace_sizes():
     assert fq.w4a16_workspace_bytes(1, 2048, 16384) >= 4 * 1 * 2048 * 4
     assert fq.w4a16_workspace_bytes(0, 2048, 16384) == 0
     assert call_w4a16(M=0, x=NULL, w=NULL, sw=NULL, y=NULL) == 0
+
+
+def call_rotate(x=FAKE, ldx=1024, perm=NULL, blocks=FAKE, smooth=NULL, post=NULL, M=4, K=1024, b=64, bits=4,
+                r=1.0, codes=FAKE, delta=FAKE, ws=FAKE, ws_bytes=1 << 30):
+    return fq.LIB.fq_rotate_quant(x, ldx, perm, blocks, smooth, post, M, K, b, bits, r, codes, delta, ws,
+                                  ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=NULL), 1), (dict(blocks=NULL), 1), (dict(codes=NULL), 1), (dict(delta=NULL), 1),
+    (dict(M=-1), 2), (dict(ldx=512), 2), (dict(K=1024 + 128, b=256, ldx=1152), 2),
+    (dict(b=256), 3), (dict(b=48), 3), (dict(K=65536, ldx=65536), 3), (dict(bits=3), 3), (dict(r=0.0), 3),
+    (dict(perm=MISALIGNED), 4), (dict(blocks=MISALIGNED), 4), (dict(post=MISALIGNED), 4), (dict(ldx=1028), 4),
+    (dict(ws=NULL, ws_bytes=0), 5), (dict(ws_bytes=4 * 4 * 1024 - 1), 5), (dict(ws=MISALIGNED), 4),
+])
+def test_rotate_quant_rejects(kw, status):
+    assert call_rotate(**kw) == status
+
+
+def test_rotate_quant_workspace_and_empty():
+    assert fq.LIB.fq_rotate_quant_workspace_bytes(4, 1024) >= 4 * 1024 * 4
+    assert fq.LIB.fq_rotate_quant_workspace_bytes(0, 1024) == 0
+    assert call_rotate(M=0, x=NULL, blocks=NULL, codes=NULL, delta=NULL, ws=NULL, ws_bytes=0) == 0
+    # the weight side takes fp32 rows: a leading dimension that is a multiple of 4 suffices
+    assert fq.LIB.fq_quantize_weights_rotated(FAKE, 1028, NULL, NULL, NULL, NULL, 16, 1024, 64, 4, FAKE, FAKE,
+                                              FAKE, 1 << 30, None) == 1
