@@ -31,6 +31,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0    # MI355X dense INT8 MFMA, TOPS (no INT4 MFMA on gfx950)
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s (the W4A16 path)
+FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector ALU, TFLOP/s (the composite rotation's fma chains)
 
 
 def parse():
@@ -295,6 +296,48 @@ def measure_points(torch, fq, synth, dev, log_fn):
     run_point("adaln_w4a16_m1", 1, 1024, 6144, 1, 4, "w4a16")
     run_point("down_w4a16_m1", 1, 16384, 2048, 1, 4, "w4a16")
     run_point("down_w4a16_m16", 16, 16384, 2048, 1, 4, "w4a16")
+    out += measure_prologue_points(torch, fq, synth, dev, log_fn)
+    return out
+
+
+def measure_prologue_points(torch, fq, synth, dev, log_fn):
+    """The activation prologue alone, block Hadamard butterfly against the stored composite
+    rotation (permutation + dense per-block matrices) on the same tokens.  Algorithmic bytes:
+    x, codes and scales, plus the permutation and the blocks for the composite one; its
+    2 M K b flops (fp32 fma chains) give the ALU side of its roofline."""
+    out = []
+    for (name, M, K, b) in (("ae_prologue_m50_k1024", 50, 1024, 128), ("ae_prologue_m50_k4096", 50, 4096, 128),
+                            ("lang_prologue_m816_k2048", 816, 2048, 128)):
+        x = synth.activations(M, K, seed=M + K + 7, outlier_frac=0.005, outlier_scale=50.0).to(dev)
+        perm = torch.from_numpy(synth.permutation(K, seed=K)).to(dev)
+        blocks = torch.from_numpy(synth.orthogonal_blocks(K // b, b, seed=b)).to(dev)
+        codes = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+        delta = torch.empty((M,), dtype=torch.float32, device=dev)
+        ws = fq.workspace(int(fq.LIB.fq_rotate_quant_workspace_bytes(M, K)), dev)
+        reps = 50
+        base = M * (2 * K + K // 2 + 4)
+        for kind in ("fwht", "rotate"):
+            if kind == "fwht":
+                call = lambda i: fq._check(fq.LIB.fq_fwht_quant(fq._p(x), K, None, None, M, K, b, 4, 1.0, fq._p(codes),
+                                                                 fq._p(delta), fq._stream()))
+                nbytes, flops = base, 0
+            else:
+                call = lambda i: fq._check(fq.LIB.fq_rotate_quant(fq._p(x), K, fq._p(perm), fq._p(blocks), None, None,
+                                                                   M, K, b, 4, 1.0, fq._p(codes), fq._p(delta),
+                                                                   fq._p(ws), ws.numel(), fq._stream()))
+                nbytes, flops = base + 4 * K + 4 * K * b, 2.0 * M * K * b
+            g = graph_of(torch, call, reps)
+            us = time_graph(torch, g, 4) / reps * 1e6
+            t_hbm = nbytes / HBM_PEAK_GBS / 1e3
+            t_alu = flops / FP32_VALU_PEAK_TFLOPS / 1e6
+            rec = {"name": f"{name}_{kind}", "kind": f"prologue_{kind}", "M": M, "K": K, "b": b, "bits": 4,
+                   "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1),
+                   "bound": "hbm" if t_hbm >= t_alu else "alu", "roofline_frac": round(max(t_hbm, t_alu) / us, 4)}
+            log_fn(json.dumps(rec))
+            out.append(rec)
+            del g
+        del x, perm, blocks, codes, delta, ws
+        torch.cuda.empty_cache()
     return out
 
 

@@ -158,7 +158,7 @@ fq_status rotate_common(const void *x, bool x_f32, int64_t ldx, const int32_t *p
   if (s != FQ_OK) return s;
   if (b > 128) return fail(FQ_ERR_UNSUPPORTED, "b=%d: the composite rotation holds blocks of at most 128", b);
   if (K > 32768) return fail(FQ_ERR_UNSUPPORTED, "K=%lld: the composite rotation handles K <= 32768", (long long)K);
-  if (M > 0x7FFFFFFF) return fail(FQ_ERR_UNSUPPORTED, "M=%lld too large", (long long)M);
+  if (M > (1ll << 20)) return fail(FQ_ERR_UNSUPPORTED, "M=%lld: the composite rotation handles M <= 2^20 rows", (long long)M);
   if (M == 0) return ok();
   if (!blocks) return fail(FQ_ERR_NULL, "blocks must be non-NULL");
   if (!aligned16(blocks) || (perm && !aligned16(perm)))
