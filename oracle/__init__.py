@@ -12,6 +12,9 @@ Parts:
   * definitions.py: float64 definitions written out with explicit matrices
     (Sylvester H_b, block rotation R, eq. (2) fold, eq. (5), eq. (8)).
   * exact.py: exact rational arithmetic of eq. (5) for tiny inputs.
+  * GPTQ in the transformed coordinates (eq. (7)): the second moment and the damped
+    inverse factor with numpy (float64 matmul, inverse, Cholesky), the column sweep in
+    fq_oracle.c.
 """
 from __future__ import annotations
 
@@ -37,6 +40,8 @@ def _lib():
         lib.fqo_fwht_quant_bf16.argtypes = [vp, i64, vp, vp, i64, i64, i64, i32, f32, vp, vp, vp]
         lib.fqo_fwht_quant_f32.argtypes = [vp, i64, vp, vp, i64, i64, i64, i32, f32, vp, vp, vp]
         lib.fqo_pack_int4.argtypes = [vp, i64, i64, vp]
+        lib.fqo_transform.argtypes = [vp, i32, i64, vp, vp, i64, i64, i64, vp]
+        lib.fqo_gptq_sweep.argtypes = [vp, i64, vp, i64, i64, i32, i64, f32, vp, vp, vp]
         lib.fqo_gemm_i64.argtypes = [vp, vp, i64, i64, i64, vp]
         lib.fqo_dequant.argtypes = [vp, vp, vp, vp, i64, i64, vp]
         lib.fqo_w4a16.argtypes = [vp, i64, vp, vp, vp, i64, i64, i64, vp, vp]
@@ -239,3 +244,73 @@ def linear(x, w_codes: np.ndarray, s_w: np.ndarray, b: int, bits: int,
     acc = gemm(codes, w_codes)
     y = dequant(acc, delta, s_w, bias)
     return codes, delta, acc, y
+
+
+def transform(x, b: int, chan_mult: Optional[np.ndarray] = None,
+              post_mult: Optional[np.ndarray] = None) -> np.ndarray:
+    """The prologue's transform alone (optional fold-before multiplier, unnormalized
+    blockwise butterfly, optional fold-after multiplier), fp32 [M, K]: the coordinates of
+    eq. (7).  x: bf16 torch tensor / uint16 bits, or float32 rows (weights)."""
+    if not isinstance(x, np.ndarray):
+        x = bf16_bits(x)
+    xx = np.ascontiguousarray(x)
+    if xx.dtype not in (np.uint16, np.float32):
+        raise TypeError(f"unsupported dtype {xx.dtype}")
+    M, K = xx.shape
+    z = np.zeros((M, K), dtype=np.float32)
+    cm = None if chan_mult is None else np.ascontiguousarray(chan_mult, dtype=np.float32)
+    po = None if post_mult is None else np.ascontiguousarray(post_mult, dtype=np.float32)
+    _check(_lib().fqo_transform(_ptr(xx), int(xx.dtype == np.uint16), K, _ptr(cm), _ptr(po), M, K, b,
+                                _ptr(z)), "transform")
+    return z
+
+
+def gptq_hessian(z: np.ndarray) -> np.ndarray:
+    """G = Z Z^T of eq. (7) in float64 (z: calibration tokens as rows [T, K], so G = z^T z)."""
+    z64 = np.asarray(z, dtype=np.float64)
+    return z64.T @ z64
+
+
+def gptq_damped(G: np.ndarray, damp: float = 0.01) -> np.ndarray:
+    """H = G + lambda I with lambda = damp * mean(diag G) (the GPTQ method's diagonal damping
+    named in Sec. III-F); a second moment that is all zero (no calibration signal) gives I."""
+    G = np.asarray(G, dtype=np.float64)
+    lam = damp * float(np.mean(np.diag(G)))
+    if lam == 0.0:
+        return np.eye(G.shape[0])
+    return G + lam * np.eye(G.shape[0])
+
+
+def gptq_factor(G: np.ndarray, damp: float = 0.01) -> np.ndarray:
+    """U: upper triangular with H^-1 = U^T U, H the damped second moment (float64)."""
+    H = gptq_damped(G, damp)
+    return np.ascontiguousarray(np.linalg.cholesky(np.linalg.inv(H)).T)
+
+
+def gptq_sweep(w_t: np.ndarray, U: np.ndarray, bits: int, blk: int = 128,
+               scale_mult: float = 1.0) -> Tuple[np.ndarray, np.ndarray]:
+    """The GPTQ column sweep on folded rows w_t fp32 [N, K] with factor U fp64 [K, K].
+    Returns (codes int8 [N, K], scales fp32 [N]); scales = fl32(max|row| * scale_mult / q)."""
+    w_t = np.ascontiguousarray(w_t, dtype=np.float32)
+    U = np.ascontiguousarray(U, dtype=np.float64)
+    N, K = w_t.shape
+    assert U.shape == (K, K)
+    codes = np.zeros((N, K), dtype=np.int8)
+    scales = np.zeros(N, dtype=np.float32)
+    scratch = np.zeros(max(1, max_threads()) * (K + blk), dtype=np.float64)
+    _check(_lib().fqo_gptq_sweep(_ptr(w_t), K, _ptr(U), N, K, bits, blk, float(scale_mult), _ptr(codes),
+                                 _ptr(scales), _ptr(scratch)), "gptq_sweep")
+    return codes, scales
+
+
+def gptq_quantize_weights(w: np.ndarray, calib, b: int, bits: int, col_scale: Optional[np.ndarray] = None,
+                          post_scale: Optional[np.ndarray] = None, smooth_inv: Optional[np.ndarray] = None,
+                          post_inv: Optional[np.ndarray] = None, damp: float = 0.01,
+                          blk: int = 128) -> Tuple[np.ndarray, np.ndarray]:
+    """Eq. (7) end to end: calibration tokens (bf16 [T, K]) through the prologue's transform
+    (with the tokens' multipliers), G = Z Z^T, the damped factor, and the sweep over the
+    folded weight rows (row j = p . H_b (s . w_j), unnormalized; scale carries c_b)."""
+    z = transform(calib, b, smooth_inv, post_inv)
+    U = gptq_factor(gptq_hessian(z), damp)
+    w_t = transform(np.ascontiguousarray(w, dtype=np.float32), b, col_scale, post_scale)
+    return gptq_sweep(w_t, U, bits, blk, float(inv_sqrt_b(b)))

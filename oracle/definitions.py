@@ -103,3 +103,41 @@ def integer_output(qw: np.ndarray, s_w: np.ndarray, qa: np.ndarray, delta: np.nd
     if bias is not None:
         y = y + np.asarray(bias, np.float64)[None, :]
     return y
+
+
+def obs_round_rows(Wt: np.ndarray, H: np.ndarray, bits: int) -> Tuple[np.ndarray, np.ndarray]:
+    """The rounding eq. (7) asks of GPTQ, written as its defining sequence of optimal-brain-
+    surgeon steps in float64 with explicit linear solves (no Cholesky factor): the columns
+    of each row are rounded in order; before column c is rounded, every column not yet
+    rounded holds the value that minimizes (w - w0) H (w - w0)^T given the rounded ones.
+    Rounding uses the row's fixed step max|w0| / q.  Returns (codes int64 [N, K], the
+    smallest distance of any rounding argument from a half-integer, for tie screening)."""
+    Wt = np.asarray(Wt, dtype=np.float64)
+    H = np.asarray(H, dtype=np.float64)
+    N, K = Wt.shape
+    q = 2 ** (bits - 1) - 1
+    codes = np.zeros((N, K), dtype=np.int64)
+    margin = np.inf
+    for j in range(N):
+        w0 = Wt[j]
+        A = np.abs(w0).max()
+        if A == 0.0:
+            continue
+        step = A / q
+        w = w0.copy()
+        for c in range(K):
+            t = w[c] / step
+            margin = min(margin, abs(abs(t - np.floor(t)) - 0.5))
+            codes[j, c] = int(np.clip(np.rint(t), -q, q))
+            fixed = np.arange(c + 1)
+            free = np.arange(c + 1, K)
+            if free.size:
+                d = codes[j, fixed] * step - w0[fixed]
+                w[free] = w0[free] - np.linalg.solve(H[np.ix_(free, free)], H[np.ix_(free, fixed)] @ d)
+    return codes, margin
+
+
+def gptq_objective(Wt: np.ndarray, Q: np.ndarray, Z: np.ndarray) -> float:
+    """||(W~ - Q) Z||_F^2 of eq. (7) in float64 (Z: calibration tokens as rows [T, K])."""
+    D = np.asarray(Wt, np.float64) - np.asarray(Q, np.float64)
+    return float(np.sum((D @ np.asarray(Z, np.float64).T) ** 2))

@@ -112,15 +112,37 @@ static int check_args(int64_t M, int64_t K, int64_t b, int bits, float r, int64_
 /* One row: optional per-channel multiplier before the rotation (fold-before S^-1,
  * Sec. III-C), blockwise FWHT, optional per-channel multiplier after it (fold-after
  * P^-1, Sec. III-C), quantize.  Each multiplier is one fp32 rounding per element. */
-static void transform_quantize_row(float *v, const float *chan_mult, const float *post_mult,
-                                   int64_t K, int64_t b, int bits, float r, float cb,
-                                   int8_t *code, float *delta) {
+static void transform_row(float *v, const float *chan_mult, const float *post_mult, int64_t K,
+                          int64_t b) {
     if (chan_mult)
         for (int64_t c = 0; c < K; ++c) v[c] = v[c] * chan_mult[c];
     for (int64_t k0 = 0; k0 < K; k0 += b) fqo_fwht_block_f32(v + k0, b);
     if (post_mult)
         for (int64_t c = 0; c < K; ++c) v[c] = v[c] * post_mult[c];
+}
+
+static void transform_quantize_row(float *v, const float *chan_mult, const float *post_mult,
+                                   int64_t K, int64_t b, int bits, float r, float cb,
+                                   int8_t *code, float *delta) {
+    transform_row(v, chan_mult, post_mult, K, b);
     quantize_token(v, K, bits, r, cb, code, delta);
+}
+
+/* The prologue's transform alone (multipliers and the unnormalized butterfly), fp32 rows
+ * z [M, K]: the coordinates in which Sec. III-F collects calibration tokens and rounds the
+ * folded weights.  x is bf16 bits (is_bf16) or fp32. */
+int fqo_transform(const void *x, int is_bf16, int64_t ldx, const float *chan_mult,
+                  const float *post_mult, int64_t M, int64_t K, int64_t b, float *z) {
+    if (check_args(M, K, b, 4, 1.0f, ldx)) return FQO_BAD_ARG;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < M; ++t) {
+        float *row = z + t * K;
+        for (int64_t c = 0; c < K; ++c)
+            row[c] = is_bf16 ? bf16_bits_to_float(((const uint16_t *)x)[t * ldx + c])
+                             : ((const float *)x)[t * ldx + c];
+        transform_row(row, chan_mult, post_mult, K, b);
+    }
+    return FQO_OK;
 }
 
 /* Activation prologue (Alg. 1 runtime, first two steps) on bf16 tokens.
@@ -280,6 +302,68 @@ int fqo_rotate_quant_f32(const float *x, int64_t ldx, const int32_t *perm, const
         float *row = scratch + (int64_t)omp_thread_slot() * 3 * K;
         rotate_quantize_row(x + t * ldx, perm, blocks, chan_mult, post_mult, K, b, bits, r,
                             codes + t * K, delta + t, row + K, row + 2 * K);
+    }
+    return FQO_OK;
+}
+
+/* GPTQ in the transformed coordinates (eq. (7), Sec. III-F): the columns of each folded
+ * weight row are rounded in order, and each rounding error is pushed onto the columns not
+ * yet rounded through U, the upper Cholesky factor of the damped inverse second moment
+ * (H^-1 = U^T U), in the lazy-batch form of the GPTQ method: within a block of `blk`
+ * columns the error goes to the block's later columns at once, to the columns after the
+ * block once per block.  Exact arithmetic is the same as the one-column-at-a-time form.
+ *
+ * Floating-point contract (fp64 throughout; the paper fixes no precision):
+ *   A = max_c |w_c| over the fp32 row (exact), q = 2^(bits-1) - 1;
+ *   scale = fl32((A * scale_mult) / q) in fp32 (the round-to-nearest weight rule's scale);
+ *   inv = q / A and step = A / q in fp64;
+ *   column c: code = clamp(rint(w_c * inv), -q, q); e = (w_c - code * step) / U[c][c];
+ *     each later column c' of the block: w_c' = fma(-e, U[c][c'], w_c');
+ *   after the block [i1, i2): each column c' >= i2: acc = fma chain over k = i1..i2-1
+ *     ascending of e_k * U[k][c'] from +0, then w_c' = w_c' - acc.
+ * A zero row gives codes 0 and scale 0.  w: fp32 [N, ldw] folded rows (the unnormalized
+ * transform's coordinates); U: fp64 [K, K] row-major (entries below the diagonal unused);
+ * codes: int8 [N, K]; scales: fp32 [N]; scratch: nthreads * (K + blk) doubles. */
+int fqo_gptq_sweep(const float *w, int64_t ldw, const double *U, int64_t N, int64_t K, int bits,
+                   int64_t blk, float scale_mult, int8_t *codes, float *scales, double *scratch) {
+    if (N < 0 || K < 1 || ldw < K || blk < 1 || (bits != 4 && bits != 8)) return FQO_BAD_ARG;
+    const int q = (1 << (bits - 1)) - 1;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t j = 0; j < N; ++j) {
+        double *wr = scratch + (int64_t)omp_thread_slot() * (K + blk);
+        double *e = wr + K;
+        const float *src = w + j * ldw;
+        int8_t *code = codes + j * K;
+        float A = 0.0f;
+        for (int64_t c = 0; c < K; ++c) {
+            float m = fabsf(src[c]);
+            if (m > A) A = m;
+        }
+        if (A == 0.0f) {
+            for (int64_t c = 0; c < K; ++c) code[c] = 0;
+            scales[j] = 0.0f;
+            continue;
+        }
+        scales[j] = (A * scale_mult) / (float)q;
+        const double inv = (double)q / (double)A, step = (double)A / (double)q;
+        for (int64_t c = 0; c < K; ++c) wr[c] = (double)src[c];
+        for (int64_t i1 = 0; i1 < K; i1 += blk) {
+            const int64_t i2 = i1 + blk < K ? i1 + blk : K;
+            for (int64_t c = i1; c < i2; ++c) {
+                double k = rint(wr[c] * inv); /* round half to even */
+                if (k > q) k = q;
+                if (k < -q) k = -q;
+                code[c] = (int8_t)k;
+                const double err = (wr[c] - k * step) / U[c * K + c];
+                e[c - i1] = err;
+                for (int64_t c2 = c + 1; c2 < i2; ++c2) wr[c2] = fma(-err, U[c * K + c2], wr[c2]);
+            }
+            for (int64_t c2 = i2; c2 < K; ++c2) {
+                double acc = 0.0;
+                for (int64_t k = i1; k < i2; ++k) acc = fma(e[k - i1], U[k * K + c2], acc);
+                wr[c2] = wr[c2] - acc;
+            }
+        }
     }
     return FQO_OK;
 }

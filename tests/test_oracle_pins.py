@@ -466,3 +466,86 @@ def test_composite_fold_identity_and_weight_rounding():
     Wt = W.astype(np.float32).astype(np.float64) @ R.T
     err = np.abs(Wt - s_w[:, None].astype(np.float64) * codes)
     assert np.all(err <= s_w[:, None] * 0.5 * (1 + 1e-4))
+
+
+# --- eq. (7): GPTQ in the transformed coordinates ---------------------------------------------
+
+def test_transform_is_the_unnormalized_block_product():
+    K, b = 256, 64
+    x = synth.activations(5, K, seed=120)
+    z = oracle.transform(x, b)
+    ref = x.float().numpy().astype(np.float64) @ (D.block_rotation(K, b) * np.sqrt(b)).T
+    np.testing.assert_allclose(z, ref, rtol=1e-5, atol=1e-4)
+    # integer tokens: every butterfly sum is exact
+    xi = torch.from_numpy(np.random.default_rng(121).integers(-50, 51, (4, K)).astype(np.float32)).to(torch.bfloat16)
+    zi = oracle.transform(xi, b)
+    np.testing.assert_array_equal(zi, xi.float().numpy() @ (D.block_rotation(K, b) * np.sqrt(b)).T.round())
+    # the prologue's codes are eq. (5) of exactly these rows
+    codes, delta = oracle.fwht_quant(x, b, 4)
+    ref_codes, _, ratio = D.quantize_eq5(z, 4)
+    ok = np.abs(np.abs(ratio - np.floor(ratio)) - 0.5) > 1e-4
+    np.testing.assert_array_equal(codes[ok], ref_codes[ok])
+
+
+def test_gptq_damping_and_empty_second_moment():
+    G = np.diag([4.0, 0.0, 2.0])
+    np.testing.assert_array_equal(oracle.gptq_damped(G, 0.01), G + 0.02 * np.eye(3))
+    np.testing.assert_array_equal(oracle.gptq_damped(np.zeros((3, 3))), np.eye(3))
+    U = oracle.gptq_factor(G + np.eye(3))
+    H = oracle.gptq_damped(G + np.eye(3))
+    np.testing.assert_allclose(U.T @ U @ H, np.eye(3), atol=1e-12)
+    assert np.all(np.tril(U, -1) == 0) and np.all(np.diag(U) > 0)
+
+
+@pytest.mark.parametrize("K,blk,bits", [(12, 128, 4), (24, 8, 4), (20, 6, 8), (16, 1, 4)])
+def test_gptq_sweep_is_sequential_obs(K, blk, bits):
+    # the lazy-batch sweep through the Cholesky factor against the defining sequence of
+    # optimal-brain-surgeon steps with explicit solves; correlated tokens, so the error
+    # feedback moves many codes away from plain rounding
+    rng = np.random.default_rng(122 + K)
+    Z = rng.standard_normal((400, K)) @ rng.standard_normal((K, K)) * 0.3
+    Wt = rng.standard_normal((30, K)).astype(np.float32)
+    H = oracle.gptq_damped(Z.T @ Z)
+    codes, scales = oracle.gptq_sweep(Wt, oracle.gptq_factor(Z.T @ Z), bits, blk)
+    ref, margin = D.obs_round_rows(Wt, H, bits)
+    assert margin > 1e-7, margin  # no decision sits on a tie in either precision
+    np.testing.assert_array_equal(codes, ref)
+    rtn, _, _ = D.quantize_eq5(Wt, bits)
+    assert (codes != rtn).mean() > 0.05
+    q = 2 ** (bits - 1) - 1
+    np.testing.assert_array_equal(scales, (np.abs(Wt).max(axis=1) / np.float32(q)).astype(np.float32))
+
+
+def test_gptq_identity_second_moment_is_rtn():
+    K, b = 256, 64
+    w = synth.weights(40, K, seed=123)
+    w_t = oracle.transform(w, b)
+    for bits in (4, 8):
+        codes, scales = oracle.gptq_sweep(w_t, np.eye(K), bits, 128, float(oracle.inv_sqrt_b(b)))
+        ref, _, ratio = D.quantize_eq5(w_t, bits)
+        ok = np.abs(np.abs(ratio - np.floor(ratio)) - 0.5) > 1e-6
+        np.testing.assert_array_equal(codes[ok], ref[ok])
+        _, s_rtn = oracle.quantize_weights(w, b, bits)
+        np.testing.assert_array_equal(scales, s_rtn)  # the same scale as round-to-nearest
+    # an all-zero second moment falls back to the identity
+    c0, _ = oracle.gptq_sweep(w_t, oracle.gptq_factor(np.zeros((K, K))), 4)
+    c1, _ = oracle.gptq_sweep(w_t, np.eye(K), 4)
+    np.testing.assert_array_equal(c0, c1)
+
+
+def test_gptq_lowers_the_eq7_objective_and_keeps_zero_rows():
+    K, b, N = 256, 64, 48
+    calib = synth.activations(600, K, seed=124, outlier_frac=0.02, outlier_scale=20.0, dist="student_t3")
+    w = synth.weights(N, K, seed=125)
+    w[3] = 0.0
+    codes, scales = oracle.gptq_quantize_weights(w, calib, b, 4)
+    rtn, s_rtn = oracle.quantize_weights(w, b, 4)
+    np.testing.assert_array_equal(scales, s_rtn)
+    assert not codes[3].any() and scales[3] == 0.0
+    z = oracle.transform(calib, b).astype(np.float64)
+    w_t = oracle.transform(w, b).astype(np.float64)
+    step = (scales / oracle.inv_sqrt_b(b)).astype(np.float64)[:, None]
+    e_gptq = D.gptq_objective(w_t, codes * step, z)
+    e_rtn = D.gptq_objective(w_t, rtn * step, z)
+    assert e_gptq < 0.8 * e_rtn, (e_gptq, e_rtn)
+    assert np.abs(codes).max() <= 7
