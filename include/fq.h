@@ -188,6 +188,57 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, co
 const char *fq_status_string(fq_status s);
 const char *fq_last_error(void);
 
+/* ---- GPTQ in the transformed coordinates (eq. (7), Sec. III-F) ----------------------------
+ * Offline rounding of folded weights against the second moment G = Z Z^T of calibration
+ * tokens taken in the runtime transform's coordinates, with diagonal damping (the GPTQ
+ * method the paper names for its four-bit weights).  Four calls:
+ *   fq_transform      tokens and weight rows into the transformed coordinates;
+ *   fq_gptq_hessian   G = Z Z^T (fp64);
+ *   fq_gptq_factor    U with (G + lambda I)^-1 = U^T U;
+ *   fq_gptq_sweep     the column sweep, codes and per-output-channel scales.
+ * All four take device pointers, enqueue on `stream` and return before the work is done. */
+
+/* The prologue's transform without the quantization: z_t = P^-1 H_b S^-1 x_t, unnormalized
+ * (Sylvester +-1 blocks, the same fp32 butterfly, stage order and multiplies as
+ * fq_fwht_quant), fp32 rows z [M, K].  x: bf16 rows (x_is_f32 = 0, ldx a multiple of 8) or
+ * fp32 rows (x_is_f32 = 1, ldx a multiple of 4); pre_mult / post_mult: fp32 [K] or NULL.
+ * K a multiple of 128 in [128, 32768]; b a power of two <= 256 dividing K.  Weight rows go
+ * through the same call (x_is_f32 = 1, pre_mult = the fold's S, post_mult = its P): since
+ * H_b is symmetric, row j of W S H_b^T P is P H_b (S w_j). */
+fq_status fq_transform(const void *x, int x_is_f32, int64_t ldx, const float *pre_mult, const float *post_mult,
+                       int64_t M, int64_t K, int b, float *z, void *stream);
+
+/* G = sum_t z_t z_t^T over T transformed tokens z [T, ldz] (fp32), in fp64, written in full
+ * (symmetric) to G [K, K]; accumulate != 0 adds to the G already there, so calibration
+ * batches can be streamed.  K a multiple of 128, at most 16384.  T = 0 with accumulate = 0
+ * clears G. */
+fq_status fq_gptq_hessian(const float *z, int64_t ldz, int64_t T, int64_t K, double *G, int accumulate,
+                          void *stream);
+
+/* U: fp64 [K, K] upper triangular (zeros below the diagonal) with H^-1 = U^T U, where
+ * H = G + lambda I, lambda = damp * mean(diag G) (damp in [0, 1], 0.01 is the GPTQ
+ * method's default); an all-zero diagonal gives H = I.  H must be positive definite
+ * (damping > 0 guarantees it for a nonzero G); otherwise U holds NaNs.
+ * ws: fq_gptq_factor_workspace_bytes(K) bytes (about 2 K^2 doubles), no initialization. */
+size_t fq_gptq_factor_workspace_bytes(int64_t K);
+fq_status fq_gptq_factor(const double *G, int64_t K, double damp, double *U, void *ws, size_t ws_bytes,
+                         void *stream);
+
+/* The GPTQ column sweep over folded weight rows w_t fp32 [N, ldw] (fq_transform's output
+ * for the weights), with U from fq_gptq_factor.  Contract (fp64; the codes are
+ * reproducible bit for bit): per row A = max |w|, scale = fl32((A * scale_mult) / q)
+ * (scale_mult = 1/sqrt(b) as a float for the block Hadamard, so the scale equals
+ * fq_quantize_weights'), inv = q / A and step = A / q; columns in blocks of 128; column c:
+ * code = clamp(rint(w_c * inv), -q, q), e = (w_c - code * step) / U[c][c], each later
+ * column c' of the block w_c' = fma(-e, U[c][c'], w_c'); after the block, each later
+ * column w_c' -= (fma chain over the block's k ascending of e_k * U[k][c'] from +0).
+ * A zero row gives codes 0 and scale 0.  w_codes int8 [N, K] (pack with fq_pack_weights);
+ * w_scale fp32 [N]; ws: fq_gptq_sweep_workspace_bytes(N, K) bytes, no initialization. */
+size_t fq_gptq_sweep_workspace_bytes(int64_t N, int64_t K);
+fq_status fq_gptq_sweep(const float *w_t, int64_t ldw, const double *U, int64_t N, int64_t K, int bits,
+                        float scale_mult, int8_t *w_codes, float *w_scale, void *ws, size_t ws_bytes,
+                        void *stream);
+
 #ifdef __cplusplus
 }
 #endif

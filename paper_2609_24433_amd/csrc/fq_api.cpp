@@ -38,6 +38,7 @@ bool is_pow2(int64_t v) { return v >= 1 && (v & (v - 1)) == 0; }
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 constexpr int64_t kMaxK = 32768;
+constexpr int64_t kMaxGptqK = 16384;  // the factor holds two K x K fp64 matrices
 
 // float nearest to 1/sqrt(b), b = 2^k: 2^(-k/2) for even k, 2^(-(k-1)/2) / sqrt(2) for odd k
 float inv_sqrt_pow2(int b) {
@@ -378,6 +379,87 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, co
   if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
   return gemm_common(codes, nibble ? fq::kANibble : fq::kAInt8, lda, delta, w_packed, w_scale, bias, y_bf16,
                      ldy, nullptr, M, N, K, bits, gws, ws_bytes - codes_bytes - delta_bytes, st);
+}
+
+// ---- GPTQ in the transformed coordinates (eq. (7)) ----
+
+fq_status fq_transform(const void *x, int x_is_f32, int64_t ldx, const float *pre_mult, const float *post_mult,
+                       int64_t M, int64_t K, int b, float *z, void *stream) {
+  fq_status s = check_prologue_shape(ldx, x_is_f32 ? 4 : 8, M, K, b, 4, 1.0f);
+  if (s != FQ_OK) return s;
+  if (M == 0) return ok();
+  if (!x || !z) return fail(FQ_ERR_NULL, "x and z must be non-NULL");
+  if (!aligned16(x) || !aligned16(z) || (pre_mult && !aligned16(pre_mult)) || (post_mult && !aligned16(post_mult)))
+    return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  hipError_t e = fq::launch_transform(x, x_is_f32 != 0, ldx, pre_mult, post_mult, M, (int)K, b, z,
+                                      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "transform launch");
+  return ok();
+}
+
+fq_status fq_gptq_hessian(const float *z, int64_t ldz, int64_t T, int64_t K, double *G, int accumulate,
+                          void *stream) {
+  fq_status s;
+  if ((s = check_k(K)) != FQ_OK) return s;
+  if (K > kMaxGptqK) return fail(FQ_ERR_UNSUPPORTED, "K=%lld: GPTQ handles K <= %lld", (long long)K, (long long)kMaxGptqK);
+  if (T < 0) return fail(FQ_ERR_SHAPE, "T=%lld < 0", (long long)T);
+  if (ldz < K) return fail(FQ_ERR_SHAPE, "ldz=%lld < K=%lld", (long long)ldz, (long long)K);
+  if (!G || (T > 0 && !z)) return fail(FQ_ERR_NULL, "z and G must be non-NULL");
+  if (!aligned16(G) || (z && !aligned16(z))) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  hipError_t e = fq::launch_gptq_hessian(z, ldz, T, (int)K, G, accumulate != 0, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "gptq_hessian launch");
+  return ok();
+}
+
+size_t fq_gptq_factor_workspace_bytes(int64_t K) {
+  if (K < 128 || K > kMaxGptqK) return 0;
+  return fq::gptq_factor_ws_bytes((int)K);
+}
+
+fq_status fq_gptq_factor(const double *G, int64_t K, double damp, double *U, void *ws, size_t ws_bytes,
+                         void *stream) {
+  fq_status s;
+  if ((s = check_k(K)) != FQ_OK) return s;
+  if (K > kMaxGptqK) return fail(FQ_ERR_UNSUPPORTED, "K=%lld: GPTQ handles K <= %lld", (long long)K, (long long)kMaxGptqK);
+  if (!(damp >= 0.0 && damp <= 1.0)) return fail(FQ_ERR_UNSUPPORTED, "damp=%g outside [0, 1]", damp);
+  if (!G || !U) return fail(FQ_ERR_NULL, "G and U must be non-NULL");
+  if (!aligned16(G) || !aligned16(U)) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  const size_t need = fq_gptq_factor_workspace_bytes(K);
+  if (!ws || ws_bytes < need)
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  hipError_t e = fq::launch_gptq_factor(G, (int)K, damp, U, ws, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "gptq_factor launch");
+  return ok();
+}
+
+size_t fq_gptq_sweep_workspace_bytes(int64_t N, int64_t K) {
+  if (N <= 0 || K < 128 || K > kMaxK) return 0;
+  return fq::gptq_sweep_ws_bytes(N, (int)K);
+}
+
+fq_status fq_gptq_sweep(const float *w_t, int64_t ldw, const double *U, int64_t N, int64_t K, int bits,
+                        float scale_mult, int8_t *w_codes, float *w_scale, void *ws, size_t ws_bytes,
+                        void *stream) {
+  fq_status s;
+  if (N < 0) return fail(FQ_ERR_SHAPE, "N=%lld < 0", (long long)N);
+  if ((s = check_k(K)) != FQ_OK) return s;
+  if ((s = check_bits(bits)) != FQ_OK) return s;
+  if (ldw < K) return fail(FQ_ERR_SHAPE, "ldw=%lld < K=%lld", (long long)ldw, (long long)K);
+  if (!(scale_mult > 0.0f)) return fail(FQ_ERR_UNSUPPORTED, "scale_mult=%g must be positive", (double)scale_mult);
+  if (N > (1ll << 24)) return fail(FQ_ERR_UNSUPPORTED, "N=%lld too large", (long long)N);
+  if (N == 0) return ok();
+  if (!w_t || !U || !w_codes || !w_scale) return fail(FQ_ERR_NULL, "w_t, U, w_codes and w_scale must be non-NULL");
+  if (!aligned16(w_t) || !aligned16(U) || !aligned16(w_codes) || !aligned16(w_scale))
+    return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  const size_t need = fq_gptq_sweep_workspace_bytes(N, K);
+  if (!ws || ws_bytes < need)
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  hipError_t e = fq::launch_gptq_sweep(w_t, ldw, U, N, (int)K, bits, scale_mult, w_codes, w_scale, ws,
+                                       static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "gptq_sweep launch");
+  return ok();
 }
 
 }  // extern "C"

@@ -91,4 +91,15 @@ struct W16Args {
 W16Plan plan_w4a16(int64_t M, int64_t N, int64_t K);
 hipError_t launch_w4a16(const W16Args &g, const W16Plan &pl, void *ws, hipStream_t s);
 
+// GPTQ in the transformed coordinates (fq_gptq.hip)
+hipError_t launch_transform(const void *x, bool x_is_f32, int64_t ldx, const float *pre, const float *post,
+                            int64_t M, int K, int b, float *z, hipStream_t s);
+hipError_t launch_gptq_hessian(const float *z, int64_t ldz, int64_t T, int K, double *G, bool accumulate,
+                               hipStream_t s);
+size_t gptq_factor_ws_bytes(int K);
+hipError_t launch_gptq_factor(const double *G, int K, double damp, double *U, void *ws, hipStream_t s);
+size_t gptq_sweep_ws_bytes(int64_t N, int K);
+hipError_t launch_gptq_sweep(const float *w, int64_t ldw, const double *U, int64_t N, int K, int bits,
+                             float scale_mult, int8_t *codes, float *scales, void *ws, hipStream_t s);
+
 }  // namespace fq

@@ -23,6 +23,8 @@ EXPORTED = ["fq_fwht_quant", "fq_quantize_weights", "fq_packed_weight_bytes", "f
             "fq_unpack_weights", "fq_gemm_workspace_bytes", "fq_gemm_w4a4", "fq_gemm_w8a8",
             "fq_linear_workspace_bytes", "fq_linear", "fq_gemm_w4a16_workspace_bytes", "fq_gemm_w4a16",
             "fq_rotate_quant_workspace_bytes", "fq_rotate_quant", "fq_quantize_weights_rotated",
+            "fq_transform", "fq_gptq_hessian", "fq_gptq_factor_workspace_bytes", "fq_gptq_factor",
+            "fq_gptq_sweep_workspace_bytes", "fq_gptq_sweep",
             "fq_status_string", "fq_last_error"]
 
 
@@ -49,6 +51,10 @@ def _load() -> ctypes.CDLL:
         "fq_gemm_w4a16": [vp, i64, vp, vp, vp, vp, i64, vp, i64, i64, i64, vp, sz, vp],
         "fq_rotate_quant": [vp, i64, vp, vp, vp, vp, i64, i64, i32, i32, f32, vp, vp, vp, sz, vp],
         "fq_quantize_weights_rotated": [vp, i64, vp, vp, vp, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp],
+        "fq_transform": [vp, i32, i64, vp, vp, i64, i64, i32, vp, vp],
+        "fq_gptq_hessian": [vp, i64, i64, i64, vp, i32, vp],
+        "fq_gptq_factor": [vp, i64, ctypes.c_double, vp, vp, sz, vp],
+        "fq_gptq_sweep": [vp, i64, vp, i64, i64, i32, f32, vp, vp, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -58,7 +64,9 @@ def _load() -> ctypes.CDLL:
                        "fq_gemm_workspace_bytes": [i64, i64, i64, i32],
                        "fq_linear_workspace_bytes": [i64, i64, i64, i32],
                        "fq_gemm_w4a16_workspace_bytes": [i64, i64, i64],
-                       "fq_rotate_quant_workspace_bytes": [i64, i64]}.items():
+                       "fq_rotate_quant_workspace_bytes": [i64, i64],
+                       "fq_gptq_factor_workspace_bytes": [i64],
+                       "fq_gptq_sweep_workspace_bytes": [i64, i64]}.items():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = sz
@@ -218,6 +226,66 @@ def quantize_weights_rotated(w: torch.Tensor, perm: Optional[torch.Tensor], bloc
                                            _p(post_scale), N, K, b, bits, _p(codes), _p(scale), _p(ws),
                                            ws.numel(), _stream()))
     return codes, scale
+
+
+def transform(x: torch.Tensor, b: int, pre_mult: Optional[torch.Tensor] = None,
+              post_mult: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """The prologue's transform without quantization: bf16 or fp32 rows [M, K] -> fp32 [M, K]
+    (unnormalized blockwise butterfly between the optional multipliers)."""
+    M, K = x.shape
+    assert x.dtype in (torch.bfloat16, torch.float32) and (M == 0 or x.stride(1) == 1)
+    z = torch.empty((M, K), dtype=torch.float32, device=x.device)
+    _check(LIB.fq_transform(_p(x), int(x.dtype == torch.float32), x.stride(0) if M else K, _p(pre_mult),
+                            _p(post_mult), M, K, b, _p(z), _stream()))
+    return z
+
+
+def gptq_hessian(z: torch.Tensor, G: Optional[torch.Tensor] = None, accumulate: bool = False) -> torch.Tensor:
+    """G (+)= z^T z in fp64 for transformed tokens z fp32 [T, K]."""
+    T, K = z.shape
+    assert z.dtype == torch.float32 and (T == 0 or z.stride(1) == 1)
+    if G is None:
+        G = torch.empty((K, K), dtype=torch.float64, device=z.device)
+    _check(LIB.fq_gptq_hessian(_p(z), z.stride(0) if T else K, T, K, _p(G), int(accumulate), _stream()))
+    return G
+
+
+def gptq_factor(G: torch.Tensor, damp: float = 0.01) -> torch.Tensor:
+    """U fp64 [K, K] upper triangular with (G + damp * mean(diag G) I)^-1 = U^T U."""
+    K = G.shape[0]
+    assert G.dtype == torch.float64 and G.is_contiguous()
+    U = torch.empty((K, K), dtype=torch.float64, device=G.device)
+    ws = workspace(int(LIB.fq_gptq_factor_workspace_bytes(K)), G.device)
+    _check(LIB.fq_gptq_factor(_p(G), K, damp, _p(U), _p(ws), ws.numel(), _stream()))
+    return U
+
+
+def gptq_sweep(w_t: torch.Tensor, U: torch.Tensor, bits: int,
+               scale_mult: float = 1.0) -> Tuple[torch.Tensor, torch.Tensor]:
+    """GPTQ column sweep on transformed weight rows w_t fp32 [N, K] -> (codes int8 [N, K],
+    scales fp32 [N])."""
+    N, K = w_t.shape
+    assert w_t.dtype == torch.float32 and w_t.stride(1) == 1 and U.dtype == torch.float64 and U.is_contiguous()
+    codes = torch.empty((N, K), dtype=torch.int8, device=w_t.device)
+    scales = torch.empty((N,), dtype=torch.float32, device=w_t.device)
+    ws = workspace(int(LIB.fq_gptq_sweep_workspace_bytes(N, K)), w_t.device)
+    _check(LIB.fq_gptq_sweep(_p(w_t), w_t.stride(0), _p(U), N, K, bits, scale_mult, _p(codes), _p(scales), _p(ws),
+                             ws.numel(), _stream()))
+    return codes, scales
+
+
+def gptq_quantize_weights(w: torch.Tensor, calib: torch.Tensor, b: int, bits: int,
+                          col_scale: Optional[torch.Tensor] = None, post_scale: Optional[torch.Tensor] = None,
+                          smooth_inv: Optional[torch.Tensor] = None, post_inv: Optional[torch.Tensor] = None,
+                          damp: float = 0.01) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Eq. (7) on the GPU: calibration tokens (bf16 [T, K]) through the runtime transform,
+    G = Z Z^T, the damped factor, and the sweep over the folded weight rows (fp32 [N, K]).
+    Returns (codes int8 [N, K], scales fp32 [N]) in the layout of quantize_weights."""
+    z = transform(calib, b, smooth_inv, post_inv)
+    U = gptq_factor(gptq_hessian(z), damp)
+    w_t = transform(w, b, col_scale, post_scale)
+    c_b = float(torch.tensor(1.0 / b ** 0.5, dtype=torch.float32).item())
+    return gptq_sweep(w_t, U, bits, c_b)
 
 
 def w4a16_workspace_bytes(M: int, N: int, K: int) -> int:

@@ -181,3 +181,32 @@ def test_rotate_quant_workspace_and_empty():
     # the weight side takes fp32 rows: a leading dimension that is a multiple of 4 suffices
     assert fq.LIB.fq_quantize_weights_rotated(FAKE, 1028, NULL, NULL, NULL, NULL, 16, 1024, 64, 4, FAKE, FAKE,
                                               FAKE, 1 << 30, None) == 1
+
+
+@pytest.mark.parametrize("call,status", [
+    (lambda: fq.LIB.fq_transform(NULL, 0, 1024, NULL, NULL, 4, 1024, 64, FAKE, None), 1),
+    (lambda: fq.LIB.fq_transform(FAKE, 0, 1024, NULL, NULL, 4, 1024, 512, FAKE, None), 3),
+    (lambda: fq.LIB.fq_transform(FAKE, 1, 1026, NULL, NULL, 4, 1024, 64, FAKE, None), 4),
+    (lambda: fq.LIB.fq_gptq_hessian(FAKE, 1024, 8, 1000, FAKE, 0, None), 3),
+    (lambda: fq.LIB.fq_gptq_hessian(FAKE, 1024, 8, 32768, FAKE, 0, None), 3),
+    (lambda: fq.LIB.fq_gptq_hessian(FAKE, 512, 8, 1024, FAKE, 0, None), 2),
+    (lambda: fq.LIB.fq_gptq_hessian(FAKE, 1024, 8, 1024, NULL, 0, None), 1),
+    (lambda: fq.LIB.fq_gptq_factor(FAKE, 1024, 2.0, FAKE, FAKE, 1 << 40, None), 3),
+    (lambda: fq.LIB.fq_gptq_factor(FAKE, 1024, 0.01, FAKE, FAKE, 8, None), 5),
+    (lambda: fq.LIB.fq_gptq_factor(FAKE, 1024, 0.01, MISALIGNED, FAKE, 1 << 40, None), 4),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 3, 1.0, FAKE, FAKE, FAKE, 1 << 40, None), 3),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1000, FAKE, 16, 1024, 4, 1.0, FAKE, FAKE, FAKE, 1 << 40, None), 2),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, NULL, 16, 1024, 4, 1.0, FAKE, FAKE, FAKE, 1 << 40, None), 1),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 4, 0.0, FAKE, FAKE, FAKE, 1 << 40, None), 3),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 4, 1.0, FAKE, FAKE, FAKE, 64, None), 5),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 0, 1024, 4, 1.0, NULL, NULL, NULL, 0, None), 0),
+])
+def test_gptq_rejects(call, status):
+    assert call() == status
+
+
+def test_gptq_workspace_sizes():
+    assert fq.LIB.fq_gptq_factor_workspace_bytes(1024) >= 2 * 1024 * 1024 * 8
+    assert fq.LIB.fq_gptq_factor_workspace_bytes(32768) == 0
+    assert fq.LIB.fq_gptq_sweep_workspace_bytes(64, 1024) >= 64 * 1024 * 8
+    assert fq.LIB.fq_gptq_sweep_workspace_bytes(0, 1024) == 0
