@@ -32,6 +32,7 @@ HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
 INT8_PEAK_TOPS = 5000.0    # MI355X dense INT8 MFMA, TOPS (no INT4 MFMA on gfx950)
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s (the W4A16 path)
 FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector ALU, TFLOP/s (the composite rotation's fma chains)
+FP64_PEAK_TFLOPS = 78.6        # MI355X fp64 vector ALU, TFLOP/s (the GPTQ stages)
 
 
 def parse():
@@ -297,6 +298,46 @@ def measure_points(torch, fq, synth, dev, log_fn):
     run_point("down_w4a16_m1", 1, 16384, 2048, 1, 4, "w4a16")
     run_point("down_w4a16_m16", 16, 16384, 2048, 1, 4, "w4a16")
     out += measure_prologue_points(torch, fq, synth, dev, log_fn)
+    out += measure_gptq_points(torch, fq, synth, dev, log_fn)
+    return out
+
+
+def measure_gptq_points(torch, fq, synth, dev, log_fn):
+    """GPTQ in the transformed coordinates (offline): each stage timed with events over one
+    call after a warm-up call.  Algorithmic fp64 flops: second moment T K (K + 1) (the
+    distinct entries), factor 2 K^3 / 3 (Cholesky and triangular inverse), sweep N K^2."""
+    out = []
+    for (name, N, K, T) in (("ae_qkv_gptq", 1536, 1024, 2048), ("ae_down_gptq", 1024, 4096, 2048)):
+        b = 128
+        calib = synth.activations(T, K, seed=K + 5, outlier_frac=0.005, outlier_scale=50.0).to(dev)
+        w = torch.from_numpy(synth.weights(N, K, seed=K + N)).to(dev)
+        c_b = float(torch.tensor(1.0 / b ** 0.5, dtype=torch.float32).item())
+        z = fq.transform(calib, b)
+        w_t = fq.transform(w, b)
+        G = fq.gptq_hessian(z)
+        U = fq.gptq_factor(G)
+        stages = (("hessian", lambda: fq.gptq_hessian(z, G), T * K * (K + 1)),
+                  ("factor", lambda: fq.gptq_factor(G), 2 * K ** 3 / 3),
+                  ("sweep", lambda: fq.gptq_sweep(w_t, U, 4, c_b), N * K ** 2))
+        rec = {"name": name, "kind": "gptq", "N": N, "K": K, "T": T, "b": b, "bits": 4}
+        total = 0.0
+        for sname, fn, flops in stages:
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3
+            total += us
+            rec[f"{sname}_us"] = round(us, 1)
+            rec[f"{sname}_fp64_frac"] = round(flops / (us * 1e-6) / (FP64_PEAK_TFLOPS * 1e12), 4)
+        rec["total_us"] = round(total, 1)
+        log_fn(json.dumps(rec))
+        out.append(rec)
+        del calib, w, z, w_t, G, U
+        torch.cuda.empty_cache()
     return out
 
 
