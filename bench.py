@@ -80,11 +80,15 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "site_traffic.json")
 CSRC = os.path.join(ROOT, "paper_2609_24433_amd", "csrc")
 
 
+TRAFFIC_SOURCES = ("fq_api.cpp", "fq_codes.hpp", "fq_device.hpp", "fq_gemm.hip", "fq_quant.hip")  # what a site's projection runs
+
+
 def sources_digest():
-    """SHA-256 over the HIP/C++ sources: counter readings are void once the kernels change."""
+    """SHA-256 over the sources of the kernels a fused projection runs (and the entry point
+    that plans them): counter readings are void once any of them changes."""
     import hashlib
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
+    for name in TRAFFIC_SOURCES:
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()

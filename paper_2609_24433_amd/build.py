@@ -20,7 +20,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfq.so")
-SOURCES = ["fq_api.cpp", "fq_quant.hip", "fq_gemm.hip", "fq_gptq.hip"]
+SOURCES = ["fq_api.cpp", "fq_quant.hip", "fq_rotate.hip", "fq_gemm.hip", "fq_gptq.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [
