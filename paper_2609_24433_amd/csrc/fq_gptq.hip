@@ -9,8 +9,9 @@
 //   factor: U upper triangular with (G + lambda I)^-1 = U^T U.  With the index reversal
 //     P, the lower Cholesky factor L of A = P H P gives H = V V^T for the upper triangular
 //     V = P L P, so U = V^-1 = P L^-1 P: a blocked Cholesky (64-wide diagonal blocks in
-//     LDS, row-parallel triangular solves, fp64 product updates of the trailing matrix)
-//     and a blocked triangular inverse;
+//     one wave's registers, row-parallel triangular solves, fp64 product updates of the
+//     trailing matrix) and a triangular inverse that merges neighbouring diagonal blocks
+//     level by level, so its large products run with many tiles;
 //   sweep: the lazy-batch column sweep in fp64, 128 columns per block: inside a block the
 //     columns are rounded one at a time for 16 rows per workgroup with the rows' block in
 //     LDS; after the block one fp64 product pushes the block's errors onto the later
@@ -94,6 +95,8 @@ struct DProd {
   int64_t m, n, kd;
   int mode;
   int lower, mirror;
+  int kskip;  // B is lower triangular: tile column j0 sums k >= j0 only (the rest are zeros)
+  int klow;   // A is lower triangular: tile row i0 sums k < i0 + 64 only
 };
 
 template <typename TA, typename TB>
@@ -115,7 +118,8 @@ __global__ __launch_bounds__(256) void dprod_kernel(DProd p) {
     for (int c = 0; c < 4; ++c) acc[r][c] = 0.0;
   const bool a_krun = p.a_sk == 1;  // consecutive lanes along k when k is the contiguous index
   const bool b_jrun = p.b_sj == 1;
-  for (int64_t k0 = 0; k0 < p.kd; k0 += KC) {
+  const int64_t kend = p.klow && i0 + T < p.kd ? i0 + T : p.kd;
+  for (int64_t k0 = p.kskip ? j0 : 0; k0 < kend; k0 += KC) {
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < (T * KC) / 256; ++u) {
@@ -128,7 +132,7 @@ __global__ __launch_bounds__(256) void dprod_kernel(DProd p) {
       bs[kb][jj] = (gj < p.n && gkb < p.kd) ? (double)Bm[gkb * p.b_sk + gj * p.b_sj] : 0.0;
     }
     __syncthreads();
-    const int kn = (int)(p.kd - k0 < KC ? p.kd - k0 : KC);
+    const int kn = (int)(kend - k0 < KC ? kend - k0 : KC);
     for (int k = 0; k < kn; ++k) {
       double av[4], bv[4];
 #pragma unroll
@@ -240,74 +244,85 @@ __global__ __launch_bounds__(256) void reverse_kernel(const double *G, int K, co
 
 constexpr int kNb = 64;  // Cholesky / inverse block
 
-// Cholesky of the diagonal block at k0 (lower), in LDS; the block's upper part is zeroed.
-__global__ __launch_bounds__(256) void potrf_block_kernel(double *A, int K, int k0) {
-  __shared__ double l[kNb][kNb + 1];
-  const int tid = threadIdx.x;
-  for (int e = tid; e < kNb * kNb; e += 256) {
-    const int i = e / kNb, j = e % kNb;
-    l[i][j] = A[(int64_t)(k0 + i) * K + k0 + j];
-  }
-  __syncthreads();
+// The three small dense kernels of the factor run one wave per 64 x 64 block, each lane
+// holding one row (or column) of 64 doubles in registers, every loop fully unrolled so the
+// register indices are static; the entries other lanes need go through LDS.
+
+// Cholesky of the diagonal block at k0 (lower), right-looking: lane i holds row i.  At step
+// j every lane publishes its entry j, reads the pivot d = sqrt(l_jj) and 1/d, and takes
+// column j's scaled entries l_cj = l_cj * (1/d) from LDS (the same product its owner forms),
+// then updates its entries j < c <= i.  Selects, no divergent branches.  The block's upper
+// part is written as zeros.
+__global__ __launch_bounds__(64) void potrf_block_kernel(double *A, int K, int k0) {
+  __shared__ double col[kNb];
+  const int i = threadIdx.x;
+  double r[kNb];
+  const double *src = A + (int64_t)(k0 + i) * K + k0;
+#pragma unroll
+  for (int c = 0; c < kNb; ++c) r[c] = src[c];
+#pragma unroll
   for (int j = 0; j < kNb; ++j) {
-    if (tid == 0) l[j][j] = sqrt(l[j][j]);
+    col[i] = r[j];
     __syncthreads();
-    if (tid > j && tid < kNb) l[tid][j] = l[tid][j] / l[j][j];
-    __syncthreads();
-    for (int e = tid; e < kNb * kNb; e += 256) {
-      const int i = e / kNb, c = e % kNb;
-      if (c > j && i >= c) l[i][c] = l[i][c] - l[i][j] * l[c][j];
+    const double d = sqrt(col[j]);
+    const double inv = 1.0 / d;
+    r[j] = i > j ? r[j] * inv : (i == j ? d : r[j]);
+#pragma unroll
+    for (int c = j + 1; c < kNb; ++c) {
+      const double lc = col[c] * inv;
+      r[c] = c <= i ? r[c] - r[j] * lc : r[c];
+      if ((c & 7) == 7) __builtin_amdgcn_sched_barrier(0);  // few LDS values live at a time
     }
     __syncthreads();
   }
-  for (int e = tid; e < kNb * kNb; e += 256) {
-    const int i = e / kNb, j = e % kNb;
-    A[(int64_t)(k0 + i) * K + k0 + j] = j <= i ? l[i][j] : 0.0;
-  }
+  double *dst = A + (int64_t)(k0 + i) * K + k0;
+#pragma unroll
+  for (int c = 0; c < kNb; ++c) dst[c] = c <= i ? r[c] : 0.0;
 }
 
-// Rows i >= k0 + 64 of the panel: x L_kk^T = a by forward substitution, one thread per
-// row, 32 rows per workgroup (the block and the rows fit the 64 KB of static LDS).
-__global__ __launch_bounds__(32) void trsm_rows_kernel(double *A, int K, int k0) {
-  __shared__ double l[kNb][kNb];   // read at wave-uniform indices only
-  __shared__ double xs[kNb][32];   // [column][thread]
+// Rows i >= k0 + 64 of the panel: x L_kk^T = a, one lane per row (64 per workgroup), the
+// row in registers: x_c = x_c / l_cc, then x_c' -= x_c l_c'c for the later c' (each entry's
+// subtractions in ascending c, the same arithmetic as the dot-product form).
+__global__ __launch_bounds__(64) void trsm_rows_kernel(double *A, int K, int k0) {
+  __shared__ double l[kNb][kNb];  // read at wave-uniform indices only
   const int tid = threadIdx.x;
-  for (int e = tid; e < kNb * kNb; e += 32) {
-    const int i = e / kNb, j = e % kNb;
-    l[i][j] = A[(int64_t)(k0 + i) * K + k0 + j];
-  }
-  const int64_t row = (int64_t)k0 + kNb + (int64_t)blockIdx.x * 32 + tid;
-  const bool ok = row < K;
-  for (int c = 0; c < kNb; ++c) xs[c][tid] = ok ? A[row * K + k0 + c] : 0.0;
+  for (int e = tid; e < kNb * kNb; e += 64) l[e / kNb][e % kNb] = A[(int64_t)(k0 + e / kNb) * K + k0 + e % kNb];
+  const int64_t row = (int64_t)k0 + kNb + (int64_t)blockIdx.x * 64 + tid;
+  const int64_t rr = row < K ? row : K - 1;  // lanes past the end solve a copy of the last row, unstored
+  double x[kNb];
+#pragma unroll
+  for (int c = 0; c < kNb; ++c) x[c] = A[rr * K + k0 + c];
   __syncthreads();
+#pragma unroll
   for (int c = 0; c < kNb; ++c) {
-    double v = xs[c][tid];
-    for (int j = 0; j < c; ++j) v = v - xs[j][tid] * l[c][j];
-    xs[c][tid] = v / l[c][c];
+    x[c] = x[c] / l[c][c];
+#pragma unroll
+    for (int c2 = c + 1; c2 < kNb; ++c2) x[c2] = x[c2] - x[c] * l[c2][c];
   }
-  if (ok)
-    for (int c = 0; c < kNb; ++c) A[row * K + k0 + c] = xs[c][tid];
+  if (row < K)
+#pragma unroll
+    for (int c = 0; c < kNb; ++c) A[row * K + k0 + c] = x[c];
 }
 
-// X_ii = L_ii^-1 for every diagonal block (grid = K / 64 x 2): thread t of half h solves
-// column 32 h + t by forward substitution.
-__global__ __launch_bounds__(32) void triinv_block_kernel(const double *A, int K, double *X) {
-  __shared__ double l[kNb][kNb];   // read at wave-uniform indices only
-  __shared__ double xs[kNb][32];   // [row][thread]
-  const int tid = threadIdx.x;
+// X_ii = L_ii^-1 for every diagonal block (grid = K / 64): lane c computes column c,
+// x = e_c, then x_m = x_m / l_mm and x_r -= l_rm x_m for r > m, m ascending.
+__global__ __launch_bounds__(64) void triinv_block_kernel(const double *A, int K, double *X) {
+  __shared__ double l[kNb][kNb];  // read at wave-uniform indices only
+  const int c = threadIdx.x;
   const int k0 = blockIdx.x * kNb;
-  const int c = blockIdx.y * 32 + tid;
-  for (int e = tid; e < kNb * kNb; e += 32) {
-    const int i = e / kNb, j = e % kNb;
-    l[i][j] = A[(int64_t)(k0 + i) * K + k0 + j];
-  }
+  for (int e = c; e < kNb * kNb; e += 64) l[e / kNb][e % kNb] = A[(int64_t)(k0 + e / kNb) * K + k0 + e % kNb];
   __syncthreads();
-  for (int r = 0; r < kNb; ++r) {
-    double v = r == c ? 1.0 : 0.0;
-    for (int m = 0; m < r; ++m) v = v - l[r][m] * xs[m][tid];
-    xs[r][tid] = r < c ? 0.0 : v / l[r][r];
+  double x[kNb];
+#pragma unroll
+  for (int r = 0; r < kNb; ++r) x[r] = r == c ? 1.0 : 0.0;
+#pragma unroll
+  for (int m = 0; m < kNb; ++m) {
+    x[m] = x[m] / l[m][m];
+#pragma unroll
+    for (int r = m + 1; r < kNb; ++r) x[r] = x[r] - l[r][m] * x[m];
   }
-  for (int r = 0; r < kNb; ++r) X[(int64_t)(k0 + r) * K + k0 + c] = xs[r][tid];
+#pragma unroll
+  for (int r = 0; r < kNb; ++r) X[(int64_t)(k0 + r) * K + k0 + c] = x[r];
 }
 
 // U[i][j] = X[K-1-i][K-1-j] on and above the diagonal, 0 below.
@@ -319,14 +334,14 @@ __global__ __launch_bounds__(256) void unreverse_kernel(const double *X, int K, 
 }
 
 size_t gptq_factor_ws_bytes(int K) {
-  return ((size_t)2 * K * K + (size_t)kNb * K) * sizeof(double) + 256;
+  return ((size_t)2 * K * K + (size_t)(K / 2) * (K / 2)) * sizeof(double) + 256;
 }
 
 hipError_t launch_gptq_factor(const double *G, int K, double damp, double *U, void *ws, hipStream_t s) {
   double *A = static_cast<double *>(ws);
   double *X = A + (size_t)K * K;
-  double *Tm = X + (size_t)K * K;  // [64, K] products of the inverse's block rows
-  double *lam = Tm + (size_t)kNb * K;
+  double *Tm = X + (size_t)K * K;  // B X_A of the inverse's merges, at most (K/2) x (K/2)
+  double *lam = Tm + (size_t)(K / 2) * (K / 2);
   const int64_t n = (int64_t)K * K;
   const unsigned ge = (unsigned)((n + 255) / 256);
   hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, G, K, damp, lam);
@@ -335,10 +350,10 @@ hipError_t launch_gptq_factor(const double *G, int K, double damp, double *U, vo
   if (e != hipSuccess) return e;
   // blocked Cholesky, lower: A = L L^T in place
   for (int k0 = 0; k0 < K; k0 += kNb) {
-    hipLaunchKernelGGL(potrf_block_kernel, dim3(1), dim3(256), 0, s, A, K, k0);
+    hipLaunchKernelGGL(potrf_block_kernel, dim3(1), dim3(64), 0, s, A, K, k0);
     const int rest = K - k0 - kNb;
     if (rest > 0) {
-      hipLaunchKernelGGL(trsm_rows_kernel, dim3((unsigned)((rest + 31) / 32)), dim3(32), 0, s, A, K, k0);
+      hipLaunchKernelGGL(trsm_rows_kernel, dim3((unsigned)((rest + 63) / 64)), dim3(64), 0, s, A, K, k0);
       DProd p{};
       p.a = A + (int64_t)(k0 + kNb) * K + k0;  // L[i][k0 + k]
       p.a_si = K;
@@ -357,39 +372,46 @@ hipError_t launch_gptq_factor(const double *G, int K, double damp, double *U, vo
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  // blocked inverse X = L^-1: diagonal blocks first, then block row i from rows < i:
-  // X[i, :i] = -X_ii (L[i, :i] X[:i, :i])
-  hipLaunchKernelGGL(triinv_block_kernel, dim3((unsigned)(K / kNb), 2), dim3(32), 0, s, A, K, X);
+  // X = L^-1: the 64-wide diagonal blocks' inverses, then pairs of neighbouring diagonal
+  // blocks merged level by level (widths 64, 128, 256, ...): for A = block 2t, C = block
+  // 2t + 1 (possibly narrower at the end) and B the part of L below A and left of C,
+  // X[C, A] = -X_C (B X_A).  Both products skip the zeros of their triangular operand.
+  hipLaunchKernelGGL(triinv_block_kernel, dim3((unsigned)(K / kNb)), dim3(64), 0, s, A, K, X);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  for (int i0 = kNb; i0 < K; i0 += kNb) {
-    DProd p{};
-    p.a = A + (int64_t)i0 * K;  // L[i0 + r][k]
-    p.a_si = K;
-    p.a_sk = 1;
-    p.b = X;  // X[k][j]
-    p.b_sk = K;
-    p.b_sj = 1;
-    p.c = Tm;
-    p.ldc = K;
-    p.m = kNb;
-    p.n = i0;
-    p.kd = i0;
-    p.mode = kSet;
-    if ((e = dprod<double, double>(p, s)) != hipSuccess) return e;
-    DProd q{};
-    q.a = X + (int64_t)i0 * K + i0;  // X_ii[r][k]
-    q.a_si = K;
-    q.a_sk = 1;
-    q.b = Tm;  // Tm[k][j]
-    q.b_sk = K;
-    q.b_sj = 1;
-    q.c = X + (int64_t)i0 * K;
-    q.ldc = K;
-    q.m = kNb;
-    q.n = i0;
-    q.kd = kNb;
-    q.mode = kSetNeg;
-    if ((e = dprod<double, double>(q, s)) != hipSuccess) return e;
+  for (int n = kNb; n < K; n *= 2) {
+    for (int o = 0; o + n < K; o += 2 * n) {
+      const int n2 = o + 2 * n <= K ? n : K - o - n;  // width of C
+      DProd p{};
+      p.a = A + (int64_t)(o + n) * K + o;  // B[r][k] = L[o + n + r][o + k]
+      p.a_si = K;
+      p.a_sk = 1;
+      p.b = X + (int64_t)o * K + o;  // X_A[k][j]
+      p.b_sk = K;
+      p.b_sj = 1;
+      p.c = Tm;
+      p.ldc = n;
+      p.m = n2;
+      p.n = n;
+      p.kd = n;
+      p.mode = kSet;
+      p.kskip = 1;
+      if ((e = dprod<double, double>(p, s)) != hipSuccess) return e;
+      DProd q{};
+      q.a = X + (int64_t)(o + n) * K + o + n;  // X_C[r][k]
+      q.a_si = K;
+      q.a_sk = 1;
+      q.b = Tm;  // Tm[k][j]
+      q.b_sk = n;
+      q.b_sj = 1;
+      q.c = X + (int64_t)(o + n) * K + o;
+      q.ldc = K;
+      q.m = n2;
+      q.n = n;
+      q.kd = n2;
+      q.mode = kSetNeg;
+      q.klow = 1;
+      if ((e = dprod<double, double>(q, s)) != hipSuccess) return e;
+    }
   }
   hipLaunchKernelGGL(unreverse_kernel, dim3(ge), dim3(256), 0, s, X, K, U);
   return hipGetLastError();

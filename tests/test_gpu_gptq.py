@@ -79,7 +79,7 @@ def test_hessian_within_summation_bound(T, K):
     assert not G0.cpu().numpy().any()
 
 
-@pytest.mark.parametrize("K", [128, 256, 1024])
+@pytest.mark.parametrize("K", [128, 256, 384, 640, 1024])
 def test_factor_matches_oracle(K):
     flush(f"gptq_factor K={K}")
     f = fq()
