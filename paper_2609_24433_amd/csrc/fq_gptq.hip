@@ -13,7 +13,7 @@
 //     trailing matrix) and a triangular inverse that merges neighbouring diagonal blocks
 //     level by level, so its large products run with many tiles;
 //   sweep: the lazy-batch column sweep in fp64, 128 columns per block: inside a block the
-//     columns are rounded one at a time for 16 rows per workgroup with the rows' block in
+//     columns are rounded one at a time for 4 rows per workgroup with the rows' block in
 //     LDS; after the block one fp64 product pushes the block's errors onto the later
 //     columns.  Every operation and its order follow the fp64 contract of the sweep, so the
 //     codes are reproducible bit for bit.
@@ -421,7 +421,7 @@ hipError_t launch_gptq_factor(const double *G, int K, double damp, double *U, vo
 // sweep
 
 constexpr int kSweepBlk = 128;  // columns per lazy batch
-constexpr int kSweepRows = 16;  // rows per in-block workgroup
+constexpr int kSweepRows = 4;   // rows per in-block workgroup (the column steps are latency-bound: more workgroups)
 
 // Per row: A = max |w| (fp32, exact), the fp32 scale, fp64 inv = q / A and step = A / q,
 // and the fp64 working copy.  One workgroup per row.
@@ -451,9 +451,9 @@ __global__ __launch_bounds__(256) void sweep_init_kernel(const float *w, int64_t
   }
 }
 
-// Columns [i1, i1 + 128) of 16 rows, one at a time: code, error, and the error pushed onto
+// Columns [i1, i1 + 128) of 4 rows, one at a time: code, error, and the error pushed onto
 // the block's later columns; the errors go to e [N, 128] for the product update.
-__global__ __launch_bounds__(256) void sweep_block_kernel(const double *U, int64_t N, int K, int bits, int i1,
+__global__ __launch_bounds__(128) void sweep_block_kernel(const double *U, int64_t N, int K, int bits, int i1,
                                                           const double *rowp, double *w64, int8_t *codes,
                                                           double *e) {
   __shared__ double wb[kSweepRows][kSweepBlk + 1];
@@ -461,7 +461,7 @@ __global__ __launch_bounds__(256) void sweep_block_kernel(const double *U, int64
   const int tid = threadIdx.x;
   const int64_t r0 = (int64_t)blockIdx.x * kSweepRows;
   const double q = (double)((1 << (bits - 1)) - 1);
-  for (int x = tid; x < kSweepRows * kSweepBlk; x += 256) {
+  for (int x = tid; x < kSweepRows * kSweepBlk; x += 128) {
     const int r = x / kSweepBlk, c = x % kSweepBlk;
     wb[r][c] = r0 + r < N ? w64[(r0 + r) * K + i1 + c] : 0.0;
   }
@@ -487,7 +487,7 @@ __global__ __launch_bounds__(256) void sweep_block_kernel(const double *U, int64
     }
     __syncthreads();
     const int rem = kSweepBlk - 1 - c;
-    for (int x = tid; x < kSweepRows * rem; x += 256) {
+    for (int x = tid; x < kSweepRows * rem; x += 128) {
       const int r = x / rem, c2 = c + 1 + x % rem;
       wb[r][c2] = __builtin_fma(-es[r], U[gc * K + i1 + c2], wb[r][c2]);
     }
@@ -513,7 +513,7 @@ hipError_t launch_gptq_sweep(const float *w, int64_t ldw, const double *U, int64
   if (err != hipSuccess) return err;
   const unsigned gb = (unsigned)((N + kSweepRows - 1) / kSweepRows);
   for (int i1 = 0; i1 < K; i1 += kSweepBlk) {
-    hipLaunchKernelGGL(sweep_block_kernel, dim3(gb), dim3(256), 0, s, U, N, K, bits, i1, rowp, w64, codes, e);
+    hipLaunchKernelGGL(sweep_block_kernel, dim3(gb), dim3(128), 0, s, U, N, K, bits, i1, rowp, w64, codes, e);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const int i2 = i1 + kSweepBlk;
     if (i2 < K) {
