@@ -157,14 +157,18 @@ __global__ __launch_bounds__(256) void rot_transform_kernel(const void *x, int64
           acc[t][3] = __builtin_fmaf(qa[buf][u].w, w, acc[t][3]);
         }
     };
+    // the reads past the last group re-read it (valid LDS, results unused): no branch in
+    // the loop, so the two register sets keep their registers instead of being copied
     load_group(0, 0);
 #pragma unroll 1
     for (int jg = 0; jg < NG; jg += 2) {
-      if (jg + 1 < NG) load_group(1, jg + 1);
+      load_group(1, jg + 1 < NG ? jg + 1 : NG - 1);
       fma_group(0);
-      if (jg + 1 < NG) {
-        if (jg + 2 < NG) load_group(0, jg + 2);
+      load_group(0, jg + 2 < NG ? jg + 2 : NG - 1);
+      if constexpr (NG % 2 == 0) {
         fma_group(1);
+      } else {
+        if (jg + 1 < NG) fma_group(1);
       }
     }
   } else {
@@ -179,24 +183,30 @@ __global__ __launch_bounds__(256) void rot_transform_kernel(const void *x, int64
     }
   }
   const int c_out = kblk * B + h * S::TI;
+  float pm[S::TI];
+#pragma unroll
+  for (int c = 0; c < S::TI; ++c) pm[c] = post_mult ? post_mult[c_out + c] : 1.0f;
 #pragma unroll
   for (int t = 0; t < TR; ++t) {
     const int64_t row = row0 + r0 + t;
     if (row < M) {
+      float v[S::TI];
 #pragma unroll
-      for (int c = 0; c < S::TI; ++c) {
-        float v = acc[t][c];
-        if (post_mult) v = v * post_mult[c_out + c];
-        z[row * K + c_out + c] = v;
+      for (int c = 0; c < S::TI; ++c) v[c] = post_mult ? acc[t][c] * pm[c] : acc[t][c];
+      if constexpr (S::TI == 4) {
+        *reinterpret_cast<float4 *>(z + row * K + c_out) = float4{v[0], v[1], v[2], v[3]};
+      } else {
+#pragma unroll
+        for (int c = 0; c < S::TI; ++c) z[row * K + c_out + c] = v[c];
       }
     }
   }
 }
 
 // One workgroup per row; thread t owns 16-channel chunks t, t + 256, ... (K <= 32768).
+template <int CPT>
 __global__ __launch_bounds__(256) void rot_quant_kernel(const float *z, int64_t M, int K, int bits, float clip_ratio,
                                                         uint8_t *codes, int64_t ld_codes, float *delta, int out_fmt) {
-  constexpr int CPT = 8;
   __shared__ float red[4];
   const int tid = threadIdx.x;
   const int64_t row = blockIdx.x;
@@ -309,8 +319,20 @@ hipError_t launch_rotate_quant(const void *x, bool x_is_f32, int64_t ldx, const 
   hipError_t e = x_is_f32 ? launch_rot_t<float>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, b, z, s)
                           : launch_rot_t<uint16_t>(x, ldx, perm, blocks, chan_mult, post_mult, M, K, b, z, s);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rot_quant_kernel, dim3((unsigned)M), dim3(256), 0, s, z, M, K, bits, clip_ratio, codes,
-                     ld_codes, delta, out_fmt);
+  // chunks per thread: the fewest that cover the row (no thread rereads a chunk it does not own)
+  const int nch = K / 16;
+  if (nch <= 256)
+    hipLaunchKernelGGL(rot_quant_kernel<1>, dim3((unsigned)M), dim3(256), 0, s, z, M, K, bits, clip_ratio, codes,
+                       ld_codes, delta, out_fmt);
+  else if (nch <= 512)
+    hipLaunchKernelGGL(rot_quant_kernel<2>, dim3((unsigned)M), dim3(256), 0, s, z, M, K, bits, clip_ratio, codes,
+                       ld_codes, delta, out_fmt);
+  else if (nch <= 1024)
+    hipLaunchKernelGGL(rot_quant_kernel<4>, dim3((unsigned)M), dim3(256), 0, s, z, M, K, bits, clip_ratio, codes,
+                       ld_codes, delta, out_fmt);
+  else
+    hipLaunchKernelGGL(rot_quant_kernel<8>, dim3((unsigned)M), dim3(256), 0, s, z, M, K, bits, clip_ratio, codes,
+                       ld_codes, delta, out_fmt);
   return hipGetLastError();
 }
 
