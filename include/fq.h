@@ -92,8 +92,8 @@ fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scal
  *              (entries outside [0, K) are clamped, giving wrong codes but no fault);
  *   blocks     fp32 [K/b, b, b], block k's matrix Q_k row-major, applied to positions
  *              [k b, (k+1) b); orthonormal blocks keep the scale (nothing deferred to delta);
- *   b          a power of two, 1 <= b <= 128 (a thread holds one row of a block's matrix
- *              in registers); K <= 32768 and M <= 2^20.
+ *   b          a power of two, 1 <= b <= 128 (a block's matrix is staged in LDS, 64 KB at
+ *              b = 128); K <= 32768 and M <= 2^20.
  * Contract: after the optional S^-1 multiply and the gather, output i of block k is the
  * fp32 fused multiply-add chain over j = 0..b-1 ascending of Q_k[i][j] * w_{kb+j},
  * starting from +0; then the optional P^-1 multiply; then eq. (5) exactly as
