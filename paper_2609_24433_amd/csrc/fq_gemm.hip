@@ -945,6 +945,22 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       pl.mt = 1;
       pl.rb = (int)((M + 15) / 16);
     }
+    // Long K with 33-64 rows (nibble codes): one 16-row tile per workgroup and 128 k steps
+    // per slice (the whole of K = 16384), 32 output channels per workgroup.  Each
+    // workgroup streams four times the weights of the 64-row plan (its sibling row blocks
+    // share them through the XCD's L2), but K needs no split: the split-K epilogue goes
+    // away.  Measured at M = 50, K 16384 -> N 2048: 11.1 against 11.7 us.
+    if (bits == 4 && M > 32 && ktot >= 128 && tune.splits <= 0 && tune.kt <= 0 && tune.wk <= 0 && tune.rb <= 0 &&
+        tune.wc <= 0) {
+      pl.mt = 1;
+      pl.rb = (int)((M + 15) / 16);
+      pl.wk = 4;
+      pl.kt = 32;
+      pl.ksteps = 128;
+      pl.splits = (ktot + 127) / 128;
+      pl.wc = 2;
+      pl.tiles = (N + 31) / 32;
+    }
     if (tune.rb > 1) {
       const int t16 = (int)((M + 15) / 16);
       const int per = (t16 + tune.rb - 1) / tune.rb;  // 16-row tiles per row block
@@ -1009,9 +1025,13 @@ static hipError_t launch_stream_wc(const GemmParams &p, int kt, int wk, dim3 gri
       case 1: return launch_stream<BITS, AFMT, MT, 1, 4, WC>(p, grid, s);
       case 2: return launch_stream<BITS, AFMT, MT, 2, 4, WC>(p, grid, s);
       case 4: return launch_stream<BITS, AFMT, MT, 4, 4, WC>(p, grid, s);
-      default:
+      case 8:
         if constexpr (AFMT == kANibble) return launch_stream<BITS, AFMT, MT, 8, 4, WC>(p, grid, s);
         return hipErrorInvalidValue;  // a 32-step int8 slice does not fit in LDS
+      default:
+        // one 16-row tile over 128 k steps (nibble codes): the whole of K = 16384 in one slice
+        if constexpr (AFMT == kANibble && MT == 1 && WC == 2) return launch_stream<BITS, AFMT, MT, 32, 4, WC>(p, grid, s);
+        return hipErrorInvalidValue;
     }
   }
   if (wk == 2) {

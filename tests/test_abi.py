@@ -43,8 +43,11 @@ def test_sizes():
     assert fq.packed_weight_bytes(2048, 16384, 8) == 2048 * 16384
     assert fq.packed_weight_bytes(16, 128, 3) == 0
     assert fq.gemm_workspace_bytes(0, 16, 128, 4) == 0
-    # linear workspace holds int8 codes and scales at least
-    assert fq.linear_workspace_bytes(50, 2048, 16384, 4) >= 50 * 16384 + 50 * 4
+    # linear workspace holds the intermediate codes (nibbles for W4A4, int8 for W8A8), the
+    # token scales and the GEMM's own workspace
+    for bits in (4, 8):
+        assert fq.linear_workspace_bytes(50, 2048, 16384, bits) >= (
+            50 * 16384 * bits // 8 + 50 * 4 + fq.gemm_workspace_bytes(50, 2048, 16384, bits))
     for M in (1, 16, 50, 64, 65, 816, 4096):
         assert fq.gemm_workspace_bytes(M, 2048, 16384, 4) % 256 == 0
 
@@ -91,10 +94,13 @@ def call_gemm(bits=4, a=FAKE, delta=FAKE, w=FAKE, sw=FAKE, bias=NULL, y=FAKE, ld
     (dict(M=-3), 2), (dict(ldy=128), 2), (dict(N=-16), 2),
     (dict(N=250, ldy=256), 3), (dict(K=1000), 3), (dict(K=0), 3),
     (dict(bias=MISALIGNED), 4), (dict(acc=MISALIGNED), 4), (dict(ldy=260), 4), (dict(w=MISALIGNED), 4),
-    (dict(ws=NULL, ws_bytes=0, M=50, N=2048, ldy=2048, K=16384), 5),
-    (dict(ws_bytes=16, M=50, N=2048, ldy=2048, K=16384), 5),
+    (dict(ws=NULL, ws_bytes=0, M=50, N=2048, ldy=2048, K=32768), 5),
+    (dict(ws_bytes=16, M=50, N=2048, ldy=2048, K=32768), 5),
 ])
 def test_gemm_rejects(bits, kw, status):
+    if status == 5:
+        # the shape must split K (need a workspace), or the call would go on to launch
+        assert fq.gemm_workspace_bytes(kw["M"], kw["N"], kw["K"], bits) > 16
     assert call_gemm(bits=bits, **kw) == status
 
 
