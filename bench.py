@@ -11,7 +11,10 @@ a site packed as one weight matrix.  Weights are folded, rounded and packed on t
 device before timing; inputs are resident in HBM when the timed region starts.
 
 Each denoising step is captured into a HIP graph and the timed region replays K of
-them.  Prints ONE JSON line.
+them.  Prints ONE JSON line, which also carries `points`: the graded single projections
+(down-projection K 16384 -> N 2048 at M = 50 / 816 / 4096 and gate-projection M = 816,
+cold weights), the weight-only INT4 projection, the prologue alone with the composite
+rotation beside the block Hadamard, and the offline GPTQ stages.
 
   python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points] [--only-points]
 """
