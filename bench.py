@@ -304,8 +304,35 @@ def measure_points(torch, fq, synth, dev, log_fn):
     run_point("adaln_w4a16_m1", 1, 1024, 6144, 1, 4, "w4a16")
     run_point("down_w4a16_m1", 1, 16384, 2048, 1, 4, "w4a16")
     run_point("down_w4a16_m16", 16, 16384, 2048, 1, 4, "w4a16")
+    out += measure_bf16_context(torch, synth, dev, log_fn, out)
     out += measure_prologue_points(torch, fq, synth, dev, log_fn)
     out += measure_gptq_points(torch, fq, synth, dev, log_fn)
+    return out
+
+
+def measure_bf16_context(torch, synth, dev, log_fn, pts):
+    """Context only (the analog of the paper's floating-point engine control): the same
+    down-projection shapes as a plain bf16 matrix product (torch.matmul, the vendor GEMM
+    library), weights rotating through >= 1 GiB of copies like the W4A4 points.  Each record
+    carries the fused W4A4 projection's speed-up over it."""
+    out = []
+    lin_us = {(p["M"], p["K"], p["N"]): p["us"] for p in pts if p["kind"] == "linear" and p["bits"] == 4}
+    for (M, K, N) in ((50, 16384, 2048), (816, 16384, 2048), (816, 2048, 16384)):
+        wt = torch.from_numpy(synth.weights(N, K, seed=K + N).T.copy()).to(dev).to(torch.bfloat16)  # [K, N]
+        copies = max(2, min(64, (1 << 30) // (wt.numel() * 2) + 1))
+        ws = [wt.clone() for _ in range(copies)]
+        del wt
+        x = synth.activations(M, K, seed=M + K, outlier_frac=0.005, outlier_scale=50.0).to(dev)
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        g = graph_of(torch, lambda i: torch.matmul(x, ws[i % copies], out=y), copies)
+        us = time_graph(torch, g, max(1, 200 // copies)) / copies * 1e6
+        rec = {"name": f"context_bf16_matmul_m{M}_k{K}_n{N}", "kind": "bf16_matmul", "M": M, "K": K, "N": N,
+               "us": round(us, 3), "TFLOPS": round(2.0 * M * N * K / us / 1e6, 2),
+               "w4a4_linear_speedup": round(us / lin_us[(M, K, N)], 2) if (M, K, N) in lin_us else None}
+        log_fn(json.dumps(rec))
+        out.append(rec)
+        del ws, x, y, g
+        torch.cuda.empty_cache()
     return out
 
 
