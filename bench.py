@@ -254,13 +254,14 @@ def measure_points(torch, fq, synth, dev, log_fn):
     they come from HBM; each point is a graph of back-to-back calls timed with events."""
     out = []
 
-    def run_point(name, M, K, N, b, bits, kind):
+    def run_point(name, M, K, N, b, bits, kind, warm=False):
         wl = synth.down_proj_sweep_point(M, b, bits) if K == 16384 else None
         w = torch.from_numpy(synth.weights(N, K, seed=K + N + bits)).to(dev)
         lin = fq.QuantLinear(w, b, bits)
         del w
         wbytes = lin.w_packed.numel()
-        copies = max(2, min(64, (1 << 30) // wbytes + 1))
+        # cold: weights rotate through >= 1 GiB of copies; warm: one copy, resident in the caches
+        copies = 1 if warm else max(2, min(64, (1 << 30) // wbytes + 1))
         wp = [lin.w_packed.clone() for _ in range(copies)]
         x = (wl.site_activation("D", 0) if wl is not None else
              synth.activations(M, K, seed=M + K, outlier_frac=0.005, outlier_scale=50.0)).to(dev)
@@ -278,12 +279,13 @@ def measure_points(torch, fq, synth, dev, log_fn):
             ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
             call = lambda i: fq.gemm(codes, delta, wp[i % copies], lin.w_scale, N, K, bits, ws=ws, out=y)
             nbytes = gemm_bytes(M, N, K, bits)
-        g = graph_of(torch, call, copies)
-        us = time_graph(torch, g, max(1, 200 // copies)) / copies * 1e6
+        calls = 50 if warm else copies
+        g = graph_of(torch, call, calls)
+        us = time_graph(torch, g, max(1, 200 // calls)) / calls * 1e6
         ops = 2.0 * M * N * K
         t_hbm = nbytes / HBM_PEAK_GBS / 1e3
         t_mfma = ops / (BF16_PEAK_TFLOPS if kind == "w4a16" else INT8_PEAK_TOPS) / 1e6
-        rec = {"name": name, "kind": kind, "M": M, "K": K, "N": N, "b": b, "bits": bits,
+        rec = {"name": name, "kind": kind, "M": M, "K": K, "N": N, "b": b, "bits": bits, "weights": "warm" if warm else "cold",
                "us": round(us, 3), "TOPS": round(ops / us / 1e6, 2), "GBps": round(nbytes / us / 1e3, 1),
                "bound": "hbm" if t_hbm >= t_mfma else "mfma",
                "roofline_frac": round(max(t_hbm, t_mfma) / us, 4)}
@@ -300,6 +302,10 @@ def measure_points(torch, fq, synth, dev, log_fn):
     run_point("down_w4a4_m816_gemm", 816, 16384, 2048, 128, 4, "gemm")
     run_point("down_w8a8_m816_linear", 816, 16384, 2048, 128, 8, "linear")
     run_point("down_w4a4_m4096_gemm", 4096, 16384, 2048, 128, 4, "gemm")
+    # warm: the same weights every call (resident in the 256 MB MALL), as shared weights are
+    # across denoising steps
+    run_point("down_w4a4_m50_linear_warm", 50, 16384, 2048, 128, 4, "linear", warm=True)
+    run_point("down_w4a4_m816_linear_warm", 816, 16384, 2048, 128, 4, "linear", warm=True)
     # weight-only INT4 (adaptive layer-norm modulation path): b = 1, no rotation
     run_point("adaln_w4a16_m1", 1, 1024, 6144, 1, 4, "w4a16")
     run_point("down_w4a16_m1", 1, 16384, 2048, 1, 4, "w4a16")
@@ -316,7 +322,8 @@ def measure_bf16_context(torch, synth, dev, log_fn, pts):
     library), weights rotating through >= 1 GiB of copies like the W4A4 points.  Each record
     carries the fused W4A4 projection's speed-up over it."""
     out = []
-    lin_us = {(p["M"], p["K"], p["N"]): p["us"] for p in pts if p["kind"] == "linear" and p["bits"] == 4}
+    lin_us = {(p["M"], p["K"], p["N"]): p["us"] for p in pts
+              if p["kind"] == "linear" and p["bits"] == 4 and p.get("weights") == "cold"}
     for (M, K, N) in ((50, 16384, 2048), (816, 16384, 2048), (816, 2048, 16384)):
         wt = torch.from_numpy(synth.weights(N, K, seed=K + N).T.copy()).to(dev).to(torch.bfloat16)  # [K, N]
         copies = max(2, min(64, (1 << 30) // (wt.numel() * 2) + 1))
