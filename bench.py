@@ -236,6 +236,20 @@ def time_graph(torch, g, replays):
     return e0.elapsed_time(e1) / 1e3 / replays
 
 
+def replay_spread(torch, g, replays):
+    """Seconds of each of `replays` replays of g, timed one by one with HIP events (for the
+    p10 / median / p90 of the per-call time)."""
+    g.replay()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(replays + 1)]
+    ev[0].record()
+    for r in range(replays):
+        g.replay()
+        ev[r + 1].record()
+    torch.cuda.synchronize()
+    return [ev[r].elapsed_time(ev[r + 1]) / 1e3 for r in range(replays)]
+
+
 def time_graph_steps(torch, graphs, K, W):
     for i in range(W):
         graphs[i % len(graphs)].replay()
@@ -251,7 +265,9 @@ def time_graph_steps(torch, graphs, K, W):
 
 def measure_points(torch, fq, synth, dev, log_fn):
     """Graded single-projection points, cold: weights rotate through >= 1 GiB of copies so
-    they come from HBM; each point is a graph of back-to-back calls timed with events."""
+    they come from HBM; each point is a graph of back-to-back calls, warmed up with >= 20
+    calls, then replayed >= 21 times with HIP events around every replay; `us` is the
+    median per-call time (p10 / p90 and the mean beside it)."""
     out = []
 
     def run_point(name, M, K, N, b, bits, kind, warm=False):
@@ -279,14 +295,24 @@ def measure_points(torch, fq, synth, dev, log_fn):
             ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
             call = lambda i: fq.gemm(codes, delta, wp[i % copies], lin.w_scale, N, K, bits, ws=ws, out=y)
             nbytes = gemm_bytes(M, N, K, bits)
+        # a graph of back-to-back calls; >= 20 warm-up calls, then 21 replays timed one by one
+        # (>= 100 calls in all): the median per-call time is the point's figure, p10 / p90 and
+        # the mean beside it
         calls = 50 if warm else copies
         g = graph_of(torch, call, calls)
-        us = time_graph(torch, g, max(1, 200 // calls)) / calls * 1e6
+        for _ in range(max(1, -(-20 // calls))):
+            g.replay()
+        reps = max(21, -(-100 // calls) | 1)
+        spread = sorted(t / calls * 1e6 for t in replay_spread(torch, g, reps))
+        us = spread[reps // 2]
+        us_mean = sum(spread) / reps
         ops = 2.0 * M * N * K
         t_hbm = nbytes / HBM_PEAK_GBS / 1e3
         t_mfma = ops / (BF16_PEAK_TFLOPS if kind == "w4a16" else INT8_PEAK_TOPS) / 1e6
         rec = {"name": name, "kind": kind, "M": M, "K": K, "N": N, "b": b, "bits": bits, "weights": "warm" if warm else "cold",
-               "us": round(us, 3), "TOPS": round(ops / us / 1e6, 2), "GBps": round(nbytes / us / 1e3, 1),
+               "us": round(us, 3), "us_p10_p90": [round(spread[reps // 10], 3), round(spread[reps - 1 - reps // 10], 3)],
+               "us_mean": round(us_mean, 3),
+               "TOPS": round(ops / us / 1e6, 2), "GBps": round(nbytes / us / 1e3, 1),
                "bound": "hbm" if t_hbm >= t_mfma else "mfma",
                "roofline_frac": round(max(t_hbm, t_mfma) / us, 4)}
         log_fn(json.dumps(rec))
