@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--traffic-site", default=None,
                     help="run only this site's fused projection 100 times (for HBM counter runs)")
+    ap.add_argument("--gemm-counters", action="store_true",
+                    help="run the tiled-GEMM points (K 16384 -> N 2048, M 816 and 4096) 10 times each, eagerly, "
+                         "for rocprofv3 --pmc runs")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 256 MiB copy-like kernel 20 times (counter calibration)")
     return ap.parse_args()
@@ -263,6 +266,22 @@ def time_graph_steps(torch, graphs, K, W):
     return e0.elapsed_time(e1) / 1e3  # seconds
 
 
+def gemm_counter_run(torch, fq, synth, dev):
+    """The tiled GEMM on the down-projection K 16384 -> N 2048 at M = 816 and 4096 (W4A4),
+    10 eager calls each, for counter collection."""
+    for M in (816, 4096):
+        K, N, b, bits = 16384, 2048, 128, 4
+        lin = fq.QuantLinear(torch.from_numpy(synth.weights(N, K, seed=K + N + bits)).to(dev), b, bits)
+        x = synth.activations(M, K, seed=M + K, outlier_frac=0.005, outlier_scale=50.0).to(dev)
+        codes, delta = fq.fwht_quant(x, b, bits)
+        ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        for _ in range(10):
+            fq.gemm(codes, delta, lin.w_packed, lin.w_scale, N, K, bits, ws=ws, out=y)
+        torch.cuda.synchronize()
+        print(json.dumps({"gemm_counters": {"M": M, "K": K, "N": N, "calls": 10}}), flush=True)
+
+
 def measure_points(torch, fq, synth, dev, log_fn):
     """Graded single-projection points, cold: weights rotate through >= 1 GiB of copies so
     they come from HBM; each point is a graph of back-to-back calls, warmed up with >= 20
@@ -465,6 +484,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(torch, dev)
+        return
+    if args.gemm_counters:
+        gemm_counter_run(torch, fq, synth, dev)
         return
     if args.traffic_site:
         traffic_run(torch, fq, synth, dev, args.traffic_site)
