@@ -549,3 +549,30 @@ def test_gptq_lowers_the_eq7_objective_and_keeps_zero_rows():
     e_rtn = D.gptq_objective(w_t, rtn * step, z)
     assert e_gptq < 0.8 * e_rtn, (e_gptq, e_rtn)
     assert np.abs(codes).max() <= 7
+
+
+# --- property tests of the oracle (hypothesis, derandomized) ----------------------------------
+
+from hypothesis import HealthCheck, given, settings, strategies as hst  # noqa: E402
+
+
+@settings(max_examples=40, derandomize=True, deadline=None, suppress_health_check=list(HealthCheck))
+@given(hst.data())
+def test_property_homogeneity_range_and_error_bound(data):
+    # Prop. 2 bit for bit under power-of-two scaling, codes in [-q, q] with full scale,
+    # and the per-element error within delta / 2, on drawn shapes and block sizes
+    bits = data.draw(hst.sampled_from([4, 8]))
+    b = 2 ** data.draw(hst.integers(0, 7))
+    K = b * data.draw(hst.integers(1, max(1, 512 // b)))
+    M = data.draw(hst.integers(1, 12))
+    k = data.draw(hst.integers(-20, 20))
+    x = synth.activations(M, K, seed=data.draw(hst.integers(0, 1 << 16)), dist="student_t3")
+    codes, delta = oracle.fwht_quant(x, b, bits)
+    c2, d2 = oracle.fwht_quant((x.float() * 2.0 ** k).to(torch.bfloat16), b, bits)
+    np.testing.assert_array_equal(c2, codes)
+    np.testing.assert_array_equal(d2, (delta.astype(np.float64) * 2.0 ** k).astype(np.float32))
+    q = 2 ** (bits - 1) - 1
+    assert np.abs(codes).max() <= q and np.all(np.abs(codes).max(axis=1) == q)
+    z = D.transform_tokens(x.float().numpy().astype(np.float64), b)  # normalized rotation
+    err = np.abs(z - delta[:, None].astype(np.float64) * codes)
+    assert np.all(err <= delta[:, None] * 0.5 * (1 + 1e-5) + 1e-30)
