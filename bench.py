@@ -205,9 +205,15 @@ def cpu_baseline(st, oracle, torch, budget_s=15.0):
         if el >= budget_s or steps >= 1000:
             break
     ops = st.wl.ops_per_step() * steps
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), model)
+    except OSError:
+        pass
     return {"value": ops / el / 1e12, "unit": "TOPS", "cores": oracle.max_threads(), "kind": "oracle",
             "sample": f"{steps} denoising steps of the action-expert layer (M=50, 7 projections), "
-                      f"{el:.1f} s"}
+                      f"{el:.1f} s", "cpu_model": model, "nproc": os.cpu_count()}
 
 
 def graph_of(torch, fn, reps):
