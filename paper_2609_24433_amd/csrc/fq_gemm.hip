@@ -862,7 +862,7 @@ static constexpr size_t tile_lds_bytes() {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Development tuning override, read once: FQ_TUNE="splits=<n>".
+// Development tuning override, read once: FQ_TUNE="splits=<n>" (and the other fields' names).
 struct Tune {
   int splits = 0;
   int wk = 0, kt = 0, wc = 0;
@@ -870,6 +870,7 @@ struct Tune {
   int loader = -1;
   int rb = 0;
   int order = -1;
+  int w16kt = 0;  // k steps per wave group of the single-token weight-only kernel
 };
 static Tune read_tune() {
   Tune t;
@@ -891,6 +892,8 @@ static Tune read_tune() {
   if (r) t.rb = atoi(r + 3);
   const char *o = strstr(e, "order=");
   if (o) t.order = atoi(o + 6);
+  const char *w16 = strstr(e, "w16slice=");
+  if (w16) t.w16kt = atoi(w16 + 9);
   return t;
 }
 
@@ -1166,15 +1169,19 @@ __device__ __forceinline__ bf16x8 nibbles_to_bf16(uint32_t w) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
-template <int MT, int KT>
+template <int MT, int KT, bool ONE>
 __global__ __launch_bounds__(256) void w4a16_stream_kernel(W16Params p) {
   constexpr int WK = 4;
   constexpr int AROW = WK * KT * 256;  // bf16 bytes per row of the slice (128 channels per step)
-  constexpr int ROWS = MT * 16;
+  constexpr int ROWS = MT * 16;        // rows of the output tile
+  // ONE (a single token): LDS holds that row only and every MFMA row reads it, so a slice
+  // of 128 k steps (K = 16384) takes 32 KB and K needs no split
+  constexpr int LROWS = ONE ? 1 : ROWS;
+  static_assert(!ONE || MT == 1, "single-token slices have one row tile");
   constexpr int CPR = AROW / 16;
-  constexpr int SLICE_KB = ROWS * AROW / 1024;
+  constexpr int SLICE_KB = LROWS * AROW / 1024;
   constexpr int IA = SLICE_KB / WK;
-  static_assert(ROWS * AROW % (1024 * WK) == 0, "slice must split into whole KBs per wave");
+  static_assert(LROWS * AROW % (1024 * WK) == 0, "slice must split into whole KBs per wave");
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
 
   const int tid = threadIdx.x;
@@ -1192,10 +1199,21 @@ __global__ __launch_bounds__(256) void w4a16_stream_kernel(W16Params p) {
   {
     const uint8_t *abase = p.x + ((int64_t)m0 * p.ldx + (int64_t)slice_begin * kTileK) * 2;
     const int valid_cols = min(WK * KT, ktot - slice_begin) * (kTileK * 2 / 16);
-    if (valid_cols == CPR)
+    if constexpr (ONE) {
+      // wave kg fills KBs [kg IA, (kg + 1) IA) of the one row (a single row is not swizzled);
+      // 16-byte chunks past the end of K read chunk 0
+#pragma unroll
+      for (int i = 0; i < IA; ++i) {
+        const int kb = kg * IA + i;
+        int col = kb * 64 + lane;
+        if (col >= valid_cols) col = 0;
+        load_to_lds16(abase + (uint32_t)(col * 16), lds + kb * 1024);
+      }
+    } else if (valid_cols == CPR) {
       stage_slice<AROW, IA, SLICE_KB, true>(abase, p.ldx * 2, mz, kg, lane, valid_cols, lds);
-    else
+    } else {
       stage_slice<AROW, IA, SLICE_KB, false>(abase, p.ldx * 2, mz, kg, lane, valid_cols, lds);
+    }
   }
   // 2. this wave's weight tiles, in k order, unconditionally (clamped past the end of K)
   sched_wall();
@@ -1222,7 +1240,7 @@ __global__ __launch_bounds__(256) void w4a16_stream_kernel(W16Params p) {
         const bf16x8 b = nibbles_to_bf16(wd[c]);
 #pragma unroll
         for (int i = 0; i < MT; ++i) {
-          const int row = i * 16 + r16;
+          const int row = ONE ? 0 : i * 16 + r16;
           const int chunk = (kg * KT + kt) * 16 + 4 * g + c;
           const uint4 av = *reinterpret_cast<const uint4 *>(lds + row * AROW + ((chunk ^ slice_swizzle<AROW>(row)) * 16));
           acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av), b, acc[i], 0, 0, 0);
@@ -1291,6 +1309,24 @@ __global__ __launch_bounds__(256) void w4a16_splitk_epilogue_kernel(W16Params p,
 W16Plan plan_w4a16(int64_t M, int64_t N, int64_t K) {
   W16Plan pl{};
   const int ktot = (int)(K / kTileK);
+  if (M == 1 && ktot > 16) {
+    // a single token: LDS holds its row only (KT KB, not 16 rows' worth), so many
+    // workgroups share a compute unit.  K up to 8192 in one slice (no split-K epilogue);
+    // longer K in slices of 32 k steps, which spreads the weight stream and its nibble
+    // widening over more compute units (measured at K 16384 -> N 2048: 8.9 us against
+    // 10.6 us for one 128-step slice per 16 channels).
+    pl.one = true;
+    pl.mt = 1;
+    const int per = (ktot + 3) / 4;  // k steps per wave group
+    pl.kt = per <= 8 ? 8 : (per <= 16 ? 16 : 8);
+    static const Tune tune = read_tune();
+    if (tune.w16kt == 4 || tune.w16kt == 8 || tune.w16kt == 16 || tune.w16kt == 32) pl.kt = tune.w16kt;
+    pl.splits = (ktot + 4 * pl.kt - 1) / (4 * pl.kt);
+    pl.tiles = N / 16;
+    pl.rb = 1;
+    pl.partial_bytes = pl.splits > 1 ? align256((size_t)pl.splits * M * N * 4) : 0;
+    return pl;
+  }
   pl.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   const int smax = 32 / pl.mt;  // k steps per slice that fit 128 KB of LDS for 16 mt rows
   const int per = ktot < smax ? ktot : smax;
@@ -1302,17 +1338,26 @@ W16Plan plan_w4a16(int64_t M, int64_t N, int64_t K) {
   return pl;
 }
 
-template <int MT, int KT>
+template <int MT, int KT, bool ONE = false>
 static hipError_t launch_w16(const W16Params &p, dim3 grid, hipStream_t s) {
-  constexpr size_t slice = (size_t)MT * 16 * 4 * KT * 256;
+  constexpr size_t slice = (size_t)(ONE ? 1 : MT * 16) * 4 * KT * 256;
   constexpr size_t red = (size_t)4 * MT * 64 * 16;
   constexpr size_t lds = slice > red ? slice : red;
   static_assert(lds <= 160 * 1024, "LDS budget");
   static bool attr = false;
-  hipError_t e = allow_lds(&w4a16_stream_kernel<MT, KT>, lds, attr);
+  hipError_t e = allow_lds(&w4a16_stream_kernel<MT, KT, ONE>, lds, attr);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((w4a16_stream_kernel<MT, KT>), grid, dim3(256), lds, s, p);
+  hipLaunchKernelGGL((w4a16_stream_kernel<MT, KT, ONE>), grid, dim3(256), lds, s, p);
   return hipGetLastError();
+}
+
+static hipError_t launch_w16_one(const W16Params &p, int kt, dim3 grid, hipStream_t s) {
+  switch (kt) {
+    case 4: return launch_w16<1, 4, true>(p, grid, s);
+    case 8: return launch_w16<1, 8, true>(p, grid, s);
+    case 16: return launch_w16<1, 16, true>(p, grid, s);
+    default: return launch_w16<1, 32, true>(p, grid, s);
+  }
 }
 
 template <int MT>
@@ -1342,7 +1387,9 @@ hipError_t launch_w4a16(const W16Args &g, const W16Plan &pl, void *ws, hipStream
   p.K = (int)g.K;
   const dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits, (unsigned)pl.rb);
   hipError_t e;
-  switch (pl.mt) {
+  if (pl.one) {
+    e = launch_w16_one(p, pl.kt, grid, s);
+  } else switch (pl.mt) {
     case 1: e = launch_w16_kt<1>(p, pl.kt, grid, s); break;
     case 2: e = launch_w16_kt<2>(p, pl.kt, grid, s); break;
     default: e = launch_w16_kt<4>(p, pl.kt, grid, s); break;

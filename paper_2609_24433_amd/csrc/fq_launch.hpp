@@ -73,6 +73,7 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStrea
 // Weight-only INT4 (bf16 activations) projection.
 struct W16Plan {
   int mt, kt;           // 16-row tiles per workgroup, k steps per wave group (4 groups)
+  bool one;             // a single token: only its row is staged, and K up to 16384 needs no split
   int splits, rb;       // K slices, row blocks
   int64_t tiles;        // 16-channel weight tiles
   size_t partial_bytes; // fp32 partials [splits][M][N] when K is split

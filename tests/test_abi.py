@@ -150,15 +150,20 @@ def call_w4a16(x=FAKE, ldx=1024, w=FAKE, sw=FAKE, bias=NULL, y=FAKE, ldy=256, ac
     (dict(M=-1), 2), (dict(ldx=512), 2), (dict(ldy=128), 2),
     (dict(N=250, ldy=256), 3), (dict(K=1000, ldx=1000), 3), (dict(K=0), 3),
     (dict(x=MISALIGNED), 4), (dict(acc=MISALIGNED), 4), (dict(ldx=1028), 4), (dict(bias=MISALIGNED), 4),
-    (dict(ws=NULL, ws_bytes=0, K=16384, ldx=16384), 5), (dict(ws_bytes=8, K=16384, ldx=16384), 5),
+    (dict(ws=NULL, ws_bytes=0, K=32768, ldx=32768), 5), (dict(ws_bytes=8, K=32768, ldx=32768), 5),
 ])
 def test_w4a16_rejects(kw, status):
+    if status == 5:
+        # the shape must split K (need a workspace), or the call would go on to launch
+        assert fq.w4a16_workspace_bytes(kw.get("M", 1), kw.get("N", 256), kw["K"]) > 8
     assert call_w4a16(**kw) == status
 
 
 def test_w4a16_workspace_sizes():
     assert fq.w4a16_workspace_bytes(1, 2048, 1024) == 0          # one K slice: no partials
+    assert fq.w4a16_workspace_bytes(1, 2048, 8192) == 0          # a single token up to K = 8192
     assert fq.w4a16_workspace_bytes(1, 2048, 16384) >= 4 * 1 * 2048 * 4
+    assert fq.w4a16_workspace_bytes(2, 2048, 16384) >= 4 * 2 * 2048 * 4
     assert fq.w4a16_workspace_bytes(0, 2048, 16384) == 0
     assert call_w4a16(M=0, x=NULL, w=NULL, sw=NULL, y=NULL) == 0
 

@@ -27,6 +27,10 @@ CASES = [
     (1, 1024, 6144, 0, False), (3, 1024, 256, 8, True), (16, 2048, 512, 0, False), (17, 2048, 256, 0, True),
     (50, 4096, 1024, 0, False), (1, 16384, 2048, 0, True), (16, 16384, 512, 16, False), (64, 128, 16, 0, False),
     (70, 1024, 256, 0, True), (130, 2048, 128, 8, False), (2, 32768, 64, 0, False),
+    # a single token past 16 k steps stages only its own row: ragged wave groups, one
+    # slice of up to 64 k steps (K = 8064: 63), split K beyond (K = 12160: 3 slices, ragged)
+    (1, 2176, 128, 0, True), (1, 4096, 256, 8, False), (1, 8064, 48, 8, True), (1, 12160, 48, 8, True),
+    (1, 32768, 64, 0, False),
 ]
 
 
