@@ -215,6 +215,7 @@ LINEAR_CASES = [
     (50, 1024, 256, 128, 4), (50, 4096, 1024, 128, 4), (50, 1024, 4096, 128, 4),
     (16, 16384, 2048, 32, 8), (1, 16384, 2048, 256, 4), (77, 2048, 256, 128, 8),
     (130, 2048, 2048, 128, 4), (33, 512, 48, 16, 4), (0, 1024, 256, 64, 4),
+    (200, 16384, 256, 128, 4),   # tiled GEMM with K split in 4 (split-K epilogue)
 ]
 
 
