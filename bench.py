@@ -13,8 +13,10 @@ device before timing; inputs are resident in HBM when the timed region starts.
 The 10-step denoising loop is captured into one HIP graph (each step also into a graph
 of its own, for a remainder of K) and the timed region runs exactly K steps.  Prints ONE JSON line, which also carries `points`: the graded single projections
 (down-projection K 16384 -> N 2048 at M = 50 / 816 / 4096 and gate-projection M = 816,
-cold weights), the weight-only INT4 projection, the prologue alone with the composite
-rotation beside the block Hadamard, and the offline GPTQ stages.
+cold weights), the rest of the down-projection sweep (M = 1, 16, 256, 4096 in W4A4 and
+W8A8; the prologue at b = 32, 64, 128, 256), the weight-only INT4 projection, the
+prologue alone with the composite rotation beside the block Hadamard, and the offline
+GPTQ stages.
 
   python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points] [--only-points]
 """
@@ -366,6 +368,10 @@ def measure_points(torch, fq, synth, dev, log_fn):
     run_point("down_w4a4_m816_gemm", 816, 16384, 2048, 128, 4, "gemm")
     run_point("down_w8a8_m816_linear", 816, 16384, 2048, 128, 8, "linear")
     run_point("down_w4a4_m4096_gemm", 4096, 16384, 2048, 128, 4, "gemm")
+    # the rest of the down-projection sweep's token counts (K 16384 -> N 2048, b = 128)
+    for bits_ in (4, 8):
+        for M_ in (1, 16, 256, 4096):
+            run_point(f"down_w{bits_}a{bits_}_m{M_}_linear", M_, 16384, 2048, 128, bits_, "linear")
     # warm: the same weights every call (resident in the 256 MB MALL), as shared weights are
     # across denoising steps
     run_point("down_w4a4_m50_linear_warm", 50, 16384, 2048, 128, 4, "linear", warm=True)
@@ -483,6 +489,26 @@ def measure_prologue_points(torch, fq, synth, dev, log_fn):
             out.append(rec)
             del g
         del x, perm, blocks, codes, delta, ws
+        torch.cuda.empty_cache()
+    # the butterfly prologue at every block size of the down-projection sweep (M = 816,
+    # K = 16384, Student-t rows): log2 b stages, the last log2(b / 16) across lanes
+    M, K = 816, 16384
+    for b in (32, 64, 128, 256):
+        x = synth.down_proj_sweep_point(M, b, 4).site_activation("D", 0).to(dev)
+        codes = torch.empty((M, K // 2), dtype=torch.uint8, device=dev)
+        delta = torch.empty((M,), dtype=torch.float32, device=dev)
+        call = lambda i: fq._check(fq.LIB.fq_fwht_quant(fq._p(x), K, None, None, M, K, b, 4, 1.0, fq._p(codes),
+                                                         fq._p(delta), fq._stream()))
+        reps = 20
+        g = graph_of(torch, call, reps)
+        us = time_graph(torch, g, 4) / reps * 1e6
+        nbytes = M * (2 * K + K // 2 + 4)
+        rec = {"name": f"sweep_prologue_m816_b{b}_fwht", "kind": "prologue_fwht", "M": M, "K": K, "b": b, "bits": 4,
+               "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1), "bound": "hbm",
+               "roofline_frac": round(nbytes / HBM_PEAK_GBS / 1e3 / us, 4)}
+        log_fn(json.dumps(rec))
+        out.append(rec)
+        del g, x, codes, delta
         torch.cuda.empty_cache()
     return out
 
