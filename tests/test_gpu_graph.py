@@ -76,6 +76,16 @@ def test_w4a16_and_rotation_graph_replays():
 
     _replays_match(call_w16, x_buf, [synth.activations(M, K, seed=s).to(DEV) for s in (7, 8)], y)
 
+    # a single token: only its row staged, K in 4 slices and the split-K epilogue
+    x1 = synth.activations(1, K, seed=14).to(DEV)
+    y1 = torch.empty((1, N), dtype=torch.bfloat16, device=DEV)
+    ws1 = f.workspace(f.w4a16_workspace_bytes(1, N, K), DEV)
+
+    def call_w16_one(out=None):
+        f.gemm_w4a16(x1, packed, s_w, N, ws=ws1, out=y1 if out is None else out)
+
+    _replays_match(call_w16_one, x1, [synth.activations(1, K, seed=s).to(DEV) for s in (15, 16)], y1)
+
     Kr = 2048
     perm = torch.from_numpy(synth.permutation(Kr, seed=9)).to(DEV)
     blocks = torch.from_numpy(synth.orthogonal_blocks(Kr // b, b, seed=10)).to(DEV)

@@ -64,3 +64,28 @@ def test_w4a16_parity(M, K, N, pad, with_bias):
     if M > 2:
         want = torch.zeros(N, dtype=torch.float32) if bias is None else torch.from_numpy(bias)
         assert torch.equal(y[1].cpu(), want.to(torch.bfloat16))
+
+
+def test_w4a16_split_workspace_reuse():
+    """Split K: the workspace (fp32 partial sums) needs no initialization (here: random
+    bytes) and one workspace serves calls of different shapes one after the other."""
+    flush("w4a16 split-K workspace reuse")
+    f = fq()
+    shapes = [(1, 16384, 512), (16, 16384, 256), (1, 32768, 128), (3, 8192, 512), (1, 16384, 512)]
+    need = max(f.w4a16_workspace_bytes(M, N, K) for M, K, N in shapes)
+    assert need > 0
+    ws = torch.randint(0, 256, (need,), dtype=torch.uint8, device=DEV)
+    for i, (M, K, N) in enumerate(shapes):
+        x = synth.activations(M, K, seed=40 + i, outlier_frac=0.01, outlier_scale=30.0)
+        w = synth.weights(N, K, seed=50 + i)
+        codes, s_w = f.quantize_weights(torch.from_numpy(w).to(DEV), 1, 4)
+        packed = f.pack_weights(codes, 4)
+        y, acc = f.gemm_w4a16(x.to(DEV), packed, s_w, N, ws=ws, want_acc=True)
+        torch.cuda.synchronize()
+        q_ref, s_ref = oracle.quantize_weights(w, 1, 4)
+        acc_ref, y_ref = oracle.w4a16(x.contiguous(), q_ref, s_ref, None)
+        absx = np.abs(x.float().numpy().astype(np.float64))
+        bound = (K - 1) * 2.0 ** -24 * (absx @ np.abs(q_ref.astype(np.float64)).T) + 1e-30
+        err = np.abs(acc.cpu().numpy().astype(np.float64) - acc_ref)
+        assert np.all(err <= bound), (M, K, N, float((err / bound).max()))
+        assert_bf16_close(y, y_ref)
