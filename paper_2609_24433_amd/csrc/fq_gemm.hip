@@ -1000,22 +1000,11 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
 
 size_t gemm_plan_workspace(const GemmPlan &pl) { return pl.partial_bytes; }
 
-template <typename Kern>
-static hipError_t allow_lds(Kern kern, size_t lds, bool &done) {
-  if (lds > 65536 && !done) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    done = true;
-  }
-  return hipSuccess;
-}
-
 template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
 static hipError_t launch_stream(const GemmParams &p, dim3 grid, hipStream_t s) {
   const size_t lds = stream_lds_bytes<BITS, AFMT, MT, KT, WK, WC>();
-  static bool attr = false;
-  hipError_t e = allow_lds(&gemm_stream_kernel<BITS, AFMT, MT, KT, WK, WC>, lds, attr);
+  static std::atomic<uint64_t> attr{0};
+  hipError_t e = allow_dynamic_lds(&gemm_stream_kernel<BITS, AFMT, MT, KT, WK, WC>, lds, attr);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, MT, KT, WK, WC>), grid, dim3(64 * WC * WK), lds, s, p);
   return hipGetLastError();
@@ -1066,8 +1055,8 @@ template <int BITS, int AFMT, int ST, int LW>
 static hipError_t launch_tile(const GemmParams &p, dim3 grid, hipStream_t s) {
   constexpr size_t lds = tile_lds_bytes<BITS, AFMT, 128, 128, ST>();
   static_assert(lds <= 160 * 1024, "LDS budget");
-  static bool attr = false;
-  hipError_t e = allow_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST, LW>, lds, attr);
+  static std::atomic<uint64_t> attr{0};
+  hipError_t e = allow_dynamic_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST, LW>, lds, attr);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128, ST, LW>), grid, dim3(256 + 64 * LW), lds, s, p);
   return hipGetLastError();
@@ -1344,8 +1333,8 @@ static hipError_t launch_w16(const W16Params &p, dim3 grid, hipStream_t s) {
   constexpr size_t red = (size_t)4 * MT * 64 * 16;
   constexpr size_t lds = slice > red ? slice : red;
   static_assert(lds <= 160 * 1024, "LDS budget");
-  static bool attr = false;
-  hipError_t e = allow_lds(&w4a16_stream_kernel<MT, KT, ONE>, lds, attr);
+  static std::atomic<uint64_t> attr{0};
+  hipError_t e = allow_dynamic_lds(&w4a16_stream_kernel<MT, KT, ONE>, lds, attr);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((w4a16_stream_kernel<MT, KT, ONE>), grid, dim3(256), lds, s, p);
   return hipGetLastError();

@@ -5,7 +5,28 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace fq {
+
+// A kernel launched with more than 64 KB of dynamic LDS must first raise its limit with
+// hipFuncSetAttribute, on every device it runs on.  `done` (one per kernel
+// instantiation) records the devices already raised, 64 at most; concurrent first
+// launches may both set the attribute, which is harmless.
+template <typename Kern>
+inline hipError_t allow_dynamic_lds(Kern kern, size_t lds, std::atomic<uint64_t> &done) {
+  if (lds <= 65536) return hipSuccess;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  const uint64_t bit = 1ull << dev;
+  if (done.load(std::memory_order_acquire) & bit) return hipSuccess;
+  e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  done.fetch_or(bit, std::memory_order_release);
+  return hipSuccess;
+}
 
 // Output layouts of the prologue.
 constexpr int kOutNibble = 0;  // canonical signed-INT4: channel 2i low nibble of byte i

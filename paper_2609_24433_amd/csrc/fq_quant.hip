@@ -253,13 +253,9 @@ static QuantShape quant_shape(int64_t M, int K) {
 
 template <typename Tin, int LOG2B, int CPT, int NT>
 static hipError_t launch_one(const QuantParams &p, size_t smem, int grid, hipStream_t s) {
-  static bool attr = false;  // more than 64 KB of dynamic LDS must be requested once
-  if (smem > 65536 && !attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&fwht_quant_kernel<Tin, LOG2B, CPT, NT>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
+  static std::atomic<uint64_t> attr{0};
+  hipError_t e = allow_dynamic_lds(&fwht_quant_kernel<Tin, LOG2B, CPT, NT>, smem, attr);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL((fwht_quant_kernel<Tin, LOG2B, CPT, NT>), dim3(grid), dim3(NT), smem, s, p);
   return hipGetLastError();
 }

@@ -266,13 +266,9 @@ static hipError_t launch_rot_tr(const void *x, int64_t ldx, const int32_t *perm,
                                 hipStream_t s) {
   constexpr size_t lds = rot_lds_bytes<B, TR>();
   static_assert(lds <= 160 * 1024, "LDS budget");
-  static bool attr = false;  // more than 64 KB of dynamic LDS must be requested once
-  if (lds > 65536 && !attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&rot_transform_kernel<Tin, B, TR>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
+  static std::atomic<uint64_t> attr{0};
+  hipError_t e = allow_dynamic_lds(&rot_transform_kernel<Tin, B, TR>, lds, attr);
+  if (e != hipSuccess) return e;
   constexpr int R = rot_rows<B, TR>();
   const int64_t gy = (M + R - 1) / R;
   if (gy > 65535) return hipErrorInvalidValue;
