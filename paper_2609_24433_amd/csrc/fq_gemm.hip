@@ -20,7 +20,8 @@
 //     output channels, a block of rows (all M, or 16 when the grid would be small) and
 //     a slice of K (split again between up to 4 wave groups that add up in LDS); the
 //     activation slice is staged to LDS in one batch.
-//   gemm_tile (M > 64): 128 x 128 output tiles fed through a ring of LDS stages, with a
+//   gemm_tile (M > 64): 128 x 128 output tiles (64 x 128 when the larger tiles would
+//     leave half the compute units idle) fed through a ring of LDS stages, with a
 //     register-level software pipeline and an optional load-issuing fifth wave.
 // When K is split across workgroups, each slice writes its raw INT32 tile to a
 // partial buffer and a small epilogue kernel adds the slices (exact) and rescales;
@@ -789,6 +790,14 @@ __global__ __launch_bounds__(256 + 64 * LW) void gemm_tile_kernel(GemmParams p) 
         }
       }
     }
+    // smaller tiles have fewer MFMAs per step than reads (int8 operands): the rest now
+    if (more) {
+#pragma unroll
+      for (; r < NREAD; ++r) {
+        __builtin_amdgcn_sched_barrier(0);
+        read_one(cur ^ 1, ks + 1, r);
+      }
+    }
     __builtin_amdgcn_sched_barrier(0);
   };
 
@@ -870,6 +879,7 @@ struct Tune {
   int loader = -1;
   int rb = 0;
   int order = -1;
+  int bm = 0, bn = 0;  // tiled workgroup tile (64 or 128)
   int w16kt = 0;  // k steps per wave group of the single-token weight-only kernel
 };
 static Tune read_tune() {
@@ -892,6 +902,10 @@ static Tune read_tune() {
   if (r) t.rb = atoi(r + 3);
   const char *o = strstr(e, "order=");
   if (o) t.order = atoi(o + 6);
+  const char *tbm = strstr(e, "bm=");
+  if (tbm) t.bm = atoi(tbm + 3);
+  const char *tbn = strstr(e, "bn=");
+  if (tbn) t.bn = atoi(tbn + 3);
   const char *w16 = strstr(e, "w16slice=");
   if (w16) t.w16kt = atoi(w16 + 9);
   return t;
@@ -972,11 +986,27 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     }
   } else {
     pl.kind = 1;
+    // K slices: split a grid of fewer than 200 tiles while each slice keeps >= 32 steps
+    auto slices = [&](int64_t tiles) {
+      int64_t s = 1;
+      while (tiles * s < 200 && s < 4 && ktot / (s * 2) >= 32) s *= 2;
+      return s;
+    };
+    // 128 x 128 tiles; 64 x 128 when the 128-row grid, split included, would leave half
+    // the compute units idle (measured: M = 256, K 16384 -> N 2048 in 19.0 against
+    // 24.0 us; M = 816, K 2048 -> N 2048 in 9.7 against 13.1 us; at M = 816,
+    // K 16384 -> N 2048 the split 128-row grid stays ahead, 39.7 against 43.1 us)
     pl.bm = 128;
     pl.bn = 128;
-    const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
-    int64_t s = 1;
-    while (tiles * s < 200 && s < 4 && ktot / (s * 2) >= 32) s *= 2;
+    {
+      const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
+      if (t128 * slices(t128) <= 128) pl.bm = 64;
+    }
+    if (tune.bm == 64 || tune.bm == 128) pl.bm = tune.bm;
+    if (tune.bn == 64 || tune.bn == 128) pl.bn = tune.bn;
+    if (pl.bm == 64 && pl.bn == 64) pl.bn = 128;  // 64 x 64 is not built
+    const int64_t tiles = ((M + pl.bm - 1) / pl.bm) * ((N + pl.bn - 1) / pl.bn);
+    int64_t s = slices(tiles);
     if (tune.splits > 0) s = tune.splits < ktot ? tune.splits : ktot;
     pl.ksteps = (int)((ktot + s - 1) / s);
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
@@ -1051,15 +1081,29 @@ static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, int wc, 
   }
 }
 
-template <int BITS, int AFMT, int ST, int LW>
+template <int BITS, int AFMT, int BM, int BN, int ST, int LW>
 static hipError_t launch_tile(const GemmParams &p, dim3 grid, hipStream_t s) {
-  constexpr size_t lds = tile_lds_bytes<BITS, AFMT, 128, 128, ST>();
+  constexpr size_t lds = tile_lds_bytes<BITS, AFMT, BM, BN, ST>();
   static_assert(lds <= 160 * 1024, "LDS budget");
   static std::atomic<uint64_t> attr{0};
-  hipError_t e = allow_dynamic_lds(&gemm_tile_kernel<BITS, AFMT, 128, 128, ST, LW>, lds, attr);
+  hipError_t e = allow_dynamic_lds(&gemm_tile_kernel<BITS, AFMT, BM, BN, ST, LW>, lds, attr);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, 128, 128, ST, LW>), grid, dim3(256 + 64 * LW), lds, s, p);
+  hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, BM, BN, ST, LW>), grid, dim3(256 + 64 * LW), lds, s, p);
   return hipGetLastError();
+}
+
+template <int BITS, int AFMT, int BM, int BN>
+static hipError_t launch_tile_shape(const GemmParams &p, const GemmPlan &pl, dim3 grid, hipStream_t s) {
+  if (pl.loader) {
+    // one wave's loads of STAGES - 2 steps must fit the 6-bit vmcnt: 4 stages only for INT4
+    if constexpr (BITS == 4)
+      return pl.stages == 4 ? launch_tile<BITS, AFMT, BM, BN, 4, 1>(p, grid, s)
+                            : launch_tile<BITS, AFMT, BM, BN, 3, 1>(p, grid, s);
+    else
+      return launch_tile<BITS, AFMT, BM, BN, 3, 1>(p, grid, s);
+  }
+  return pl.stages == 4 ? launch_tile<BITS, AFMT, BM, BN, 4, 0>(p, grid, s)
+                        : launch_tile<BITS, AFMT, BM, BN, 3, 0>(p, grid, s);
 }
 
 template <int BITS, int AFMT>
@@ -1074,15 +1118,12 @@ static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStre
     }
   } else {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
-    if (pl.loader) {
-      // one wave's loads of STAGES - 2 steps must fit the 6-bit vmcnt: 4 stages only for INT4
-      if constexpr (BITS == 4)
-        e = pl.stages == 4 ? launch_tile<BITS, AFMT, 4, 1>(p, grid, s) : launch_tile<BITS, AFMT, 3, 1>(p, grid, s);
-      else
-        e = launch_tile<BITS, AFMT, 3, 1>(p, grid, s);
-    }
+    if (pl.bm == 64)
+      e = launch_tile_shape<BITS, AFMT, 64, 128>(p, pl, grid, s);
+    else if (pl.bn == 64)
+      e = launch_tile_shape<BITS, AFMT, 128, 64>(p, pl, grid, s);
     else
-      e = pl.stages == 4 ? launch_tile<BITS, AFMT, 4, 0>(p, grid, s) : launch_tile<BITS, AFMT, 3, 0>(p, grid, s);
+      e = launch_tile_shape<BITS, AFMT, 128, 128>(p, pl, grid, s);
   }
   if (e != hipSuccess || pl.splits == 1) return e;
   const int64_t threads = (int64_t)p.M * (p.N / 4);

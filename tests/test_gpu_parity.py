@@ -155,7 +155,8 @@ def test_pack_unpack_round_trip(bits, N, K):
 # ------------------------------------------------------------------ GEMM + epilogue (eq. (8))
 
 GEMM_CASES = [
-    # (M, N, K) -- streaming kernel for M <= 64, tiled kernel above, split-K where the plan asks
+    # (M, N, K) -- streaming kernel for M <= 64, tiled kernel above (64 x 128 tiles on
+    # these small grids; 128 x 128 in the full-size tests), split-K where the plan asks
     (1, 16, 128), (16, 48, 1024), (17, 256, 1024), (50, 2048, 4096), (64, 272, 2048),
     (65, 256, 1024), (130, 400, 1024), (300, 272, 2048), (50, 1024, 16384), (200, 128, 8192),
     # 33-64 rows with long K: 16-row blocks over 128-step slices (one or two K slices)
