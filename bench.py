@@ -14,7 +14,9 @@ The 10-step denoising loop is captured into one HIP graph (each step also into a
 of its own, for a remainder of K) and the timed region runs exactly K steps.  Prints ONE JSON line, which also carries `points`: the graded single projections
 (down-projection K 16384 -> N 2048 at M = 50 / 816 / 4096 and gate-projection M = 816,
 cold weights), the rest of the down-projection sweep (M = 1, 16, 256, 4096 in W4A4 and
-W8A8; the prologue at b = 32, 64, 128, 256), the weight-only INT4 projection, the
+W8A8; the prologue at b = 32, 64, 128, 256), the 18-layer selective-INT8 backbone chain
+(time per layer and end to end, cosine against the fp32 chain), the weight-only INT4
+projection, the
 prologue alone with the composite rotation beside the block Hadamard, and the offline
 GPTQ stages.
 
@@ -396,6 +398,7 @@ def measure_points(torch, fq, synth, dev, log_fn):
     run_point("down_w4a16_m16", 16, 16384, 2048, 1, 4, "w4a16")
     out += measure_bf16_context(torch, synth, dev, log_fn, out)
     out += measure_prologue_points(torch, fq, synth, dev, log_fn)
+    out += measure_mixed_chain(torch, fq, synth, dev, log_fn)
     out += measure_gptq_points(torch, fq, synth, dev, log_fn)
     return out
 
@@ -525,6 +528,100 @@ def measure_prologue_points(torch, fq, synth, dev, log_fn):
         del g, x, codes, delta
         torch.cuda.empty_cache()
     return out
+
+
+def measure_mixed_chain(torch, fq, synth, dev, log_fn, layers=18):
+    """Selective-INT8 language backbone: `layers` layers of the width-2048 shapes at
+    M = 816 (q|k|v 2048 -> 2560 and gate|up 2048 -> 32768 W4A4; o 2048 -> 2048 and down
+    16384 -> 2048 W8A8; b = 128).  Per layer: a = RMSNorm(h) (eps 1e-6), q|k|v = Lin_A(a)
+    with the norm's gain folded into the weights; o = Lin_O(q), q standing in for the
+    attention output; h1 = h + o; g|u = Lin_B(RMSNorm(h1)), gain folded; d =
+    Lin_D(silu(g) * u); h = h1 + d.  Norms, SwiGLU and residuals run in fp32 torch (outside
+    the projection).  Weights N(0, 0.02) drawn on the device (torch generator seeded
+    4000 + layer), gains U(0.5, 1.5); h0 = the backbone's seeded activations.  Times the
+    whole quantized chain and its 4 fused projections per layer (HIP graphs) and reports
+    the cosine of the final hidden state against the same chain in fp32 with the
+    unquantized weights and explicit gains."""
+    M, D, KV, F, b = 816, 2048, 256, 16384, 128
+    shapes = {"A": (D + 2 * KV, D, 4), "O": (D, D, 8), "B": (2 * F, D, 4), "D": (D, F, 8)}
+
+    def layer_weights(l):
+        g = torch.Generator(device=dev)
+        g.manual_seed(4000 + l)
+        w = {s_: torch.randn((n, k), generator=g, device=dev, dtype=torch.float32) * 0.02
+             for s_, (n, k, _) in shapes.items()}
+        gain = {s_: torch.rand((D,), generator=g, device=dev, dtype=torch.float32) + 0.5 for s_ in ("A", "B")}
+        return w, gain
+
+    def rms(h):
+        return h * torch.rsqrt(torch.mean(h * h, dim=1, keepdim=True) + 1e-6)
+
+    lins, ws_bytes = [], 0
+    for l in range(layers):
+        w, gain = layer_weights(l)
+        lins.append({s_: fq.QuantLinear(w[s_], b, bits, col_scale=gain.get(s_))
+                     for s_, (_, _, bits) in shapes.items()})
+        ws_bytes = max([ws_bytes] + [fq.linear_workspace_bytes(M, n, k, bits) for n, k, bits in shapes.values()])
+        del w, gain
+    ws = fq.workspace(ws_bytes, dev)
+    h0 = synth.backbone_layer_mixed(0).site_activation("A", 0).to(dev).float()
+    h = torch.empty_like(h0)
+    a_in = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
+    qkv = torch.empty((M, D + 2 * KV), dtype=torch.bfloat16, device=dev)
+    o = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
+    b_in = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
+    gu = torch.empty((M, 2 * F), dtype=torch.bfloat16, device=dev)
+    m_in = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
+    dn = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
+
+    def forward(i):
+        h.copy_(h0)
+        for L in lins:
+            a_in.copy_(rms(h))
+            L["A"](a_in, ws=ws, out=qkv)
+            L["O"](qkv[:, :D], ws=ws, out=o)
+            h.add_(o.float())
+            b_in.copy_(rms(h))
+            L["B"](b_in, ws=ws, out=gu)
+            m_in.copy_(torch.nn.functional.silu(gu[:, :F].float()) * gu[:, F:].float())
+            L["D"](m_in, ws=ws, out=dn)
+            h.add_(dn.float())
+
+    def projections(i):
+        for L in lins:
+            L["A"](a_in, ws=ws, out=qkv)
+            L["O"](qkv[:, :D], ws=ws, out=o)
+            L["B"](b_in, ws=ws, out=gu)
+            L["D"](m_in, ws=ws, out=dn)
+
+    g_chain = graph_of(torch, forward, 1)
+    us_chain = time_graph(torch, g_chain, 5) * 1e6
+    g_chain.replay()
+    torch.cuda.synchronize()
+    h_q = h.clone()
+    g_proj = graph_of(torch, projections, 1)
+    us_proj = time_graph(torch, g_proj, 5) * 1e6
+    del g_chain, g_proj
+
+    # fp32 reference chain (unquantized weights, gains applied to the activations)
+    hr = h0.clone()
+    for l in range(layers):
+        w, gain = layer_weights(l)
+        qkv_r = (gain["A"] * rms(hr)) @ w["A"].t()
+        hr = hr + qkv_r[:, :D] @ w["O"].t()
+        gu_r = (gain["B"] * rms(hr)) @ w["B"].t()
+        hr = hr + (torch.nn.functional.silu(gu_r[:, :F]) * gu_r[:, F:]) @ w["D"].t()
+        del w, gain
+    cos = torch.nn.functional.cosine_similarity(h_q.flatten(), hr.flatten(), dim=0).item()
+    ops = layers * 2.0 * M * sum(n * k for n, k, _ in shapes.values())
+    rec = {"name": f"mixed_chain_{layers}l_m{M}", "kind": "chain", "layers": layers, "M": M, "b": b,
+           "us_total": round(us_chain, 1), "us_per_layer": round(us_chain / layers, 2),
+           "projections_us_per_layer": round(us_proj / layers, 2),
+           "projection_TOPS": round(ops / us_proj / 1e6, 1), "cosine_vs_fp32": round(cos, 6)}
+    log_fn(json.dumps(rec))
+    del lins, ws
+    torch.cuda.empty_cache()
+    return [rec]
 
 
 def main():
