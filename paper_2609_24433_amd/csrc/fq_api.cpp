@@ -100,6 +100,8 @@ fq_status check_gemm(const void *a, const float *delta, const void *w, const flo
   if ((s = check_k(K)) != FQ_OK) return s;
   if (N % 16) return fail(FQ_ERR_UNSUPPORTED, "N=%lld is not a multiple of 16", (long long)N);
   if (N > (1ll << 24) || M > (1ll << 24)) return fail(FQ_ERR_UNSUPPORTED, "M or N too large");
+  // keeps every tile count and tile index of the launch grids within 31 bits
+  if (M * N > (1ll << 40)) return fail(FQ_ERR_UNSUPPORTED, "M x N = %lld outputs is too large", (long long)(M * N));
   if (ldy < N) return fail(FQ_ERR_SHAPE, "ldy=%lld < N=%lld", (long long)ldy, (long long)N);
   if (ldy % 8) return fail(FQ_ERR_ALIGN, "ldy=%lld is not a multiple of 8", (long long)ldy);
   if (M == 0 || N == 0) return FQ_OK;
@@ -319,6 +321,7 @@ fq_status fq_gemm_w4a16(const void *x_bf16, int64_t ldx, const void *w_packed, c
   if (M == 0 || N == 0) return ok();
   if (acc_out && !aligned16(acc_out)) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
   const fq::W16Plan pl = fq::plan_w4a16(M, N, K);
+  if (pl.rb > 65535) return fail(FQ_ERR_UNSUPPORTED, "M=%lld: at most %d rows", (long long)M, 64 * 65535);
   if (pl.partial_bytes > 0 && (!ws || ws_bytes < pl.partial_bytes))
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", pl.partial_bytes,
                 ws ? ws_bytes : (size_t)0);

@@ -93,6 +93,7 @@ def call_gemm(bits=4, a=FAKE, delta=FAKE, w=FAKE, sw=FAKE, bias=NULL, y=FAKE, ld
     (dict(a=NULL), 1), (dict(delta=NULL), 1), (dict(w=NULL), 1), (dict(sw=NULL), 1), (dict(y=NULL), 1),
     (dict(M=-3), 2), (dict(ldy=128), 2), (dict(N=-16), 2),
     (dict(N=250, ldy=256), 3), (dict(K=1000), 3), (dict(K=0), 3),
+    (dict(M=1 << 24, N=1 << 20, ldy=1 << 20), 3),  # more outputs than the launch grids index
     (dict(bias=MISALIGNED), 4), (dict(acc=MISALIGNED), 4), (dict(ldy=260), 4), (dict(w=MISALIGNED), 4),
     (dict(ws=NULL, ws_bytes=0, M=50, N=2048, ldy=2048, K=32768), 5),
     (dict(ws_bytes=16, M=50, N=2048, ldy=2048, K=32768), 5),
@@ -149,6 +150,7 @@ def call_w4a16(x=FAKE, ldx=1024, w=FAKE, sw=FAKE, bias=NULL, y=FAKE, ldy=256, ac
     (dict(x=NULL), 1), (dict(w=NULL), 1), (dict(sw=NULL), 1), (dict(y=NULL), 1),
     (dict(M=-1), 2), (dict(ldx=512), 2), (dict(ldy=128), 2),
     (dict(N=250, ldy=256), 3), (dict(K=1000, ldx=1000), 3), (dict(K=0), 3),
+    (dict(M=1 << 23, N=16, ldy=16), 3),  # more 64-row blocks than the grid's z dimension holds
     (dict(x=MISALIGNED), 4), (dict(acc=MISALIGNED), 4), (dict(ldx=1028), 4), (dict(bias=MISALIGNED), 4),
     (dict(ws=NULL, ws_bytes=0, K=32768, ldx=32768), 5), (dict(ws_bytes=8, K=32768, ldx=32768), 5),
 ])
