@@ -24,7 +24,8 @@
  *   - M = 0 (or N = 0) is a valid no-op.
  *   - Layouts are row-major.  `ld*` arguments are row strides in elements.
  *   - Shape limits: K % 128 == 0, 128 <= K <= 32768, N % 16 == 0, b a power of two
- *     with 1 <= b <= 256 and K % b == 0, bits in {4, 8}, 0 < clip_ratio <= 1.
+ *     with 1 <= b <= 256 and K % b == 0, bits in {4, 8}, 0 < clip_ratio <= 1; for the
+ *     GEMMs M, N <= 2^24 and M * N <= 2^40 (FQ_ERR_UNSUPPORTED beyond).
  *   - Alignment: every pointer 16-byte aligned; ldx and ldy multiples of 8.
  *
  * Numerical contract of the prologue (so that codes are reproducible bit for bit):
@@ -164,7 +165,7 @@ fq_status fq_gemm_w8a8(const void *a_codes, const float *delta, const void *w_pa
  * The sums are floating point on the bf16 matrix cores (every product of a bf16 and a
  * code is exact in fp32; the additions round), so they agree with an exact sum within
  * (K - 1) 2^-24 sum_c |x_tc q_jc|, not bit for bit.  Same shape limits as the other
- * entry points. */
+ * entry points, and M <= 64 * 65535. */
 size_t fq_gemm_w4a16_workspace_bytes(int64_t M, int64_t N, int64_t K);
 fq_status fq_gemm_w4a16(const void *x_bf16, int64_t ldx, const void *w_packed, const float *w_scale,
                         const float *bias, void *y_bf16, int64_t ldy, float *acc_out, int64_t M,
