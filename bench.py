@@ -439,14 +439,13 @@ def measure_gptq_points(torch, fq, synth, dev, log_fn):
         b = 128
         calib = synth.activations(T, K, seed=K + 5, outlier_frac=0.005, outlier_scale=50.0).to(dev)
         w = torch.from_numpy(synth.weights(N, K, seed=K + N)).to(dev)
-        c_b = float(torch.tensor(1.0 / b ** 0.5, dtype=torch.float32).item())
         z = fq.transform(calib, b)
         w_t = fq.transform(w, b)
         G = fq.gptq_hessian(z)
         U = fq.gptq_factor(G)
         stages = (("hessian", lambda: fq.gptq_hessian(z, G), T * K * (K + 1)),
                   ("factor", lambda: fq.gptq_factor(G), 2 * K ** 3 / 3),
-                  ("sweep", lambda: fq.gptq_sweep(w_t, U, 4, c_b), N * K ** 2))
+                  ("sweep", lambda: fq.gptq_sweep(w_t, U, b, 4), N * K ** 2))
         rec = {"name": name, "kind": "gptq", "N": N, "K": K, "T": T, "b": b, "bits": 4}
         total = 0.0
         for sname, fn, flops in stages:

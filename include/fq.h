@@ -25,8 +25,13 @@
  *   - Layouts are row-major.  `ld*` arguments are row strides in elements.
  *   - Shape limits: K % 128 == 0, 128 <= K <= 32768, N % 16 == 0, b a power of two
  *     with 1 <= b <= 256 and K % b == 0, bits in {4, 8}, 0 < clip_ratio <= 1; for the
- *     GEMMs M, N <= 2^24 and M * N <= 2^40 (FQ_ERR_UNSUPPORTED beyond).
+ *     GEMMs M, N <= 2^24 and M * N <= 2^40 (FQ_ERR_UNSUPPORTED beyond).  K is held to
+ *     whole 128-channel steps because the kernel-native weight tiles and every k step of
+ *     the GEMMs span 128 input channels; the paper's only requirement is that b divides K
+ *     (Sec. III-C), and every layer width of the workloads is a multiple of 1024.
  *   - Alignment: every pointer 16-byte aligned; ldx and ldy multiples of 8.
+ *   - No aliasing: an output (codes, scales, y, acc_out, a workspace) may not overlap
+ *     another output or an input, over the bytes the call touches (FQ_ERR_ALIAS).
  *
  * Numerical contract of the prologue (so that codes are reproducible bit for bit):
  *   the transform is an fp32 butterfly on the UNNORMALIZED Sylvester matrix with
@@ -55,7 +60,8 @@ typedef enum {
   FQ_ERR_UNSUPPORTED = 3, /* sizes outside the supported range, bad b / bits / clip ratio */
   FQ_ERR_ALIGN = 4,       /* pointer or leading dimension misaligned */
   FQ_ERR_WORKSPACE = 5,   /* workspace missing or smaller than required */
-  FQ_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed */
+  FQ_ERR_HIP = 6,         /* a HIP runtime call or kernel launch failed */
+  FQ_ERR_ALIAS = 7        /* an output buffer overlaps another output or an input */
 } fq_status;
 
 /* Runtime prologue, Alg. 1 runtime steps 1-2 (Sec. III-C transform, eq. (5)).
@@ -226,19 +232,19 @@ fq_status fq_gptq_factor(const double *G, int64_t K, double damp, double *U, voi
                          void *stream);
 
 /* The GPTQ column sweep over folded weight rows w_t fp32 [N, ldw] (fq_transform's output
- * for the weights), with U from fq_gptq_factor.  Contract (fp64; the codes are
- * reproducible bit for bit): per row A = max |w|, scale = fl32((A * scale_mult) / q)
- * (scale_mult = 1/sqrt(b) as a float for the block Hadamard, so the scale equals
- * fq_quantize_weights'), inv = q / A and step = A / q; columns in blocks of 128; column c:
- * code = clamp(rint(w_c * inv), -q, q), e = (w_c - code * step) / U[c][c], each later
- * column c' of the block w_c' = fma(-e, U[c][c'], w_c'); after the block, each later
- * column w_c' -= (fma chain over the block's k ascending of e_k * U[k][c'] from +0).
- * A zero row gives codes 0 and scale 0.  w_codes int8 [N, K] (pack with fq_pack_weights);
- * w_scale fp32 [N]; ws: fq_gptq_sweep_workspace_bytes(N, K) bytes, no initialization. */
+ * for the weights, with the same block size b), with U from fq_gptq_factor.  Contract
+ * (fp64; the codes are reproducible bit for bit): per row A = max |w|, scale =
+ * fl32((A * c_b) / q) with c_b the float nearest 1/sqrt(b) (the block Hadamard's
+ * normalization, deferred to the scale exactly as in fq_quantize_weights), inv = q / A and
+ * step = A / q; columns in blocks of 128; column c: code = clamp(rint(w_c * inv), -q, q),
+ * e = (w_c - code * step) / U[c][c], each later column c' of the block w_c' =
+ * fma(-e, U[c][c'], w_c'); after the block, each later column w_c' -= (fma chain over the
+ * block's k ascending of e_k * U[k][c'] from +0).  A zero row gives codes 0 and scale 0.
+ * w_codes int8 [N, K] (pack with fq_pack_weights); w_scale fp32 [N];
+ * ws: fq_gptq_sweep_workspace_bytes(N, K) bytes, no initialization. */
 size_t fq_gptq_sweep_workspace_bytes(int64_t N, int64_t K);
-fq_status fq_gptq_sweep(const float *w_t, int64_t ldw, const double *U, int64_t N, int64_t K, int bits,
-                        float scale_mult, int8_t *w_codes, float *w_scale, void *ws, size_t ws_bytes,
-                        void *stream);
+fq_status fq_gptq_sweep(const float *w_t, int64_t ldw, const double *U, int64_t N, int64_t K, int b, int bits,
+                        int8_t *w_codes, float *w_scale, void *ws, size_t ws_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 
 #include "../../include/fq.h"
 #include "fq_launch.hpp"
@@ -36,6 +37,27 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 bool is_pow2(int64_t v) { return v >= 1 && (v & (v - 1)) == 0; }
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Byte range [p, p + n) of a caller buffer, for the no-overlap preconditions.
+struct Span {
+  uintptr_t lo, hi;
+};
+Span span(const void *p, size_t n) { return Span{reinterpret_cast<uintptr_t>(p), reinterpret_cast<uintptr_t>(p) + n}; }
+bool overlap(Span a, Span b) { return a.lo && b.lo && a.lo < b.hi && b.lo < a.hi; }
+// True when an output range overlaps another output or any input (NULL ranges are empty).
+bool outputs_alias(std::initializer_list<Span> outs, std::initializer_list<Span> ins) {
+  for (auto o = outs.begin(); o != outs.end(); ++o) {
+    for (auto p = o + 1; p != outs.end(); ++p)
+      if (overlap(*o, *p)) return true;
+    for (const Span &i : ins)
+      if (overlap(*o, i)) return true;
+  }
+  return false;
+}
+// Bytes spanned by `rows` rows of `row_bytes` bytes at a stride of `ld_bytes`.
+size_t rows_span(int64_t rows, int64_t ld_bytes, int64_t row_bytes) {
+  return rows <= 0 ? 0 : (size_t)(rows - 1) * (size_t)ld_bytes + (size_t)row_bytes;
+}
 
 constexpr int64_t kMaxK = 32768;
 constexpr int64_t kMaxGptqK = 16384;  // the factor holds two K x K fp64 matrices
@@ -92,6 +114,18 @@ fq_status check_prologue(const void *x, int64_t ldx, int ld_mult, const float *s
   return FQ_OK;
 }
 
+// No-overlap precondition of a prologue: the codes, the scales and `extra` (a workspace, or
+// an empty span) against each other and against the rows, the multipliers and `extra_in`.
+fq_status check_prologue_alias(const void *x, int64_t ldx, int in_bytes, const float *smooth, const float *post,
+                               int64_t M, int64_t K, int bits, const void *codes, const float *delta,
+                               Span extra = Span{0, 0}, Span extra_in = Span{0, 0}) {
+  if (outputs_alias({span(codes, (size_t)M * (size_t)K * (size_t)bits / 8), span(delta, (size_t)M * 4), extra},
+                    {span(x, rows_span(M, ldx * in_bytes, K * in_bytes)), span(smooth, (size_t)K * 4),
+                     span(post, (size_t)K * 4), extra_in}))
+    return fail(FQ_ERR_ALIAS, "codes, scales and workspace must not overlap each other or an input");
+  return FQ_OK;
+}
+
 fq_status check_gemm(const void *a, const float *delta, const void *w, const float *w_scale,
                      const float *bias, const void *y, int64_t ldy, const int32_t *acc_out,
                      int64_t M, int64_t N, int64_t K) {
@@ -115,7 +149,7 @@ fq_status check_gemm(const void *a, const float *delta, const void *w, const flo
 fq_status gemm_common(const void *a_codes, int a_fmt, int64_t lda, const float *delta,
                       const void *w_packed, const float *w_scale, const float *bias, void *y,
                       int64_t ldy, int32_t *acc_out, int64_t M, int64_t N, int64_t K, int bits,
-                      void *ws, size_t ws_bytes, hipStream_t stream) {
+                      void *ws, size_t ws_bytes, hipStream_t stream, bool go = true) {
   const fq::GemmPlan pl = fq::plan_gemm(M, N, K, bits);
   const size_t need = fq::gemm_plan_workspace(pl);
   if (need > 0 && (!ws || ws_bytes < need))
@@ -136,8 +170,8 @@ fq_status gemm_common(const void *a_codes, int a_fmt, int64_t lda, const float *
   g.N = N;
   g.K = K;
   g.bits = bits;
-  hipError_t e = fq::launch_gemm(g, pl, ws, stream);
-  if (e != hipSuccess) return hip_fail(e, "gemm launch");
+  hipError_t e = fq::launch_gemm(g, pl, ws, stream, go);
+  if (e != hipSuccess) return hip_fail(e, go ? "gemm launch" : "gemm kernel selection");
   return ok();
 }
 
@@ -149,8 +183,69 @@ fq_status gemm_entry(int bits, const void *a_codes, const float *delta, const vo
   if (M == 0 || N == 0) return ok();
   const int a_fmt = bits == 4 ? fq::kANibble : fq::kAInt8;
   const int64_t lda = bits == 4 ? K / 2 : K;
+  const size_t need = fq_gemm_workspace_bytes(M, N, K, bits);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (outputs_alias({span(y, rows_span(M, ldy * 2, N * 2)), span(acc_out, acc_out ? (size_t)M * N * 4 : 0),
+                     span(need ? ws : nullptr, need)},
+                    {span(a_codes, (size_t)M * lda), span(delta, (size_t)M * 4),
+                     span(w_packed, fq_packed_weight_bytes(N, K, bits)), span(w_scale, (size_t)N * 4),
+                     span(bias, bias ? (size_t)N * 4 : 0)}))
+    return fail(FQ_ERR_ALIAS, "y, acc_out and the workspace must not overlap each other or an input");
   return gemm_common(a_codes, a_fmt, lda, delta, w_packed, w_scale, bias, y, ldy, acc_out, M, N, K,
                      bits, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+// fq_linear workspace: [codes (nibbles for W4A4, int8 for W8A8)][delta][split-K partials]
+size_t linear_ws_bytes(int64_t M, int64_t N, int64_t K, int bits) {
+  if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
+  return align256((size_t)M * (size_t)K * (size_t)bits / 8) + align256((size_t)M * 4) +
+         fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
+}
+
+// The fused projection: both stages are validated, and the GEMM's kernel is resolved,
+// before the prologue is enqueued, so a failing call enqueues nothing.
+fq_status linear_common(const void *x_bf16, int64_t ldx, const float *smooth_inv, const float *post_inv,
+                        int64_t M, int64_t K, int64_t N, int b, int bits, float clip_ratio,
+                        const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,
+                        int64_t ldy, void *ws, size_t ws_bytes, void *stream) {
+  fq_status s = check_prologue_shape(ldx, 8, M, K, b, bits, clip_ratio);
+  if (s != FQ_OK) return s;
+  if (M > 0 && smooth_inv && !aligned16(smooth_inv)) return fail(FQ_ERR_ALIGN, "smooth_inv must be 16-byte aligned");
+  if (M > 0 && post_inv && !aligned16(post_inv)) return fail(FQ_ERR_ALIGN, "post_inv must be 16-byte aligned");
+  s = check_gemm(x_bf16, w_scale, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K);
+  if (s != FQ_OK) return s;
+  if (M == 0 || N == 0) return ok();
+  const size_t codes_bytes = align256((size_t)M * (size_t)K * (size_t)bits / 8);
+  const size_t delta_bytes = align256((size_t)M * 4);
+  const size_t need = linear_ws_bytes(M, N, K, bits);
+  if (!ws || ws_bytes < need)
+    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
+  if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  if (outputs_alias({span(y_bf16, rows_span(M, ldy * 2, N * 2)), span(ws, need)},
+                    {span(x_bf16, rows_span(M, ldx * 2, K * 2)), span(smooth_inv, smooth_inv ? (size_t)K * 4 : 0),
+                     span(post_inv, post_inv ? (size_t)K * 4 : 0), span(w_packed, fq_packed_weight_bytes(N, K, bits)),
+                     span(w_scale, (size_t)N * 4), span(bias, bias ? (size_t)N * 4 : 0)}))
+    return fail(FQ_ERR_ALIAS, "y and the workspace must not overlap each other or an input");
+  uint8_t *codes = static_cast<uint8_t *>(ws);
+  float *delta = reinterpret_cast<float *>(codes + codes_bytes);
+  void *gws = codes + codes_bytes + delta_bytes;
+  const size_t gws_bytes = ws_bytes - codes_bytes - delta_bytes;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // W4A4 codes between the two kernels are canonical nibbles (half the bytes of int8, the
+  // same per-step cost in the GEMMs, which widen them in registers); W8A8 codes are int8.
+  const bool nibble = bits == 4;
+  const int fmt = nibble ? fq::kOutNibble : fq::kOutInt8;
+  const int afmt = nibble ? fq::kANibble : fq::kAInt8;
+  const int64_t lda = nibble ? K / 2 : K;
+  s = gemm_common(codes, afmt, lda, delta, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K, bits, gws,
+                  gws_bytes, st, /*go=*/false);
+  if (s != FQ_OK) return s;
+  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, post_inv, M, (int)K, b, bits,
+                                       clip_ratio, inv_sqrt_pow2(b), codes, lda, delta, fmt, st);
+  if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
+  return gemm_common(codes, afmt, lda, delta, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K, bits, gws,
+                     gws_bytes, st);
 }
 
 fq_status rotate_common(const void *x, bool x_f32, int64_t ldx, const int32_t *perm, const float *blocks,
@@ -170,6 +265,10 @@ fq_status rotate_common(const void *x, bool x_f32, int64_t ldx, const int32_t *p
   if (!ws || ws_bytes < need)
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  s = check_prologue_alias(x, ldx, x_f32 ? 4 : 2, pre, post, M, K, fmt == fq::kOutNibble ? 4 : 8, codes, delta,
+                           span(ws, need), span(blocks, (size_t)K * b * 4));
+  if (s != FQ_OK) return s;
+  if (perm && overlap(span(perm, (size_t)K * 4), span(ws, need))) return fail(FQ_ERR_ALIAS, "perm overlaps the workspace");
   hipError_t e = fq::launch_rotate_quant(x, x_f32, ldx, perm, blocks, pre, post, M, (int)K, b, bits, r,
                                          static_cast<uint8_t *>(codes), ldc, delta, fmt,
                                          static_cast<float *>(ws), static_cast<hipStream_t>(stream));
@@ -190,6 +289,7 @@ const char *fq_status_string(fq_status s) {
     case FQ_ERR_ALIGN: return "misaligned pointer or leading dimension";
     case FQ_ERR_WORKSPACE: return "workspace too small";
     case FQ_ERR_HIP: return "HIP runtime error";
+    case FQ_ERR_ALIAS: return "output overlaps another buffer";
   }
   return "unknown status";
 }
@@ -202,6 +302,8 @@ fq_status fq_fwht_quant(const void *x_bf16, int64_t ldx, const float *smooth_inv
   fq_status s = check_prologue(x_bf16, ldx, 8, smooth_inv, post_inv, M, K, b, bits, clip_ratio, a_codes, delta);
   if (s != FQ_OK) return s;
   if (M == 0) return ok();
+  s = check_prologue_alias(x_bf16, ldx, 2, smooth_inv, post_inv, M, K, bits, a_codes, delta);
+  if (s != FQ_OK) return s;
   const int fmt = bits == 4 ? fq::kOutNibble : fq::kOutInt8;
   const int64_t ldc = bits == 4 ? K / 2 : K;
   hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, post_inv, M, (int)K, b, bits,
@@ -217,6 +319,8 @@ fq_status fq_quantize_weights(const float *w, int64_t ldw, const float *col_scal
   fq_status s = check_prologue(w, ldw, 4, col_scale, post_scale, N, K, b, bits, 1.0f, w_codes, w_scale);
   if (s != FQ_OK) return s;
   if (N == 0) return ok();
+  s = check_prologue_alias(w, ldw, 4, col_scale, post_scale, N, K, 8, w_codes, w_scale);
+  if (s != FQ_OK) return s;
   hipError_t e = fq::launch_fwht_quant(w, true, ldw, col_scale, post_scale, N, (int)K, b, bits, 1.0f,
                                        inv_sqrt_pow2(b), reinterpret_cast<uint8_t *>(w_codes), K,
                                        w_scale, fq::kOutInt8, static_cast<hipStream_t>(stream));
@@ -263,6 +367,8 @@ fq_status fq_pack_weights(const int8_t *w_codes, int64_t N, int64_t K, int bits,
   if (N == 0) return ok();
   if (!w_codes || !w_packed) return fail(FQ_ERR_NULL, "w_codes and w_packed must be non-NULL");
   if (!aligned16(w_codes) || !aligned16(w_packed)) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  if (overlap(span(w_codes, (size_t)N * K), span(w_packed, fq_packed_weight_bytes(N, K, bits))))
+    return fail(FQ_ERR_ALIAS, "w_codes and w_packed must not overlap");
   hipError_t e = fq::launch_pack_weights(w_codes, N, (int)K, bits, static_cast<uint8_t *>(w_packed),
                                          static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack launch");
@@ -279,6 +385,8 @@ fq_status fq_unpack_weights(const void *w_packed, int64_t N, int64_t K, int bits
   if (N == 0) return ok();
   if (!w_codes || !w_packed) return fail(FQ_ERR_NULL, "w_codes and w_packed must be non-NULL");
   if (!aligned16(w_codes) || !aligned16(w_packed)) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  if (overlap(span(w_codes, (size_t)N * K), span(w_packed, fq_packed_weight_bytes(N, K, bits))))
+    return fail(FQ_ERR_ALIAS, "w_codes and w_packed must not overlap");
   hipError_t e = fq::launch_unpack_weights(static_cast<const uint8_t *>(w_packed), N, (int)K, bits,
                                            w_codes, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "unpack launch");
@@ -338,50 +446,26 @@ fq_status fq_gemm_w4a16(const void *x_bf16, int64_t ldx, const void *w_packed, c
   g.M = M;
   g.N = N;
   g.K = K;
+  if (outputs_alias({span(y_bf16, rows_span(M, ldy * 2, N * 2)), span(acc_out, acc_out ? (size_t)M * N * 4 : 0),
+                     span(pl.partial_bytes ? ws : nullptr, pl.partial_bytes)},
+                    {span(x_bf16, rows_span(M, ldx * 2, K * 2)), span(w_packed, fq_packed_weight_bytes(N, K, 4)),
+                     span(w_scale, (size_t)N * 4), span(bias, bias ? (size_t)N * 4 : 0)}))
+    return fail(FQ_ERR_ALIAS, "y, acc_out and the workspace must not overlap each other or an input");
   hipError_t e = fq::launch_w4a16(g, pl, ws, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "w4a16 launch");
   return ok();
 }
 
-// fq_linear workspace: [codes (nibbles for W4A4, int8 for W8A8)][delta][split-K partials]
 size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
-  if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
-  return align256((size_t)M * (size_t)K * (size_t)bits / 8) + align256((size_t)M * 4) +
-         fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
+  return linear_ws_bytes(M, N, K, bits);
 }
 
 fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, const float *post_inv,
                     int64_t M, int64_t K, int64_t N, int b, int bits, float clip_ratio,
                     const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,
                     int64_t ldy, void *ws, size_t ws_bytes, void *stream) {
-  // validate both stages before enqueueing either
-  fq_status s = check_prologue_shape(ldx, 8, M, K, b, bits, clip_ratio);
-  if (s != FQ_OK) return s;
-  if (M > 0 && smooth_inv && !aligned16(smooth_inv)) return fail(FQ_ERR_ALIGN, "smooth_inv must be 16-byte aligned");
-  if (M > 0 && post_inv && !aligned16(post_inv)) return fail(FQ_ERR_ALIGN, "post_inv must be 16-byte aligned");
-  s = check_gemm(x_bf16, w_scale, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K);
-  if (s != FQ_OK) return s;
-  if (M == 0 || N == 0) return ok();
-  const size_t codes_bytes = align256((size_t)M * (size_t)K * (size_t)bits / 8);
-  const size_t delta_bytes = align256((size_t)M * 4);
-  const size_t need = fq_linear_workspace_bytes(M, N, K, bits);
-  if (!ws || ws_bytes < need)
-    return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
-  if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
-  uint8_t *codes = static_cast<uint8_t *>(ws);
-  float *delta = reinterpret_cast<float *>(codes + codes_bytes);
-  void *gws = codes + codes_bytes + delta_bytes;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  // W4A4 codes between the two kernels are canonical nibbles (half the bytes of int8, the
-  // same per-step cost in the GEMMs, which widen them in registers); W8A8 codes are int8.
-  const bool nibble = bits == 4;
-  const int fmt = nibble ? fq::kOutNibble : fq::kOutInt8;
-  const int64_t lda = nibble ? K / 2 : K;
-  hipError_t e = fq::launch_fwht_quant(x_bf16, false, ldx, smooth_inv, post_inv, M, (int)K, b, bits,
-                                       clip_ratio, inv_sqrt_pow2(b), codes, lda, delta, fmt, st);
-  if (e != hipSuccess) return hip_fail(e, "fwht_quant launch");
-  return gemm_common(codes, nibble ? fq::kANibble : fq::kAInt8, lda, delta, w_packed, w_scale, bias, y_bf16,
-                     ldy, nullptr, M, N, K, bits, gws, ws_bytes - codes_bytes - delta_bytes, st);
+  return linear_common(x_bf16, ldx, smooth_inv, post_inv, M, K, N, b, bits, clip_ratio, w_packed, w_scale, bias,
+                       y_bf16, ldy, ws, ws_bytes, stream);
 }
 
 // ---- GPTQ in the transformed coordinates (eq. (7)) ----
@@ -394,6 +478,13 @@ fq_status fq_transform(const void *x, int x_is_f32, int64_t ldx, const float *pr
   if (!x || !z) return fail(FQ_ERR_NULL, "x and z must be non-NULL");
   if (!aligned16(x) || !aligned16(z) || (pre_mult && !aligned16(pre_mult)) || (post_mult && !aligned16(post_mult)))
     return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  {
+    const int in_bytes = x_is_f32 ? 4 : 2;
+    if (outputs_alias({span(z, (size_t)M * K * 4)}, {span(x, rows_span(M, ldx * in_bytes, K * in_bytes)),
+                                                      span(pre_mult, pre_mult ? (size_t)K * 4 : 0),
+                                                      span(post_mult, post_mult ? (size_t)K * 4 : 0)}))
+      return fail(FQ_ERR_ALIAS, "z must not overlap an input");
+  }
   hipError_t e = fq::launch_transform(x, x_is_f32 != 0, ldx, pre_mult, post_mult, M, (int)K, b, z,
                                       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "transform launch");
@@ -409,6 +500,8 @@ fq_status fq_gptq_hessian(const float *z, int64_t ldz, int64_t T, int64_t K, dou
   if (ldz < K) return fail(FQ_ERR_SHAPE, "ldz=%lld < K=%lld", (long long)ldz, (long long)K);
   if (!G || (T > 0 && !z)) return fail(FQ_ERR_NULL, "z and G must be non-NULL");
   if (!aligned16(G) || (z && !aligned16(z))) return fail(FQ_ERR_ALIGN, "pointers must be 16-byte aligned");
+  if (T > 0 && overlap(span(G, (size_t)K * K * 8), span(z, rows_span(T, ldz * 4, K * 4))))
+    return fail(FQ_ERR_ALIAS, "G must not overlap z");
   hipError_t e = fq::launch_gptq_hessian(z, ldz, T, (int)K, G, accumulate != 0, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "gptq_hessian launch");
   return ok();
@@ -431,6 +524,8 @@ fq_status fq_gptq_factor(const double *G, int64_t K, double damp, double *U, voi
   if (!ws || ws_bytes < need)
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  if (outputs_alias({span(U, (size_t)K * K * 8), span(ws, need)}, {span(G, (size_t)K * K * 8)}))
+    return fail(FQ_ERR_ALIAS, "U and the workspace must not overlap each other or G");
   hipError_t e = fq::launch_gptq_factor(G, (int)K, damp, U, ws, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "gptq_factor launch");
   return ok();
@@ -441,15 +536,14 @@ size_t fq_gptq_sweep_workspace_bytes(int64_t N, int64_t K) {
   return fq::gptq_sweep_ws_bytes(N, (int)K);
 }
 
-fq_status fq_gptq_sweep(const float *w_t, int64_t ldw, const double *U, int64_t N, int64_t K, int bits,
-                        float scale_mult, int8_t *w_codes, float *w_scale, void *ws, size_t ws_bytes,
-                        void *stream) {
+fq_status fq_gptq_sweep(const float *w_t, int64_t ldw, const double *U, int64_t N, int64_t K, int b, int bits,
+                        int8_t *w_codes, float *w_scale, void *ws, size_t ws_bytes, void *stream) {
   fq_status s;
   if (N < 0) return fail(FQ_ERR_SHAPE, "N=%lld < 0", (long long)N);
   if ((s = check_k(K)) != FQ_OK) return s;
   if ((s = check_bits(bits)) != FQ_OK) return s;
+  if ((s = check_block(b, K)) != FQ_OK) return s;
   if (ldw < K) return fail(FQ_ERR_SHAPE, "ldw=%lld < K=%lld", (long long)ldw, (long long)K);
-  if (!(scale_mult > 0.0f)) return fail(FQ_ERR_UNSUPPORTED, "scale_mult=%g must be positive", (double)scale_mult);
   if (N > (1ll << 24)) return fail(FQ_ERR_UNSUPPORTED, "N=%lld too large", (long long)N);
   if (N == 0) return ok();
   if (!w_t || !U || !w_codes || !w_scale) return fail(FQ_ERR_NULL, "w_t, U, w_codes and w_scale must be non-NULL");
@@ -459,7 +553,11 @@ fq_status fq_gptq_sweep(const float *w_t, int64_t ldw, const double *U, int64_t 
   if (!ws || ws_bytes < need)
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
-  hipError_t e = fq::launch_gptq_sweep(w_t, ldw, U, N, (int)K, bits, scale_mult, w_codes, w_scale, ws,
+  if (outputs_alias({span(w_codes, (size_t)N * K), span(w_scale, (size_t)N * 4), span(ws, need)},
+                    {span(w_t, rows_span(N, ldw * 4, K * 4)), span(U, (size_t)K * K * 8)}))
+    return fail(FQ_ERR_ALIAS, "codes, scales and the workspace must not overlap each other or an input");
+  // the block Hadamard's normalization, deferred to the scale as in the prologue
+  hipError_t e = fq::launch_gptq_sweep(w_t, ldw, U, N, (int)K, bits, inv_sqrt_pow2(b), w_codes, w_scale, ws,
                                        static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "gptq_sweep launch");
   return ok();

@@ -31,8 +31,6 @@
 #include "fq_launch.hpp"
 #include <type_traits>
 
-#include <cstdlib>
-#include <cstring>
 
 namespace fq {
 
@@ -871,48 +869,7 @@ static constexpr size_t tile_lds_bytes() {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Development tuning override, read once: FQ_TUNE="splits=<n>" (and the other fields' names).
-struct Tune {
-  int splits = 0;
-  int wk = 0, kt = 0, wc = 0;
-  int stages = 0;
-  int loader = -1;
-  int rb = 0;
-  int order = -1;
-  int bm = 0, bn = 0;  // tiled workgroup tile (64 or 128)
-  int w16kt = 0;  // k steps per wave group of the single-token weight-only kernel
-};
-static Tune read_tune() {
-  Tune t;
-  const char *e = getenv("FQ_TUNE");
-  if (!e) return t;
-  const char *s = strstr(e, "splits=");
-  if (s) t.splits = atoi(s + 7);
-  const char *g = strstr(e, "stages=");
-  if (g) t.stages = atoi(g + 7);
-  const char *w = strstr(e, "wk=");
-  if (w) t.wk = atoi(w + 3);
-  const char *k = strstr(e, "kt=");
-  if (k) t.kt = atoi(k + 3);
-  const char *c = strstr(e, "wc=");
-  if (c) t.wc = atoi(c + 3);
-  const char *l = strstr(e, "loader=");
-  if (l) t.loader = atoi(l + 7);
-  const char *r = strstr(e, "rb=");
-  if (r) t.rb = atoi(r + 3);
-  const char *o = strstr(e, "order=");
-  if (o) t.order = atoi(o + 6);
-  const char *tbm = strstr(e, "bm=");
-  if (tbm) t.bm = atoi(tbm + 3);
-  const char *tbn = strstr(e, "bn=");
-  if (tbn) t.bn = atoi(tbn + 3);
-  const char *w16 = strstr(e, "w16slice=");
-  if (w16) t.w16kt = atoi(w16 + 9);
-  return t;
-}
-
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
-  static const Tune tune = read_tune();
   GemmPlan pl{};
   const int ktot = (int)(K / kTileK);
   if (M <= 64) {
@@ -934,14 +891,6 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       pl.wk = 4;
       pl.kt = per <= 4 ? 1 : (per <= 8 ? 2 : (per <= 16 ? 4 : 8));
     }
-    if (tune.splits > 0) {
-      int per = (ktot + tune.splits - 1) / tune.splits;  // k steps per slice
-      pl.wk = per > 16 && bits == 4 ? 4 : (per > 8 ? 2 : 1);
-      int kt = (per + pl.wk - 1) / pl.wk;
-      pl.kt = kt >= 8 ? 8 : (kt >= 4 ? 4 : (kt >= 2 ? 2 : 1));
-    }
-    if (tune.wk > 0) pl.wk = tune.wk;
-    if (tune.kt > 0) pl.kt = tune.kt;
     pl.ksteps = pl.kt * pl.wk;
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
     pl.wc = 4;
@@ -950,7 +899,6 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
         pl.wc = wc;
         break;
       }
-    if (tune.wc > 0) pl.wc = tune.wc;
     pl.tiles = (N + 16 * pl.wc - 1) / (16 * pl.wc);
     // A grid that fills at most half the compute units also splits the rows: one 16-row
     // tile per workgroup, so each workgroup widens a quarter of the activation codes
@@ -958,7 +906,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     // row blocks read the same weights; when the tile count is a multiple of 8 they run
     // on one XCD (workgroups go round-robin over the 8 XCDs) and its L2 serves the repeats.
     pl.rb = 1;
-    if (tune.rb <= 0 && M > 16 && pl.tiles * pl.splits <= 128) {
+    if (M > 16 && pl.tiles * pl.splits <= 128) {
       pl.mt = 1;
       pl.rb = (int)((M + 15) / 16);
     }
@@ -967,8 +915,7 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     // workgroup streams four times the weights of the 64-row plan (its sibling row blocks
     // share them through the XCD's L2), but K needs no split: the split-K epilogue goes
     // away.  Measured at M = 50, K 16384 -> N 2048: 11.1 against 11.7 us.
-    if (bits == 4 && M > 32 && ktot >= 128 && tune.splits <= 0 && tune.kt <= 0 && tune.wk <= 0 && tune.rb <= 0 &&
-        tune.wc <= 0) {
+    if (bits == 4 && M > 32 && ktot >= 128) {
       pl.mt = 1;
       pl.rb = (int)((M + 15) / 16);
       pl.wk = 4;
@@ -977,12 +924,6 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       pl.splits = (ktot + 127) / 128;
       pl.wc = 2;
       pl.tiles = (N + 31) / 32;
-    }
-    if (tune.rb > 1) {
-      const int t16 = (int)((M + 15) / 16);
-      const int per = (t16 + tune.rb - 1) / tune.rb;  // 16-row tiles per row block
-      pl.mt = per <= 1 ? 1 : (per <= 2 ? 2 : 4);
-      pl.rb = (int)((M + 16 * pl.mt - 1) / (16 * pl.mt));
     }
   } else {
     pl.kind = 1;
@@ -1002,12 +943,8 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
       if (t128 * slices(t128) <= 128) pl.bm = 64;
     }
-    if (tune.bm == 64 || tune.bm == 128) pl.bm = tune.bm;
-    if (tune.bn == 64 || tune.bn == 128) pl.bn = tune.bn;
-    if (pl.bm == 64 && pl.bn == 64) pl.bn = 128;  // 64 x 64 is not built
     const int64_t tiles = ((M + pl.bm - 1) / pl.bm) * ((N + pl.bn - 1) / pl.bn);
     int64_t s = slices(tiles);
-    if (tune.splits > 0) s = tune.splits < ktot ? tune.splits : ktot;
     pl.ksteps = (int)((ktot + s - 1) / s);
     pl.splits = (ktot + pl.ksteps - 1) / pl.ksteps;
     pl.tiles = tiles;
@@ -1019,12 +956,9 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     const bool lone = tiles * pl.splits <= 256;
     pl.loader = lone && bits == 4 ? 1 : 0;
     pl.stages = lone ? 4 : 3;
-    if (tune.stages > 0) pl.stages = tune.stages;
-    if (tune.loader >= 0) pl.loader = tune.loader;
     // Tile ids in workgroup order, rows of tiles along N (measured 2-4% faster at M = 816
     // than grouping consecutive tiles on one XCD or running down the rows first).
     pl.order = 2;
-    if (tune.order >= 0) pl.order = tune.order & 3;
   }
   pl.partial_bytes = pl.splits > 1 ? align256((size_t)pl.splits * M * N * 4) : 0;
   return pl;
@@ -1032,102 +966,103 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
 
 size_t gemm_plan_workspace(const GemmPlan &pl) { return pl.partial_bytes; }
 
+// Every launcher below takes `go`: false resolves the kernel the plan selects and raises
+// its dynamic-LDS limit without launching anything, so that a caller can find out whether
+// a plan is launchable before it enqueues other work.
 template <int BITS, int AFMT, int MT, int KT, int WK, int WC>
-static hipError_t launch_stream(const GemmParams &p, dim3 grid, hipStream_t s) {
+static hipError_t launch_stream(const GemmParams &p, dim3 grid, hipStream_t s, bool go) {
   const size_t lds = stream_lds_bytes<BITS, AFMT, MT, KT, WK, WC>();
   static std::atomic<uint64_t> attr{0};
   hipError_t e = allow_dynamic_lds(&gemm_stream_kernel<BITS, AFMT, MT, KT, WK, WC>, lds, attr);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !go) return e;
   hipLaunchKernelGGL((gemm_stream_kernel<BITS, AFMT, MT, KT, WK, WC>), grid, dim3(64 * WC * WK), lds, s, p);
   return hipGetLastError();
 }
 
 template <int BITS, int AFMT, int MT, int WC>
-static hipError_t launch_stream_wc(const GemmParams &p, int kt, int wk, dim3 grid, hipStream_t s) {
+static hipError_t launch_stream_wc(const GemmParams &p, int kt, int wk, dim3 grid, hipStream_t s, bool go) {
   if (wk == 4) {
     switch (kt) {
-      case 1: return launch_stream<BITS, AFMT, MT, 1, 4, WC>(p, grid, s);
-      case 2: return launch_stream<BITS, AFMT, MT, 2, 4, WC>(p, grid, s);
-      case 4: return launch_stream<BITS, AFMT, MT, 4, 4, WC>(p, grid, s);
+      case 1: return launch_stream<BITS, AFMT, MT, 1, 4, WC>(p, grid, s, go);
+      case 2: return launch_stream<BITS, AFMT, MT, 2, 4, WC>(p, grid, s, go);
+      case 4: return launch_stream<BITS, AFMT, MT, 4, 4, WC>(p, grid, s, go);
       case 8:
-        if constexpr (AFMT == kANibble) return launch_stream<BITS, AFMT, MT, 8, 4, WC>(p, grid, s);
+        if constexpr (AFMT == kANibble) return launch_stream<BITS, AFMT, MT, 8, 4, WC>(p, grid, s, go);
         return hipErrorInvalidValue;  // a 32-step int8 slice does not fit in LDS
-      default:
+      case 32:
         // one 16-row tile over 128 k steps (nibble codes): the whole of K = 16384 in one slice
-        if constexpr (AFMT == kANibble && MT == 1 && WC == 2) return launch_stream<BITS, AFMT, MT, 32, 4, WC>(p, grid, s);
+        if constexpr (AFMT == kANibble && MT == 1 && WC == 2) return launch_stream<BITS, AFMT, MT, 32, 4, WC>(p, grid, s, go);
         return hipErrorInvalidValue;
+      default: return hipErrorInvalidValue;
     }
   }
-  if (wk == 2) {
+  if (wk == 1) {
     switch (kt) {
-      case 1: return launch_stream<BITS, AFMT, MT, 1, 2, WC>(p, grid, s);
-      case 2: return launch_stream<BITS, AFMT, MT, 2, 2, WC>(p, grid, s);
-      case 4: return launch_stream<BITS, AFMT, MT, 4, 2, WC>(p, grid, s);
-      default: return launch_stream<BITS, AFMT, MT, 8, 2, WC>(p, grid, s);
+      case 1: return launch_stream<BITS, AFMT, MT, 1, 1, WC>(p, grid, s, go);
+      case 2: return launch_stream<BITS, AFMT, MT, 2, 1, WC>(p, grid, s, go);
+      default: return hipErrorInvalidValue;
     }
   }
-  switch (kt) {
-    case 1: return launch_stream<BITS, AFMT, MT, 1, 1, WC>(p, grid, s);
-    case 2: return launch_stream<BITS, AFMT, MT, 2, 1, WC>(p, grid, s);
-    case 4: return launch_stream<BITS, AFMT, MT, 4, 1, WC>(p, grid, s);
-    default: return launch_stream<BITS, AFMT, MT, 8, 1, WC>(p, grid, s);
-  }
+  return hipErrorInvalidValue;
 }
 
 template <int BITS, int AFMT, int MT>
-static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, int wc, dim3 grid, hipStream_t s) {
+static hipError_t launch_stream_mt(const GemmParams &p, int kt, int wk, int wc, dim3 grid, hipStream_t s, bool go) {
   switch (wc) {
-    case 1: return launch_stream_wc<BITS, AFMT, MT, 1>(p, kt, wk, grid, s);
-    case 2: return launch_stream_wc<BITS, AFMT, MT, 2>(p, kt, wk, grid, s);
-    default: return launch_stream_wc<BITS, AFMT, MT, 4>(p, kt, wk, grid, s);
+    case 1: return launch_stream_wc<BITS, AFMT, MT, 1>(p, kt, wk, grid, s, go);
+    case 2: return launch_stream_wc<BITS, AFMT, MT, 2>(p, kt, wk, grid, s, go);
+    case 4: return launch_stream_wc<BITS, AFMT, MT, 4>(p, kt, wk, grid, s, go);
+    default: return hipErrorInvalidValue;
   }
 }
 
 template <int BITS, int AFMT, int BM, int BN, int ST, int LW>
-static hipError_t launch_tile(const GemmParams &p, dim3 grid, hipStream_t s) {
+static hipError_t launch_tile(const GemmParams &p, dim3 grid, hipStream_t s, bool go) {
   constexpr size_t lds = tile_lds_bytes<BITS, AFMT, BM, BN, ST>();
   static_assert(lds <= 160 * 1024, "LDS budget");
   static std::atomic<uint64_t> attr{0};
   hipError_t e = allow_dynamic_lds(&gemm_tile_kernel<BITS, AFMT, BM, BN, ST, LW>, lds, attr);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || !go) return e;
   hipLaunchKernelGGL((gemm_tile_kernel<BITS, AFMT, BM, BN, ST, LW>), grid, dim3(256 + 64 * LW), lds, s, p);
   return hipGetLastError();
 }
 
 template <int BITS, int AFMT, int BM, int BN>
-static hipError_t launch_tile_shape(const GemmParams &p, const GemmPlan &pl, dim3 grid, hipStream_t s) {
+static hipError_t launch_tile_shape(const GemmParams &p, const GemmPlan &pl, dim3 grid, hipStream_t s, bool go) {
+  if (pl.stages != 3 && pl.stages != 4) return hipErrorInvalidValue;
   if (pl.loader) {
     // one wave's loads of STAGES - 2 steps must fit the 6-bit vmcnt: 4 stages only for INT4
     if constexpr (BITS == 4)
-      return pl.stages == 4 ? launch_tile<BITS, AFMT, BM, BN, 4, 1>(p, grid, s)
-                            : launch_tile<BITS, AFMT, BM, BN, 3, 1>(p, grid, s);
+      return pl.stages == 4 ? launch_tile<BITS, AFMT, BM, BN, 4, 1>(p, grid, s, go)
+                            : launch_tile<BITS, AFMT, BM, BN, 3, 1>(p, grid, s, go);
     else
-      return launch_tile<BITS, AFMT, BM, BN, 3, 1>(p, grid, s);
+      return pl.stages == 3 ? launch_tile<BITS, AFMT, BM, BN, 3, 1>(p, grid, s, go) : hipErrorInvalidValue;
   }
-  return pl.stages == 4 ? launch_tile<BITS, AFMT, BM, BN, 4, 0>(p, grid, s)
-                        : launch_tile<BITS, AFMT, BM, BN, 3, 0>(p, grid, s);
+  return pl.stages == 4 ? launch_tile<BITS, AFMT, BM, BN, 4, 0>(p, grid, s, go)
+                        : launch_tile<BITS, AFMT, BM, BN, 3, 0>(p, grid, s, go);
 }
 
 template <int BITS, int AFMT>
-static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStream_t s) {
+static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStream_t s, bool go) {
   hipError_t e;
   if (pl.kind == 0) {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits, (unsigned)pl.rb);
     switch (pl.mt) {
-      case 1: e = launch_stream_mt<BITS, AFMT, 1>(p, pl.kt, pl.wk, pl.wc, grid, s); break;
-      case 2: e = launch_stream_mt<BITS, AFMT, 2>(p, pl.kt, pl.wk, pl.wc, grid, s); break;
-      default: e = launch_stream_mt<BITS, AFMT, 4>(p, pl.kt, pl.wk, pl.wc, grid, s); break;
+      case 1: e = launch_stream_mt<BITS, AFMT, 1>(p, pl.kt, pl.wk, pl.wc, grid, s, go); break;
+      case 2: e = launch_stream_mt<BITS, AFMT, 2>(p, pl.kt, pl.wk, pl.wc, grid, s, go); break;
+      case 4: e = launch_stream_mt<BITS, AFMT, 4>(p, pl.kt, pl.wk, pl.wc, grid, s, go); break;
+      default: e = hipErrorInvalidValue; break;
     }
   } else {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits);
-    if (pl.bm == 64)
-      e = launch_tile_shape<BITS, AFMT, 64, 128>(p, pl, grid, s);
-    else if (pl.bn == 64)
-      e = launch_tile_shape<BITS, AFMT, 128, 64>(p, pl, grid, s);
+    if (pl.bm == 64 && pl.bn == 128)
+      e = launch_tile_shape<BITS, AFMT, 64, 128>(p, pl, grid, s, go);
+    else if (pl.bm == 128 && pl.bn == 128)
+      e = launch_tile_shape<BITS, AFMT, 128, 128>(p, pl, grid, s, go);
     else
-      e = launch_tile_shape<BITS, AFMT, 128, 128>(p, pl, grid, s);
+      e = hipErrorInvalidValue;
   }
-  if (e != hipSuccess || pl.splits == 1) return e;
+  if (e != hipSuccess || pl.splits == 1 || !go) return e;
   const int64_t threads = (int64_t)p.M * (p.N / 4);
   const unsigned blocks = (unsigned)((threads + 255) / 256);
   hipLaunchKernelGGL((splitk_epilogue_kernel<Fmt<BITS, AFMT>::shift>), dim3(blocks), dim3(256), 0, s, p,
@@ -1135,7 +1070,7 @@ static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s) {
+hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s, bool go) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
   GemmParams p;
   p.a = g.a;
@@ -1154,8 +1089,8 @@ hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStrea
   p.partial = pl.splits > 1 ? reinterpret_cast<int32_t *>(ws) : nullptr;
   p.order = pl.order;
   if (g.bits == 4)
-    return g.a_fmt == kANibble ? launch_gemm_t<4, kANibble>(p, pl, s) : hipErrorInvalidValue;
-  return launch_gemm_t<8, kAInt8>(p, pl, s);
+    return g.a_fmt == kANibble ? launch_gemm_t<4, kANibble>(p, pl, s, go) : hipErrorInvalidValue;
+  return launch_gemm_t<8, kAInt8>(p, pl, s, go);
 }
 
 // ----------------------------------------------------------------------------------------
@@ -1351,8 +1286,6 @@ W16Plan plan_w4a16(int64_t M, int64_t N, int64_t K) {
     pl.mt = 1;
     const int per = (ktot + 3) / 4;  // k steps per wave group
     pl.kt = per <= 8 ? 8 : (per <= 16 ? 16 : 8);
-    static const Tune tune = read_tune();
-    if (tune.w16kt == 4 || tune.w16kt == 8 || tune.w16kt == 16 || tune.w16kt == 32) pl.kt = tune.w16kt;
     pl.splits = (ktot + 4 * pl.kt - 1) / (4 * pl.kt);
     pl.tiles = N / 16;
     pl.rb = 1;
@@ -1366,11 +1299,6 @@ W16Plan plan_w4a16(int64_t M, int64_t N, int64_t K) {
   const int smax = 16 / pl.mt;
   const int per = ktot < smax ? ktot : smax;
   pl.kt = per <= 4 ? 1 : (per <= 8 ? 2 : 4);
-  {
-    static const Tune tune = read_tune();
-    if (tune.w16kt >= 1 && tune.w16kt <= 8 && (tune.w16kt & (tune.w16kt - 1)) == 0 && tune.w16kt * 256 * 4 * 16 * pl.mt <= 128 * 1024)
-      pl.kt = tune.w16kt;
-  }
   pl.splits = (ktot + 4 * pl.kt - 1) / (4 * pl.kt);
   pl.tiles = N / 16;
   pl.rb = (int)((M + 16 * pl.mt - 1) / (16 * pl.mt));

@@ -88,8 +88,10 @@ struct GemmArgs {
   int bits;
 };
 
-// ws: at least gemm_plan_workspace(pl) bytes of scratch (no initialization needed)
-hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s);
+// ws: at least gemm_plan_workspace(pl) bytes of scratch (no initialization needed).
+// go = false launches nothing: it only resolves the plan's kernel and raises its LDS
+// limit, returning an error when the plan has no kernel.
+hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s, bool go = true);
 
 // Weight-only INT4 (bf16 activations) projection.
 struct W16Plan {

@@ -17,7 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libfq.so")
 
 FQ_OK = 0
 _STATUS = {1: "FQ_ERR_NULL", 2: "FQ_ERR_SHAPE", 3: "FQ_ERR_UNSUPPORTED", 4: "FQ_ERR_ALIGN",
-           5: "FQ_ERR_WORKSPACE", 6: "FQ_ERR_HIP"}
+           5: "FQ_ERR_WORKSPACE", 6: "FQ_ERR_HIP", 7: "FQ_ERR_ALIAS"}
 
 EXPORTED = ["fq_fwht_quant", "fq_quantize_weights", "fq_packed_weight_bytes", "fq_pack_weights",
             "fq_unpack_weights", "fq_gemm_workspace_bytes", "fq_gemm_w4a4", "fq_gemm_w8a8",
@@ -54,7 +54,7 @@ def _load() -> ctypes.CDLL:
         "fq_transform": [vp, i32, i64, vp, vp, i64, i64, i32, vp, vp],
         "fq_gptq_hessian": [vp, i64, i64, i64, vp, i32, vp],
         "fq_gptq_factor": [vp, i64, ctypes.c_double, vp, vp, sz, vp],
-        "fq_gptq_sweep": [vp, i64, vp, i64, i64, i32, f32, vp, vp, vp, sz, vp],
+        "fq_gptq_sweep": [vp, i64, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -108,6 +108,19 @@ def code_bytes(K: int, bits: int) -> int:
     return K * bits // 8
 
 
+def _require(cond: bool, msg: str) -> None:
+    if not cond:
+        raise ValueError(msg)
+
+
+def _check_out(out: Optional[torch.Tensor], M: int, N: int) -> None:
+    """A caller-supplied output must be what the library writes: bf16 [M, N] rows with unit
+    column stride (the row stride is passed on as ldy)."""
+    if out is not None:
+        _require(out.dtype == torch.bfloat16 and tuple(out.shape) == (M, N) and (M == 0 or out.stride(1) == 1),
+                 "out: bf16 [M, N] with unit column stride")
+
+
 def fwht_quant(x: torch.Tensor, b: int, bits: int, clip_ratio: float = 1.0,
                smooth_inv: Optional[torch.Tensor] = None, out_codes: Optional[torch.Tensor] = None,
                out_delta: Optional[torch.Tensor] = None,
@@ -116,6 +129,12 @@ def fwht_quant(x: torch.Tensor, b: int, bits: int, clip_ratio: float = 1.0,
     smooth_inv: fold-before S^-1 (before the rotation); post_inv: fold-after P^-1 (after it)."""
     M, K = x.shape
     assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
+    if out_codes is not None:
+        _require(out_codes.dtype in (torch.uint8, torch.int8) and out_codes.is_contiguous()
+                 and tuple(out_codes.shape) == (M, code_bytes(K, bits)), "out_codes: contiguous [M, K*bits/8] bytes")
+    if out_delta is not None:
+        _require(out_delta.dtype == torch.float32 and out_delta.is_contiguous() and out_delta.numel() == M,
+                 "out_delta: contiguous fp32 [M]")
     codes = out_codes if out_codes is not None else torch.empty((M, code_bytes(K, bits)), dtype=torch.uint8, device=x.device)
     delta = out_delta if out_delta is not None else torch.empty((M,), dtype=torch.float32, device=x.device)
     _check(LIB.fq_fwht_quant(_p(x), x.stride(0) if M else K, _p(smooth_inv), _p(post_inv), M, K, b, bits,
@@ -172,6 +191,9 @@ def gemm(a_codes: torch.Tensor, delta: torch.Tensor, w_packed: torch.Tensor, w_s
          ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None):
     """Integer GEMM + eq. (8) epilogue.  Returns y bf16 [M, N] (and int32 acc if want_acc)."""
     M = a_codes.shape[0]
+    _require(a_codes.dtype in (torch.uint8, torch.int8) and tuple(a_codes.shape) == (M, code_bytes(K, bits))
+             and a_codes.is_contiguous(), "a_codes: canonical contiguous [M, K*bits/8] bytes")
+    _check_out(out, M, N)
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=a_codes.device)
     acc = torch.empty((M, N), dtype=torch.int32, device=a_codes.device) if want_acc else None
     if ws is None:
@@ -189,6 +211,7 @@ def linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: in
     """Fused projection: bf16 x [M, K] -> bf16 y [M, N]."""
     M, K = x.shape
     assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
+    _check_out(out, M, N)
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
     if ws is None:
         ws = workspace(linear_workspace_bytes(M, N, K, bits), x.device)
@@ -260,16 +283,15 @@ def gptq_factor(G: torch.Tensor, damp: float = 0.01) -> torch.Tensor:
     return U
 
 
-def gptq_sweep(w_t: torch.Tensor, U: torch.Tensor, bits: int,
-               scale_mult: float = 1.0) -> Tuple[torch.Tensor, torch.Tensor]:
-    """GPTQ column sweep on transformed weight rows w_t fp32 [N, K] -> (codes int8 [N, K],
-    scales fp32 [N])."""
+def gptq_sweep(w_t: torch.Tensor, U: torch.Tensor, b: int, bits: int) -> Tuple[torch.Tensor, torch.Tensor]:
+    """GPTQ column sweep on weight rows w_t fp32 [N, K] transformed with block size b ->
+    (codes int8 [N, K], scales fp32 [N])."""
     N, K = w_t.shape
     assert w_t.dtype == torch.float32 and w_t.stride(1) == 1 and U.dtype == torch.float64 and U.is_contiguous()
     codes = torch.empty((N, K), dtype=torch.int8, device=w_t.device)
     scales = torch.empty((N,), dtype=torch.float32, device=w_t.device)
     ws = workspace(int(LIB.fq_gptq_sweep_workspace_bytes(N, K)), w_t.device)
-    _check(LIB.fq_gptq_sweep(_p(w_t), w_t.stride(0), _p(U), N, K, bits, scale_mult, _p(codes), _p(scales), _p(ws),
+    _check(LIB.fq_gptq_sweep(_p(w_t), w_t.stride(0), _p(U), N, K, b, bits, _p(codes), _p(scales), _p(ws),
                              ws.numel(), _stream()))
     return codes, scales
 
@@ -284,8 +306,7 @@ def gptq_quantize_weights(w: torch.Tensor, calib: torch.Tensor, b: int, bits: in
     z = transform(calib, b, smooth_inv, post_inv)
     U = gptq_factor(gptq_hessian(z), damp)
     w_t = transform(w, b, col_scale, post_scale)
-    c_b = float(torch.tensor(1.0 / b ** 0.5, dtype=torch.float32).item())
-    return gptq_sweep(w_t, U, bits, c_b)
+    return gptq_sweep(w_t, U, b, bits)
 
 
 def w4a16_workspace_bytes(M: int, N: int, K: int) -> int:
@@ -299,6 +320,7 @@ def gemm_w4a16(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N
     (and the fp32 sums if want_acc)."""
     M, K = x.shape
     assert x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1)
+    _check_out(out, M, N)
     y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
     acc = torch.empty((M, N), dtype=torch.float32, device=x.device) if want_acc else None
     if ws is None:

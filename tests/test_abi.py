@@ -33,8 +33,8 @@ def test_library_exports_symbol(name):
 
 
 def test_status_strings():
-    for s in range(7):
-        assert fq.LIB.fq_status_string(s)
+    for s in range(8):
+        assert fq.LIB.fq_status_string(s) not in (None, b"", b"unknown status")
     assert fq.LIB.fq_status_string(99) == b"unknown status"
 
 
@@ -207,12 +207,13 @@ def test_rotate_quant_workspace_and_empty():
     (lambda: fq.LIB.fq_gptq_factor(FAKE, 1024, 2.0, FAKE, FAKE, 1 << 40, None), 3),
     (lambda: fq.LIB.fq_gptq_factor(FAKE, 1024, 0.01, FAKE, FAKE, 8, None), 5),
     (lambda: fq.LIB.fq_gptq_factor(FAKE, 1024, 0.01, MISALIGNED, FAKE, 1 << 40, None), 4),
-    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 3, 1.0, FAKE, FAKE, FAKE, 1 << 40, None), 3),
-    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1000, FAKE, 16, 1024, 4, 1.0, FAKE, FAKE, FAKE, 1 << 40, None), 2),
-    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, NULL, 16, 1024, 4, 1.0, FAKE, FAKE, FAKE, 1 << 40, None), 1),
-    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 4, 0.0, FAKE, FAKE, FAKE, 1 << 40, None), 3),
-    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 4, 1.0, FAKE, FAKE, FAKE, 64, None), 5),
-    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 0, 1024, 4, 1.0, NULL, NULL, NULL, 0, None), 0),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 128, 3, FAKE, FAKE, FAKE, 1 << 40, None), 3),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1000, FAKE, 16, 1024, 128, 4, FAKE, FAKE, FAKE, 1 << 40, None), 2),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, NULL, 16, 1024, 128, 4, FAKE, FAKE, FAKE, 1 << 40, None), 1),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 48, 4, FAKE, FAKE, FAKE, 1 << 40, None), 3),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 512, 4, FAKE, FAKE, FAKE, 1 << 40, None), 3),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 16, 1024, 128, 4, FAKE, FAKE, FAKE, 64, None), 5),
+    (lambda: fq.LIB.fq_gptq_sweep(FAKE, 1024, FAKE, 0, 1024, 128, 4, NULL, NULL, NULL, 0, None), 0),
 ])
 def test_gptq_rejects(call, status):
     assert call() == status
@@ -223,3 +224,84 @@ def test_gptq_workspace_sizes():
     assert fq.LIB.fq_gptq_factor_workspace_bytes(32768) == 0
     assert fq.LIB.fq_gptq_sweep_workspace_bytes(64, 1024) >= 64 * 1024 * 8
     assert fq.LIB.fq_gptq_sweep_workspace_bytes(0, 1024) == 0
+
+
+# ---- K outside whole 128-channel steps (the weight tiles' width) is rejected everywhere ----
+
+@pytest.mark.parametrize("K", [32, 96, 160, 1024 + 32])
+def test_k_not_whole_steps_rejected(K):
+    b = 32
+    assert call_quant(K=K, ldx=max(K, 1024), b=b) == 3
+    for bits in (4, 8):
+        assert call_gemm(bits=bits, K=K) == 3
+    assert call_linear(K=K, ldx=max(K, 1024), b=b) == 3
+    assert fq.LIB.fq_pack_weights(FAKE, 32, K, 4, FAKE, None) == 3
+    assert call_w4a16(K=K, ldx=max(K, 1024)) == 3
+    assert "multiple of 128" in fq.LIB.fq_last_error().decode() or "outside" in fq.LIB.fq_last_error().decode()
+
+
+# ---- outputs may not overlap inputs or each other (FQ_ERR_ALIAS = 7) ----
+
+BASE = 1 << 24  # fake, never dereferenced addresses: these calls fail validation
+
+
+def _ptr(off):
+    return ctypes.c_void_p(BASE + off)
+
+
+def test_fwht_quant_alias_rejected():
+    # x rows [BASE, BASE + 4 * 2048); codes inside them
+    assert call_quant(x=_ptr(0), codes=_ptr(1024), delta=_ptr(1 << 20)) == 7
+    assert call_quant(x=_ptr(0), codes=_ptr(1 << 20), delta=_ptr((1 << 20) + 256)) == 7   # codes and delta
+    assert call_quant(x=_ptr(0), codes=_ptr(1 << 20), delta=_ptr(2 << 20), smooth=_ptr((2 << 20) - 16)) == 7
+
+
+def test_gemm_alias_rejected():
+    # y overlaps the codes; acc overlaps y; the workspace overlaps the weights
+    assert call_gemm(a=_ptr(0), y=_ptr(256), delta=_ptr(1 << 20), w=_ptr(2 << 20), sw=_ptr(3 << 20)) == 7
+    assert call_gemm(a=_ptr(0), y=_ptr(1 << 20), acc=_ptr((1 << 20) + 4096), delta=_ptr(2 << 20),
+                     w=_ptr(3 << 20), sw=_ptr(4 << 20)) == 7
+    assert call_gemm(M=50, N=2048, ldy=2048, K=32768, a=_ptr(0), y=_ptr(4 << 20), delta=_ptr(5 << 20),
+                     w=_ptr(8 << 20), sw=_ptr(6 << 20), ws=_ptr(9 << 20)) == 7
+
+
+def test_linear_alias_rejected():
+    # the workspace overlaps y; y overlaps x
+    assert call_linear(x=_ptr(0), y=_ptr(1 << 20), ws=_ptr((1 << 20) + 4096), w=_ptr(2 << 20),
+                       sw=_ptr(3 << 20)) == 7
+    assert call_linear(x=_ptr(0), y=_ptr(2048), ws=_ptr(4 << 20), w=_ptr(2 << 20), sw=_ptr(3 << 20)) == 7
+
+
+def test_gptq_and_transform_alias_rejected():
+    assert fq.LIB.fq_transform(_ptr(0), 1, 1024, NULL, NULL, 4, 1024, 64, _ptr(4096), None) == 7
+    assert fq.LIB.fq_gptq_hessian(_ptr(0), 1024, 8, 1024, _ptr(1024), 0, None) == 7
+
+
+# ---- no development override is read by the shipped library ----
+
+def test_library_reads_no_tuning_environment():
+    with open(fq.LIB_PATH, "rb") as f:
+        blob = f.read()
+    assert b"FQ_TUNE" not in blob
+    assert b"getenv" not in blob
+
+
+# ---- the binding checks caller-supplied outputs before calling the library ----
+
+def test_binding_rejects_mismatched_outputs():
+    import torch
+    codes = torch.zeros((4, 512), dtype=torch.uint8)
+    delta = torch.zeros((4,), dtype=torch.float32)
+    w = torch.zeros((16 * 512,), dtype=torch.uint8)
+    sw = torch.zeros((16,), dtype=torch.float32)
+    for bad in (torch.empty((4, 16), dtype=torch.float32), torch.empty((4, 32), dtype=torch.bfloat16),
+                torch.empty((16, 4), dtype=torch.bfloat16).t()):
+        with pytest.raises(ValueError):
+            fq.gemm(codes, delta, w, sw, 16, 1024, 4, out=bad)
+    with pytest.raises(ValueError):
+        fq.gemm(torch.zeros((4, 1024), dtype=torch.uint8), delta, w, sw, 16, 1024, 4)  # int8-wide codes for W4A4
+    x = torch.zeros((4, 1024), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        fq.linear(x, w, sw, 16, 64, 4, out=torch.empty((4, 16), dtype=torch.float16))
+    with pytest.raises(ValueError):
+        fq.fwht_quant(x, 64, 4, out_codes=torch.empty((4, 1024), dtype=torch.uint8))

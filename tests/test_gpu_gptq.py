@@ -109,7 +109,7 @@ def test_sweep_bit_exact_given_the_factor(N, K, bits):
     w_t = oracle.transform(w, b)
     U = oracle.gptq_factor(oracle.gptq_hessian(_calib(2 * K, K, b, seed=K + 1)), 0.01)
     cb = float(oracle.inv_sqrt_b(b))
-    codes, scales = f.gptq_sweep(_dev(w_t), _dev(U), bits, cb)
+    codes, scales = f.gptq_sweep(_dev(w_t), _dev(U), b, bits)
     torch.cuda.synchronize()
     c_ref, s_ref = oracle.gptq_sweep(w_t, U, bits, 128, cb)
     np.testing.assert_array_equal(scales.cpu().numpy(), s_ref)

@@ -349,6 +349,47 @@ def test_dequant_matches_eq8_and_zero_token_gives_bias():
     np.testing.assert_array_equal(y[3], bias.astype(np.float64))
 
 
+def test_dequant_one_hot_is_eq8_exactly():
+    """Eq. (8) pinned on one-hot codes: the only nonzero accumulator of each row is
+    q^W q^A at a known (t, j), so y = s_j delta_t q^W q^A + b_j there and y = b_j elsewhere.
+    Scales and biases are distinct per row and per channel, so a swapped index, a dropped
+    factor or a dropped bias changes the result; with power-of-two scales every product is
+    exact in double and the comparison is exact; with general scales it is checked against
+    exact rational arithmetic to within two roundings."""
+    from fractions import Fraction
+    M, N, K = 3, 5, 128
+    hits = [(0, 2, 17, 5, -7), (1, 4, 90, -3, 6), (2, 0, 127, 7, 7)]  # (t, j, c, qA, qW)
+    qa = np.zeros((M, K), np.int8)
+    qw = np.zeros((N, K), np.int8)
+    for t, j, c, a, w in hits:
+        qa[t, c] = a
+        qw[j, c] = w
+    acc = oracle.gemm(qa, qw)
+    for scales in ("pow2", "general"):
+        if scales == "pow2":
+            delta = np.array([2.0 ** -3, 2.0 ** -9, 2.0 ** 4], np.float32)
+            s_w = np.array([2.0 ** -1, 2.0 ** -6, 2.0 ** 2, 2.0 ** -11, 2.0 ** 5], np.float32)
+            bias = np.array([0.5, -0.25, 3.0, -8.0, 0.125], np.float32)
+        else:
+            delta = synth.random_scales(M, seed=85)
+            s_w = synth.random_scales(N, seed=86)
+            bias = synth.random_scales(N, seed=87, low=-1, high=1)
+        y = oracle.dequant(acc, delta, s_w, bias)
+        for t in range(M):
+            for j in range(N):
+                a = sum(int(qa[t, c]) * int(qw[j, c]) for c in range(K))
+                exact = Fraction(float(s_w[j])) * Fraction(float(delta[t])) * a + Fraction(float(bias[j]))
+                if scales == "pow2":
+                    assert y[t, j] == float(exact), (t, j)
+                else:
+                    assert abs(Fraction(y[t, j]) - exact) <= 2 * abs(exact) * Fraction(1, 2 ** 52) + Fraction(1, 2 ** 1074)
+        hit = {(t, j) for t, j, *_ in hits}
+        for t in range(M):
+            for j in range(N):
+                if (t, j) not in hit:
+                    assert y[t, j] == float(bias[j])
+
+
 def test_pack_int4_canonical_nibbles():
     codes = np.array([[1, -1, -7, 7, 0, -8 + 1, 3, -2]], dtype=np.int8)
     packed = oracle.pack_int4(codes)
