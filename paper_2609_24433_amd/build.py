@@ -20,7 +20,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfq.so")
-SOURCES = ["fq_api.cpp", "fq_quant.hip", "fq_rotate.hip", "fq_gemm.hip", "fq_gptq.hip"]
+SOURCES = ["fq_api.cpp", "fq_quant.hip", "fq_rotate.hip", "fq_gemm.hip", "fq_gptq.hip", "fq_small.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [
@@ -30,7 +30,7 @@ COMMON_FLAGS = [
 ]
 
 
-EXTRA_FLAGS = {"fq_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+EXTRA_FLAGS = {"fq_gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"], "fq_small.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def _hipcc() -> str:

@@ -196,11 +196,19 @@ fq_status gemm_entry(int bits, const void *a_codes, const float *delta, const vo
                      bits, ws, ws_bytes, static_cast<hipStream_t>(stream));
 }
 
-// fq_linear workspace: [codes (nibbles for W4A4, int8 for W8A8)][delta][split-K partials]
+// fq_linear workspace: none when one fused kernel runs the projection (few tokens, K up
+// to 4096); otherwise [codes (nibbles for W4A4, int8 for W8A8)][delta][split-K partials]
 size_t linear_ws_bytes(int64_t M, int64_t N, int64_t K, int bits) {
   if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
+  if (fq::plan_small(M, N, K, bits).ok) return 0;
   return align256((size_t)M * (size_t)K * (size_t)bits / 8) + align256((size_t)M * 4) +
          fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
+}
+
+int log2_pow2(int b) {
+  int k = 0;
+  while ((1 << k) < b) ++k;
+  return k;
 }
 
 // The fused projection: both stages are validated, and the GEMM's kernel is resolved,
@@ -219,19 +227,42 @@ fq_status linear_common(const void *x_bf16, int64_t ldx, const float *smooth_inv
   const size_t codes_bytes = align256((size_t)M * (size_t)K * (size_t)bits / 8);
   const size_t delta_bytes = align256((size_t)M * 4);
   const size_t need = linear_ws_bytes(M, N, K, bits);
-  if (!ws || ws_bytes < need)
+  if (need > 0 && (!ws || ws_bytes < need))
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
-  if (!aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
-  if (outputs_alias({span(y_bf16, rows_span(M, ldy * 2, N * 2)), span(ws, need)},
+  if (need > 0 && !aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  if (outputs_alias({span(y_bf16, rows_span(M, ldy * 2, N * 2)), span(need ? ws : nullptr, need)},
                     {span(x_bf16, rows_span(M, ldx * 2, K * 2)), span(smooth_inv, smooth_inv ? (size_t)K * 4 : 0),
                      span(post_inv, post_inv ? (size_t)K * 4 : 0), span(w_packed, fq_packed_weight_bytes(N, K, bits)),
                      span(w_scale, (size_t)N * 4), span(bias, bias ? (size_t)N * 4 : 0)}))
     return fail(FQ_ERR_ALIAS, "y and the workspace must not overlap each other or an input");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const fq::SmallPlan sp = fq::plan_small(M, N, K, bits);
+  if (sp.ok) {
+    fq::SmallArgs a;
+    a.x = x_bf16;
+    a.ldx = ldx;
+    a.chan_mult = smooth_inv;
+    a.post_mult = post_inv;
+    a.w = static_cast<const uint8_t *>(w_packed);
+    a.w_scale = w_scale;
+    a.bias = bias;
+    a.y = static_cast<uint16_t *>(y_bf16);
+    a.ldy = ldy;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.log2b = log2_pow2(b);
+    a.bits = bits;
+    a.clip_ratio = clip_ratio;
+    a.cb = inv_sqrt_pow2(b);
+    hipError_t e = fq::launch_linear_small(a, sp, st);
+    if (e != hipSuccess) return hip_fail(e, "fused projection launch");
+    return ok();
+  }
   uint8_t *codes = static_cast<uint8_t *>(ws);
   float *delta = reinterpret_cast<float *>(codes + codes_bytes);
   void *gws = codes + codes_bytes + delta_bytes;
   const size_t gws_bytes = ws_bytes - codes_bytes - delta_bytes;
-  hipStream_t st = static_cast<hipStream_t>(stream);
   // W4A4 codes between the two kernels are canonical nibbles (half the bytes of int8, the
   // same per-step cost in the GEMMs, which widen them in registers); W8A8 codes are int8.
   const bool nibble = bits == 4;

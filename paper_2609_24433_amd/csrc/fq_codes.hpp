@@ -18,47 +18,155 @@ __device__ __forceinline__ int quantize_bits(float u, float inv, float lim) {
   return __float_as_int(t + 12582912.0f);
 }
 
-// Pack 16 quantized bit patterns (natural channel order; low byte = code) and store them.
+// Pack 16 quantized bit patterns (natural channel order; low byte = code) into canonical
+// nibbles (8 bytes: channel 2i in the low nibble of byte i) or int8 (16 bytes).
+__device__ __forceinline__ uint2 pack_chunk_nibbles(const int (&c)[16]) {
+  uint32_t w[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t b[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) b[i] = ((uint32_t)c[8 * h + 2 * i] & 0xFu) | ((uint32_t)c[8 * h + 2 * i + 1] << 4);
+    // low bytes of b[0..3] -> one word
+    const uint32_t lo = __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u);
+    const uint32_t hi = __builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu);
+    w[h] = lo | hi;
+  }
+  return make_uint2(w[0], w[1]);
+}
+
+__device__ __forceinline__ uint4 pack_chunk_int8(const int (&c)[16]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t lo = __builtin_amdgcn_perm((uint32_t)c[4 * i + 1], (uint32_t)c[4 * i], 0x0c0c0400u);
+    const uint32_t hi = __builtin_amdgcn_perm((uint32_t)c[4 * i + 3], (uint32_t)c[4 * i + 2], 0x04000c0cu);
+    w[i] = lo | hi;
+  }
+  return make_uint4(w[0], w[1], w[2], w[3]);
+}
+
+// Pack chunk `chunk` of a row and store it at its canonical place in row_out.
 __device__ __forceinline__ void store_chunk_bits(uint8_t *row_out, int chunk, const int (&c)[16],
                                                  int out_fmt) {
-  if (out_fmt == kOutNibble) {
-    uint32_t w[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      uint32_t b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        b[i] = ((uint32_t)c[8 * h + 2 * i] & 0xFu) | ((uint32_t)c[8 * h + 2 * i + 1] << 4);
-      // low bytes of b[0..3] -> one word
-      const uint32_t lo = __builtin_amdgcn_perm(b[1], b[0], 0x0c0c0400u);
-      const uint32_t hi = __builtin_amdgcn_perm(b[3], b[2], 0x04000c0cu);
-      w[h] = lo | hi;
-    }
-    *reinterpret_cast<uint2 *>(row_out + (int64_t)chunk * 8) = make_uint2(w[0], w[1]);
-  } else {
-    uint32_t w[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t lo = __builtin_amdgcn_perm((uint32_t)c[4 * i + 1], (uint32_t)c[4 * i], 0x0c0c0400u);
-      const uint32_t hi = __builtin_amdgcn_perm((uint32_t)c[4 * i + 3], (uint32_t)c[4 * i + 2], 0x04000c0cu);
-      w[i] = lo | hi;
-    }
-    *reinterpret_cast<uint4 *>(row_out + (int64_t)chunk * 16) = make_uint4(w[0], w[1], w[2], w[3]);
-  }
+  if (out_fmt == kOutNibble)
+    *reinterpret_cast<uint2 *>(row_out + (int64_t)chunk * 8) = pack_chunk_nibbles(c);
+  else
+    *reinterpret_cast<uint4 *>(row_out + (int64_t)chunk * 16) = pack_chunk_int8(c);
 }
 
 // Value of lane (l ^ M) of the wave, for M < 32: DPP quad permutations for 1 and 2, a
 // 16-lane row rotation by 8 for 8, the LDS crossbar's bit-mask swizzle (no memory) for 4
-// and 16.  Pure data movement: the butterfly sums stay bit-exact.
+// and 16.  Every lane's source is valid, so the DPP moves need no old value.  Pure data
+// movement: the butterfly sums stay bit-exact.
 template <int M>
 __device__ __forceinline__ float lane_xor(float v) {
   const int x = __float_as_int(v);
   int r;
-  if constexpr (M == 1) r = __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);       // quad_perm 1,0,3,2
-  else if constexpr (M == 2) r = __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);  // quad_perm 2,3,0,1
-  else if constexpr (M == 8) r = __builtin_amdgcn_update_dpp(0, x, 0x128, 0xF, 0xF, false); // row_ror:8
-  else r = __builtin_amdgcn_ds_swizzle(x, (M << 10) | 0x1F);                                // xor M in 32 lanes
+  if constexpr (M == 1) r = __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false);       // quad_perm 1,0,3,2
+  else if constexpr (M == 2) r = __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false);  // quad_perm 2,3,0,1
+  else if constexpr (M == 8) r = __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false); // row_ror:8
+  else r = __builtin_amdgcn_ds_swizzle(x, (M << 10) | 0x1F);                          // xor M in 32 lanes
   return __int_as_float(r);
+}
+
+// ---- the prologue's per-chunk arithmetic (one 16-channel chunk per register array) ----
+
+// Raw 16-channel chunk as loaded: bf16 = 2 x 16 bytes, fp32 = 4 x 16 bytes.
+template <typename Tin>
+struct Chunk {
+  static constexpr int U4 = sizeof(Tin) == 2 ? 2 : 4;
+  uint4 u[U4];
+};
+
+template <typename Tin>
+__device__ __forceinline__ void load_chunk(const void *base, int64_t off, Chunk<Tin> &c) {
+  const uint4 *p = reinterpret_cast<const uint4 *>(reinterpret_cast<const Tin *>(base) + off);
+#pragma unroll
+  for (int i = 0; i < Chunk<Tin>::U4; ++i) c.u[i] = p[i];
+}
+
+template <typename Tin>
+__device__ __forceinline__ void unpack_chunk(const Chunk<Tin> &c, float (&v)[16]) {
+  if constexpr (sizeof(Tin) == 2) {
+    const uint32_t w[8] = {c.u[0].x, c.u[0].y, c.u[0].z, c.u[0].w, c.u[1].x, c.u[1].y, c.u[1].z, c.u[1].w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      v[2 * i] = bf16_lo(w[i]);
+      v[2 * i + 1] = bf16_hi(w[i]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[4 * i] = __uint_as_float(c.u[i].x);
+      v[4 * i + 1] = __uint_as_float(c.u[i].y);
+      v[4 * i + 2] = __uint_as_float(c.u[i].z);
+      v[4 * i + 3] = __uint_as_float(c.u[i].w);
+    }
+  }
+}
+
+// v *= m elementwise (one fp32 rounding per element): the fold multipliers.
+__device__ __forceinline__ void mul_chunk(float (&v)[16], const float4 (&m)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[4 * i] = v[4 * i] * m[i].x;
+    v[4 * i + 1] = v[4 * i + 1] * m[i].y;
+    v[4 * i + 2] = v[4 * i + 2] * m[i].z;
+    v[4 * i + 3] = v[4 * i + 3] * m[i].w;
+  }
+}
+
+// One butterfly stage of span H inside a chunk of CW registers: (a, c) -> (a + c, a - c).
+template <int H, int CW = 16>
+__device__ __forceinline__ void chunk_stage(float (&v)[CW]) {
+#pragma unroll
+  for (int i = 0; i < CW; i += 2 * H) {
+#pragma unroll
+    for (int j = i; j < i + H; ++j) {
+      float a = v[j], c = v[j + H];
+      v[j] = a + c;
+      v[j + H] = a - c;
+    }
+  }
+}
+
+// Butterfly stage h = CW M across lanes: chunk j pairs with chunk j ^ M, held by lane ^ M.
+// The lower chunk keeps a + c, the upper one a - c, as fma(+-1, own, partner): one
+// rounding of the exact sum or difference, the same as the add or subtract.
+template <int M, int CPT, int CW = 16>
+__device__ __forceinline__ void lane_stage(float (&v)[CPT][CW], int tau) {
+  const float sgn = (tau & M) ? -1.0f : 1.0f;
+#pragma unroll
+  for (int c = 0; c < CPT; ++c)
+#pragma unroll
+    for (int i = 0; i < CW; ++i) v[c][i] = __builtin_fmaf(sgn, v[c][i], lane_xor<M>(v[c][i]));
+}
+
+// The blockwise unnormalized Sylvester transform of a row held as CW-channel chunks
+// c * TPR + tau by consecutive lanes: stages h = 1 .. b/2 in ascending order, h < CW
+// inside each chunk and h >= CW across lanes (a b-block is b/CW consecutive chunks in
+// consecutive lanes of one wave).  b = 2^log2b is uniform across the wave, so the stage
+// branches are too.  The result does not depend on CW: every stage is the same pair
+// update in the same order.
+template <int CPT, int CW = 16>
+__device__ __forceinline__ void row_transform(float (&v)[CPT][CW], int log2b, int tau) {
+  static_assert(CW == 8 || CW == 16, "chunk width");
+  constexpr int L = CW == 16 ? 4 : 3;  // stages inside a chunk
+#pragma unroll
+  for (int c = 0; c < CPT; ++c) {
+    if (log2b > 0) chunk_stage<1, CW>(v[c]);
+    if (log2b > 1) chunk_stage<2, CW>(v[c]);
+    if (log2b > 2) chunk_stage<4, CW>(v[c]);
+    if constexpr (CW == 16)
+      if (log2b > 3) chunk_stage<8, CW>(v[c]);
+  }
+  if (log2b > L) lane_stage<1, CPT, CW>(v, tau);
+  if (log2b > L + 1) lane_stage<2, CPT, CW>(v, tau);
+  if (log2b > L + 2) lane_stage<4, CPT, CW>(v, tau);
+  if (log2b > L + 3) lane_stage<8, CPT, CW>(v, tau);
+  if constexpr (CW == 8)
+    if (log2b > L + 4) lane_stage<16, CPT, CW>(v, tau);
 }
 
 }  // namespace fq

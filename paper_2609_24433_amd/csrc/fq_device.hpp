@@ -57,4 +57,72 @@ __device__ __forceinline__ v4i mfma16x16x64(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
 }
 
+__device__ __forceinline__ void lds_fence() { asm volatile("" ::: "memory"); }
+
+// Instruction-scheduling wall: the compiler moves nothing across it.
+__device__ __forceinline__ void sched_wall() { __builtin_amdgcn_sched_barrier(0); }
+
+// Workgroup barrier that waits only for this wave's LDS accesses.  __syncthreads() also
+// waits for every outstanding global load (vmcnt(0)), which would drain a prefetch ring.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  lds_fence();
+}
+
+// 16 bytes per lane from global memory straight into LDS; a wave fills the contiguous
+// KB at `lds_dst` (lane l -> lds_dst + 16 l).  The builtin exists only for the device
+// pass, so the host pass (which only needs the kernel stub) sees an empty body.
+__device__ __forceinline__ void load_to_lds16(const void *src, void *lds_dst) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
+#else
+  (void)src;
+  (void)lds_dst;
+#endif
+}
+
+// 16-byte LDS read the compiler does not track.  The compiler cannot tell LDS locations
+// written by direct-to-LDS loads from the ones read here, so it would hold an ordinary
+// LDS read until every such load in flight has landed; a kernel that reads one region
+// while another region is still being filled issues its own waits instead: a
+// wait_vmcnt for the loads that fill the region (and a barrier), and lgkm_wait_all()
+// before the result is used.
+__device__ __forceinline__ uint4 lds_read16_untracked(const void *p) {
+  uint4 v;
+  const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  return v;
+}
+__device__ __forceinline__ float lds_read4_untracked(const void *p) {
+  float v;
+  const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+  asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(a) : "memory");
+  return v;
+}
+__device__ __forceinline__ void lgkm_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// LDS writes the compiler does not track (same reason); an lds_barrier() orders them.
+__device__ __forceinline__ void lds_write4_untracked(void *p, float v) {
+  const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+  asm volatile("ds_write_b32 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+__device__ __forceinline__ void lds_write8_untracked(void *p, uint2 v) {
+  const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+  const v2i w{(int)v.x, (int)v.y};
+  asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(w) : "memory");
+}
+__device__ __forceinline__ void lds_write16_untracked(void *p, uint4 v) {
+  const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));
+  const v4i w{(int)v.x, (int)v.y, (int)v.z, (int)v.w};
+  asm volatile("ds_write_b128 %0, %1" ::"v"(a), "v"(w) : "memory");
+}
+
+// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+
 }  // namespace fq

@@ -182,18 +182,6 @@ __device__ __forceinline__ v4i w_operand(const uint8_t *tile, int l, int c) {
   }
 }
 
-__device__ __forceinline__ void lds_fence() { asm volatile("" ::: "memory"); }
-
-// Instruction-scheduling wall: the compiler moves nothing across it.
-__device__ __forceinline__ void sched_wall() { __builtin_amdgcn_sched_barrier(0); }
-
-// Workgroup barrier that waits only for this wave's LDS accesses.  __syncthreads() also
-// waits for every outstanding global load (vmcnt(0)), which would drain a prefetch ring.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0)
-  __builtin_amdgcn_s_barrier();
-  lds_fence();
-}
 
 // ---------------- output stage ----------------
 //
@@ -323,25 +311,6 @@ __global__ __launch_bounds__(256) void splitk_epilogue_kernel(GemmParams p, int 
   const uint32_t o0 = f32_to_bf16(rescale(a[0], sw.x, dt, bj.x)) | (f32_to_bf16(rescale(a[1], sw.y, dt, bj.y)) << 16);
   const uint32_t o1 = f32_to_bf16(rescale(a[2], sw.z, dt, bj.z)) | (f32_to_bf16(rescale(a[3], sw.w, dt, bj.w)) << 16);
   *reinterpret_cast<uint2 *>(p.y + (int64_t)m * p.ldy + n) = make_uint2(o0, o1);
-}
-
-// 16 bytes per lane from global memory straight into LDS; a wave fills the contiguous
-// KB at `lds_dst` (lane l -> lds_dst + 16 l).  The builtin exists only for the device
-// pass, so the host pass (which only needs the kernel stub) sees an empty body.
-__device__ __forceinline__ void load_to_lds16(const void *src, void *lds_dst) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, lds_dst, 16, 0, 0);
-#else
-  (void)src;
-  (void)lds_dst;
-#endif
-}
-
-// s_waitcnt vmcnt(n) leaving the other counters alone (gfx9 encoding)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
 // Waits until at most `later` ring stages of LPS loads each are still in flight.

@@ -93,6 +93,29 @@ struct GemmArgs {
 // limit, returning an error when the plan has no kernel.
 hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s, bool go = true);
 
+// The fused projection for few tokens (fq_small.hip): one kernel per call, each workgroup
+// quantizing its own r rows and multiplying them against 64 ncw output channels.
+struct SmallPlan {
+  bool ok;          // false: the shape is outside what the fused kernel handles
+  int r, cpt, ncw;  // rows per workgroup, 16-channel chunks per prologue thread, 64-channel groups per workgroup / 64
+  int rb, groups;   // grid: output-channel groups x row blocks
+};
+struct SmallArgs {
+  const void *x;  // bf16 [M, ldx]
+  int64_t ldx;
+  const float *chan_mult, *post_mult;
+  const uint8_t *w;
+  const float *w_scale, *bias;
+  uint16_t *y;
+  int64_t ldy;
+  int64_t M, N, K;
+  int log2b, bits;
+  float clip_ratio, cb;
+};
+SmallPlan plan_small(int64_t M, int64_t N, int64_t K, int bits);
+// go = false resolves the kernel and raises its LDS limit without launching.
+hipError_t launch_linear_small(const SmallArgs &a, const SmallPlan &pl, hipStream_t s, bool go = true);
+
 // Weight-only INT4 (bf16 activations) projection.
 struct W16Plan {
   int mt, kt;           // 16-row tiles per workgroup, k steps per wave group (4 groups)

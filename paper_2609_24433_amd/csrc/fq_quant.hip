@@ -37,40 +37,6 @@ struct QuantParams {
   int tpr_log2;
 };
 
-// Raw 16-channel chunk as loaded: bf16 = 2 x 16 bytes, fp32 = 4 x 16 bytes.
-template <typename Tin>
-struct Chunk {
-  static constexpr int U4 = sizeof(Tin) == 2 ? 2 : 4;
-  uint4 u[U4];
-};
-
-template <typename Tin>
-__device__ __forceinline__ void load_chunk(const void *base, int64_t off, Chunk<Tin> &c) {
-  const uint4 *p = reinterpret_cast<const uint4 *>(reinterpret_cast<const Tin *>(base) + off);
-#pragma unroll
-  for (int i = 0; i < Chunk<Tin>::U4; ++i) c.u[i] = p[i];
-}
-
-template <typename Tin>
-__device__ __forceinline__ void unpack_chunk(const Chunk<Tin> &c, float (&v)[16]) {
-  if constexpr (sizeof(Tin) == 2) {
-    const uint32_t w[8] = {c.u[0].x, c.u[0].y, c.u[0].z, c.u[0].w, c.u[1].x, c.u[1].y, c.u[1].z, c.u[1].w};
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      v[2 * i] = bf16_lo(w[i]);
-      v[2 * i + 1] = bf16_hi(w[i]);
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[4 * i] = __uint_as_float(c.u[i].x);
-      v[4 * i + 1] = __uint_as_float(c.u[i].y);
-      v[4 * i + 2] = __uint_as_float(c.u[i].z);
-      v[4 * i + 3] = __uint_as_float(c.u[i].w);
-    }
-  }
-}
-
 // In-place butterfly over n consecutive register values, stages h = 1 .. hmax/2.
 template <int N, int HMAX>
 __device__ __forceinline__ void butterfly(float (&v)[N]) {
@@ -86,18 +52,6 @@ __device__ __forceinline__ void butterfly(float (&v)[N]) {
       }
     }
   }
-}
-
-// Butterfly stage h = 16 M across lanes: chunk j pairs with chunk j ^ M, held by lane ^ M.
-// The lower chunk keeps a + c, the upper one a - c, as fma(+-1, own, partner): one
-// rounding of the exact sum or difference, the same as the add or subtract.
-template <int M, int CPT>
-__device__ __forceinline__ void lane_stage(float (&v)[CPT][16], int tau) {
-  const float sgn = (tau & M) ? -1.0f : 1.0f;
-#pragma unroll
-  for (int c = 0; c < CPT; ++c)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) v[c][i] = __builtin_fmaf(sgn, v[c][i], lane_xor<M>(v[c][i]));
 }
 
 // NT threads per workgroup; a row is handled by TPR = 2^tpr_log2 consecutive threads,

@@ -113,10 +113,14 @@ def call_linear(x=FAKE, ldx=1024, M=50, K=1024, N=256, b=64, bits=4, r=1.0, w=FA
 @pytest.mark.parametrize("kw,status", [
     (dict(x=NULL), 1), (dict(w=NULL), 1), (dict(y=NULL), 1), (dict(sw=NULL), 1),
     (dict(ldx=512), 2), (dict(ldy=100), 2), (dict(b=5), 3), (dict(bits=6), 3), (dict(N=40, ldy=40), 3),
-    (dict(r=-1.0), 3), (dict(ws=NULL, ws_bytes=0), 5), (dict(ws_bytes=100), 5), (dict(ws=MISALIGNED), 4),
-    (dict(smooth=MISALIGNED), 4), (dict(post=MISALIGNED), 4),
+    (dict(r=-1.0), 3), (dict(smooth=MISALIGNED), 4), (dict(post=MISALIGNED), 4),
+    # shapes that need a workspace (too long for the one-kernel path)
+    (dict(ws=NULL, ws_bytes=0, K=16384, ldx=16384), 5), (dict(ws_bytes=100, K=16384, ldx=16384), 5),
+    (dict(ws=MISALIGNED, K=16384, ldx=16384), 4),
 ])
 def test_linear_rejects(kw, status):
+    if status in (4, 5) and "ws" in kw or "ws_bytes" in kw:
+        assert fq.linear_workspace_bytes(kw.get("M", 50), kw.get("N", 256), kw["K"], kw.get("bits", 4)) > 100
     assert call_linear(**kw) == status
 
 
@@ -266,10 +270,13 @@ def test_gemm_alias_rejected():
 
 
 def test_linear_alias_rejected():
-    # the workspace overlaps y; y overlaps x
-    assert call_linear(x=_ptr(0), y=_ptr(1 << 20), ws=_ptr((1 << 20) + 4096), w=_ptr(2 << 20),
-                       sw=_ptr(3 << 20)) == 7
+    # the workspace overlaps y (a shape that needs one); y overlaps x
+    assert fq.linear_workspace_bytes(50, 256, 16384, 4) > 0
+    assert call_linear(K=16384, ldx=16384, x=_ptr(0), y=_ptr(4 << 20), ws=_ptr((4 << 20) + 4096),
+                       w=_ptr(8 << 20), sw=_ptr(3 << 20)) == 7
     assert call_linear(x=_ptr(0), y=_ptr(2048), ws=_ptr(4 << 20), w=_ptr(2 << 20), sw=_ptr(3 << 20)) == 7
+    assert call_linear(x=_ptr(0), y=_ptr(1 << 20), ws=NULL, ws_bytes=0, w=_ptr((1 << 20) + 64),
+                       sw=_ptr(3 << 20)) == 7  # y overlaps the weights
 
 
 def test_gptq_and_transform_alias_rejected():
