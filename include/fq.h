@@ -191,6 +191,22 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, co
                     const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,
                     int64_t ldy, void *ws, size_t ws_bytes, void *stream);
 
+/* fq_linear for callers that cannot allocate memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): the same arguments, kernels and
+ * outputs bit for bit, without a workspace argument.  Its scratch is a device array inside
+ * the library, fq_linear_static_max_workspace_bytes() = 64 MiB on every device the library
+ * runs on, held until the process ends; a shape whose fq_linear_workspace_bytes exceeds it
+ * is rejected with FQ_ERR_WORKSPACE before anything is enqueued.  The call allocates and
+ * frees nothing (the array's device address is looked up once per device, on the first
+ * call made with that device current).  All calls on one device share the array: calls
+ * that may overlap on a device (different streams, different threads without ordering)
+ * race; calls ordered on one stream do not.  The scratch needs no initialization. */
+size_t fq_linear_static_max_workspace_bytes(void);
+fq_status fq_linear_static(const void *x_bf16, int64_t ldx, const float *smooth_inv, const float *post_inv,
+                           int64_t M, int64_t K, int64_t N, int b, int bits, float clip_ratio,
+                           const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,
+                           int64_t ldy, void *stream);
+
 /* Static description of a status code, and the thread-local message of the last failure. */
 const char *fq_status_string(fq_status s);
 const char *fq_last_error(void);

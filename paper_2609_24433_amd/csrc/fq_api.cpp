@@ -5,11 +5,18 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <atomic>
 #include <cstring>
 #include <initializer_list>
 
 #include "../../include/fq.h"
 #include "fq_launch.hpp"
+
+// Scratch of fq_linear_static: the workspace of fq_linear in a file-scope device array
+// instead of a caller's buffer.  In host code `scratch` names a host-side stand-in, not the
+// device array: its device address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
 
 namespace {
 
@@ -279,6 +286,28 @@ fq_status linear_common(const void *x_bf16, int64_t ldx, const float *smooth_inv
                      gws_bytes, st);
 }
 
+// Device address of `scratch` on the current device, looked up once per device with that
+// device current (each device holds its own copy of the array).  Concurrent first calls
+// may both look it up; they store the same address.
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch_ptr[kMaxDevices];
+
+fq_status static_scratch(void **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(FQ_ERR_UNSUPPORTED, "device %d beyond %d devices", dev, kMaxDevices);
+  void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(FQ_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return FQ_OK;
+}
+
 fq_status rotate_common(const void *x, bool x_f32, int64_t ldx, const int32_t *perm, const float *blocks,
                         const float *pre, const float *post, int64_t M, int64_t K, int b, int bits, float r,
                         void *codes, int64_t ldc, float *delta, int fmt, void *ws, size_t ws_bytes,
@@ -497,6 +526,27 @@ fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, co
                     int64_t ldy, void *ws, size_t ws_bytes, void *stream) {
   return linear_common(x_bf16, ldx, smooth_inv, post_inv, M, K, N, b, bits, clip_ratio, w_packed, w_scale, bias,
                        y_bf16, ldy, ws, ws_bytes, stream);
+}
+
+size_t fq_linear_static_max_workspace_bytes(void) { return kStaticScratchBytes; }
+
+fq_status fq_linear_static(const void *x_bf16, int64_t ldx, const float *smooth_inv, const float *post_inv,
+                           int64_t M, int64_t K, int64_t N, int b, int bits, float clip_ratio,
+                           const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,
+                           int64_t ldy, void *stream) {
+  // the shape checks come first, so that a bad shape reports itself rather than a size
+  fq_status s = check_prologue_shape(ldx, 8, M, K, b, bits, clip_ratio);
+  if (s != FQ_OK) return s;
+  if ((s = check_gemm(x_bf16, w_scale, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K)) != FQ_OK) return s;
+  if (M == 0 || N == 0) return ok();
+  const size_t need = linear_ws_bytes(M, N, K, bits);
+  if (need > kStaticScratchBytes)
+    return fail(FQ_ERR_WORKSPACE, "this shape needs %zu bytes of scratch; fq_linear_static holds %zu", need,
+                kStaticScratchBytes);
+  void *ws = nullptr;
+  if (need > 0 && (s = static_scratch(&ws)) != FQ_OK) return s;
+  return linear_common(x_bf16, ldx, smooth_inv, post_inv, M, K, N, b, bits, clip_ratio, w_packed, w_scale, bias,
+                       y_bf16, ldy, ws, need > 0 ? kStaticScratchBytes : 0, stream);
 }
 
 // ---- GPTQ in the transformed coordinates (eq. (7)) ----

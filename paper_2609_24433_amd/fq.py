@@ -25,6 +25,7 @@ EXPORTED = ["fq_fwht_quant", "fq_quantize_weights", "fq_packed_weight_bytes", "f
             "fq_rotate_quant_workspace_bytes", "fq_rotate_quant", "fq_quantize_weights_rotated",
             "fq_transform", "fq_gptq_hessian", "fq_gptq_factor_workspace_bytes", "fq_gptq_factor",
             "fq_gptq_sweep_workspace_bytes", "fq_gptq_sweep",
+            "fq_linear_static_max_workspace_bytes", "fq_linear_static",
             "fq_status_string", "fq_last_error"]
 
 
@@ -55,6 +56,7 @@ def _load() -> ctypes.CDLL:
         "fq_gptq_hessian": [vp, i64, i64, i64, vp, i32, vp],
         "fq_gptq_factor": [vp, i64, ctypes.c_double, vp, vp, sz, vp],
         "fq_gptq_sweep": [vp, i64, vp, i64, i64, i32, i32, vp, vp, vp, sz, vp],
+        "fq_linear_static": [vp, i64, vp, vp, i64, i64, i64, i32, i32, f32, vp, vp, vp, vp, i64, vp],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -66,7 +68,8 @@ def _load() -> ctypes.CDLL:
                        "fq_gemm_w4a16_workspace_bytes": [i64, i64, i64],
                        "fq_rotate_quant_workspace_bytes": [i64, i64],
                        "fq_gptq_factor_workspace_bytes": [i64],
-                       "fq_gptq_sweep_workspace_bytes": [i64, i64]}.items():
+                       "fq_gptq_sweep_workspace_bytes": [i64, i64],
+                       "fq_linear_static_max_workspace_bytes": []}.items():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = sz
@@ -218,6 +221,22 @@ def linear(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: in
     _check(LIB.fq_linear(_p(x), x.stride(0) if M else K, _p(smooth_inv), _p(post_inv), M, K, N, b, bits, clip_ratio,
                          _p(w_packed), _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N, _p(ws), ws.numel(),
                          _stream()))
+    return y
+
+
+def linear_static(x: torch.Tensor, w_packed: torch.Tensor, w_scale: torch.Tensor, N: int, b: int, bits: int,
+                  clip_ratio: float = 1.0, smooth_inv: Optional[torch.Tensor] = None,
+                  bias: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                  post_inv: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """fq_linear without a workspace argument: the library's own device scratch (calls that
+    overlap on one device race)."""
+    M, K = x.shape
+    _require(x.dtype == torch.bfloat16 and (M == 0 or x.stride(1) == 1), "x: bf16 [M, K] with unit column stride")
+    _check_out(out, M, N)
+    y = out if out is not None else torch.empty((M, N), dtype=torch.bfloat16, device=x.device)
+    _check(LIB.fq_linear_static(_p(x), x.stride(0) if M else K, _p(smooth_inv), _p(post_inv), M, K, N, b, bits,
+                                clip_ratio, _p(w_packed), _p(w_scale), _p(bias), _p(y), y.stride(0) if M else N,
+                                _stream()))
     return y
 
 

@@ -312,3 +312,15 @@ def test_binding_rejects_mismatched_outputs():
         fq.linear(x, w, sw, 16, 64, 4, out=torch.empty((4, 16), dtype=torch.float16))
     with pytest.raises(ValueError):
         fq.fwht_quant(x, 64, 4, out_codes=torch.empty((4, 1024), dtype=torch.uint8))
+
+
+def test_linear_static_rejects_before_any_device_call():
+    """The scratch limit and the argument checks come before the library touches a device."""
+    f = fq.LIB.fq_linear_static
+    assert fq.LIB.fq_linear_static_max_workspace_bytes() == 64 << 20
+    assert fq.linear_workspace_bytes(4096, 2048, 32768, 8) > 64 << 20
+    assert f(FAKE, 32768, NULL, NULL, 4096, 32768, 2048, 128, 8, 1.0, FAKE, FAKE, NULL, FAKE, 2048, None) == 5
+    assert b"fq_linear_static holds" in fq.LIB.fq_last_error()
+    assert f(NULL, 1024, NULL, NULL, 4, 1024, 256, 64, 4, 1.0, FAKE, FAKE, NULL, FAKE, 256, None) == 1
+    assert f(FAKE, 1024, NULL, NULL, 4, 1000, 256, 64, 4, 1.0, FAKE, FAKE, NULL, FAKE, 256, None) == 3
+    assert f(NULL, 1024, NULL, NULL, 0, 1024, 256, 64, 4, 1.0, NULL, NULL, NULL, NULL, 256, None) == 0
