@@ -1,30 +1,43 @@
 """Benchmark of the W4A4 runtime quantized projection on one MI355X.
 
-Default workload: the action-expert layer at width 1024 (M = 50 action tokens per
-denoising step; q/k/v/o 1024->1024 with k/v 1024->256, gate/up 1024->4096, down
-4096->1024; all W4A4 with Hadamard block 128; 10 denoising steps with fresh seeded
-activations and shared weights).  One step = one denoising step of the whole hot path
-as Alg. 1 runs it at runtime: each of the 4 activation sites is transformed and
-quantized once and its consumers (q|k|v, o, gate|up, down) run their integer GEMMs
-with the rescale epilogue -- one fused projection (fq_linear) per site, the consumers of
-a site packed as one weight matrix.  Weights are folded, rounded and packed on the
-device before timing; inputs are resident in HBM when the timed region starts.
+Workload of the headline line: the action-expert layer at width 1024 (M = 50 action
+tokens per denoising step; q/k/v/o 1024->1024 with k/v 1024->256, gate/up 1024->4096,
+down 4096->1024; all W4A4 with Hadamard block 128; 10 denoising steps with fresh seeded
+activations and shared weights).  One step = one denoising step of the whole hot path as
+Alg. 1 runs it at runtime: each of the 4 activation sites is transformed and quantized
+once and its consumers (q|k|v, o, gate|up, down) run their integer GEMMs with the rescale
+epilogue -- one fused projection (fq_linear) per site, the consumers of a site packed as
+one weight matrix.  Weights are folded, rounded and packed on the device before timing;
+inputs are resident in HBM when the timed region starts.  The 10-step denoising loop is
+captured into one HIP graph (each step also into a graph of its own, for a remainder of K)
+and the timed region runs exactly K steps.
 
-The 10-step denoising loop is captured into one HIP graph (each step also into a graph
-of its own, for a remainder of K) and the timed region runs exactly K steps.  Prints ONE JSON line, which also carries `points`: the graded single projections
-(down-projection K 16384 -> N 2048 at M = 50 / 816 / 4096 and gate-projection M = 816,
-cold weights), the rest of the down-projection sweep (M = 1, 16, 256, 4096 in W4A4 and
-W8A8; the prologue at b = 32, 64, 128, 256), the 18-layer selective-INT8 backbone chain
-(time per layer and end to end, cosine against the fp32 chain), the weight-only INT4
-projection, the
-prologue alone with the composite rotation beside the block Hadamard, and the offline
-GPTQ stages.
+The JSON line also carries
+  roofline   the step's longest launch, timed with cold weights (rotating copies of >= 1 GiB
+             so that they come from HBM), resident weights beside it;
+  graded     the graded single projections: the down-projection K 16384 -> N 2048 at
+             M = 50, 816 and 4096, W4A4 and W8A8, the fused projection and its GEMM alone,
+             and the backbone's gate (2048 -> 16384) and down projections at M = 816, cold;
+  points     every other configuration: the single linear (M 64, 1024 -> 1024, b 64), the
+             action-expert sites with cold and resident weights, every projection of the
+             backbone layer at M = 816, the whole down-projection sweep (48 points: M in
+             {1, 16, 50, 256, 816, 4096} x b in {32, 64, 128, 256} x W4A4 / W8A8), the
+             prologue alone (block Hadamard against the composite rotation), weight-only
+             INT4, the offline GPTQ stages, the 18-layer selective-INT8 backbone chain at
+             b = 128 and b = 1, and bf16 torch.matmul context points;
+  cpu_baseline  the CPU oracle on the host cores (all threads, and one thread).
+Each graded and point record carries `rocprof_us`, the per-call kernel time of the same
+point in the committed rocprofv3 summary (profiles/points_kernels_by_grid.json, written by
+--summarize-trace from a `--rocprof-points` trace) while its source digest matches.
 
-  python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points] [--only-points]
+  python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points] [--points GROUPS]
+  python bench.py --rocprof-points           (under rocprofv3 --kernel-trace --stats)
+  python bench.py --summarize-trace CSV --manifest STDOUT_OF_THAT_RUN
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -40,6 +53,12 @@ INT8_PEAK_TOPS = 5000.0    # MI355X dense INT8 MFMA, TOPS (no INT4 MFMA on gfx95
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s (the W4A16 path)
 FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector ALU, TFLOP/s (the composite rotation's fma chains)
 FP64_PEAK_TFLOPS = 78.6        # MI355X fp64 vector ALU, TFLOP/s (the GPTQ stages)
+COLD_BYTES = 1 << 30       # weights rotate through >= 1 GiB of copies (4x the 256 MB MALL)
+
+CSRC = os.path.join(ROOT, "paper_2609_24433_amd", "csrc")
+PROFILES = os.path.join(ROOT, "profiles")
+TRAFFIC_FILE = os.path.join(PROFILES, "site_traffic.json")
+POINTS_TRACE_FILE = os.path.join(PROFILES, "points_kernels_by_grid.json")
 
 
 def parse():
@@ -49,16 +68,19 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-points", action="store_true")
-    ap.add_argument("--only-points", action="store_true",
-                    help="measure only the graded single projections (profiling aid)")
     ap.add_argument("--quiet", action="store_true")
     ap.add_argument("--traffic-site", default=None,
                     help="run only this site's fused projection 100 times (for HBM counter runs)")
-    ap.add_argument("--gemm-counters", action="store_true",
-                    help="run the tiled-GEMM points (K 16384 -> N 2048, M 816 and 4096) 10 times each, eagerly, "
-                         "for rocprofv3 --pmc runs")
+    ap.add_argument("--counter-point", default=None,
+                    help="run one named point's calls eagerly (for rocprofv3 --pmc runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 256 MiB copy-like kernel 20 times (counter calibration)")
+    ap.add_argument("--rocprof-points", action="store_true",
+                    help="run every timed point eagerly, one idle-separated segment each (for a kernel trace)")
+    ap.add_argument("--summarize-trace", default=None, metavar="CSV",
+                    help="summarize a --rocprof-points kernel trace into profiles/ and exit")
+    ap.add_argument("--manifest", default=None, help="stdout of the --rocprof-points run (its point list)")
+    ap.add_argument("--points", default=None, help="comma-separated point groups to run (default: all)")
     return ap.parse_args()
 
 
@@ -84,21 +106,23 @@ def linear_bytes(M, N, K, bits, bias=False):
     return 2 * M * K + N * K * bits // 8 + 4 * N + 2 * M * N + (4 * N if bias else 0)
 
 
-# --------------------------------------------------------------------------- HBM traffic
+def roofline(nbytes, ops, us, peak_ops=INT8_PEAK_TOPS):
+    """Bound, achieved and fraction of the roofline for one call of `us` microseconds."""
+    t_hbm = nbytes / HBM_PEAK_GBS / 1e3
+    t_mfma = ops / peak_ops / 1e6
+    if t_hbm >= t_mfma:
+        return {"bound": "hbm", "achieved": round(nbytes / us / 1e3, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(t_hbm / us, 4)}
+    return {"bound": "mfma", "achieved": round(ops / us / 1e6, 1), "peak": peak_ops, "unit": "TOPS",
+            "frac": round(t_mfma / us, 4)}
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "site_traffic.json")
-CSRC = os.path.join(ROOT, "paper_2609_24433_amd", "csrc")
 
-
-TRAFFIC_SOURCES = ("fq_api.cpp", "fq_codes.hpp", "fq_device.hpp", "fq_gemm.hip", "fq_quant.hip")  # what a site's projection runs
-
+# --------------------------------------------------------------------------- source digest
 
 def sources_digest():
-    """SHA-256 over the sources of the kernels a fused projection runs (and the entry point
-    that plans them): counter readings are void once any of them changes."""
-    import hashlib
+    """SHA-256 over the library sources: a profile reading is void once any of them changes."""
     h = hashlib.sha256()
-    for name in TRAFFIC_SOURCES:
+    for name in sorted(os.listdir(CSRC)):
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()
@@ -106,8 +130,7 @@ def sources_digest():
 
 def measured_traffic(site, part="linear"):
     """HBM bytes per call of `site` from the committed rocprofv3 counter runs (FETCH_SIZE
-    and WRITE_SIZE, each scaled by the same counter on a copy of known size): the whole
-    fused projection (part "linear") or its GEMM kernel alone (part "gemm"); None when
+    and WRITE_SIZE, each scaled by the same counter on a copy of known size); None when
     there is no reading for these sources and this site."""
     try:
         with open(TRAFFIC_FILE) as f:
@@ -125,114 +148,20 @@ def measured_traffic(site, part="linear"):
     return int(round(fetch + write))
 
 
-def traffic_run(torch, fq, synth, dev, site):
-    st = ExpertStep(torch, fq, synth, dev)
-    for i in range(100):
-        st.run_site(site, i % st.n_steps)
-    torch.cuda.synchronize()
-    print(json.dumps({"traffic_site": site, "calls": 100}), flush=True)
-
-
-def copy_calibration(torch, dev):
-    n = 64 << 20  # float32 elements: 256 MiB read and 256 MiB written per launch
-    a = torch.ones(n, dtype=torch.float32, device=dev)
-    b = torch.empty_like(a)
-    for _ in range(20):
-        torch.add(a, 0.0, out=b)
-    torch.cuda.synchronize()
-    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 20}), flush=True)
-
-
-# --------------------------------------------------------------------------- workload
-
-class ExpertStep:
-    """Device state of the action-expert layer.  Consumers of one activation site share
-    that site's transform and quantization (Alg. 1 runtime; Sec. III-B shared sites), so
-    their folded weights are packed as one matrix (q|k|v, gate|up): per-output-channel
-    scales make this exactly the same as separate consumers.  One fused projection
-    (fq_linear) runs per site."""
-
-    def __init__(self, torch, fq, synth, dev, n_steps=10):
-        self.torch, self.fq = torch, fq
-        self.wl = synth.action_expert_layer()
-        wl = self.wl
-        self.b = wl.b
-        self.sites = wl.sites()
-        self.site_projs = {s: [p for p in wl.projections if p.site == s] for s in self.sites}
-        self.site_N = {s: sum(p.N for p in ps) for s, ps in self.site_projs.items()}
-        self.w_host = {s: np.concatenate([wl.projection_weight(p) for p in ps], axis=0)
-                       for s, ps in self.site_projs.items()}
-        self.lin = {}
-        for s in self.sites:
-            w = torch.from_numpy(self.w_host[s]).to(dev)
-            self.lin[s] = fq.QuantLinear(w, wl.b, 4)
-            del w
-        self.x = {s: [wl.site_activation(s, t).to(dev) for t in range(n_steps)] for s in self.sites}
-        M = wl.M
-        self.y = {s: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for s, N in self.site_N.items()}
-        self.ws = {s: fq.workspace(fq.linear_workspace_bytes(M, self.site_N[s], K, 4), dev)
-                   for s, K in self.sites.items()}
-        self.n_steps = n_steps
-
-    def run_site(self, s, t):
-        self.lin[s](self.x[s][t], ws=self.ws[s], out=self.y[s])
-
-    def gemm_call(self, s, t=0):
-        """The site's GEMM alone, on the codes and scales of step t's prologue: a
-        callable that launches it (for timing the GEMM kernel by itself)."""
-        fq, wl = self.fq, self.wl
-        K, N = self.sites[s], self.site_N[s]
-        codes, delta = fq.fwht_quant(self.x[s][t], self.b, 4)
-        ws = fq.workspace(fq.gemm_workspace_bytes(wl.M, N, K, 4), codes.device)
-        lin, y = self.lin[s], self.y[s]
-        return lambda i: fq.gemm(codes, delta, lin.w_packed, lin.w_scale, N, K, 4, ws=ws, out=y)
-
-    def run(self, t):
-        """Enqueue one denoising step: the 4 sites in order."""
-        for s in self.sites:
-            self.run_site(s, t)
-
-
-def check_step(st, oracle, torch):
-    """Every site of step 0 against the oracle (bf16 within 1e-2 of the row absmax)."""
-    st.run(0)
-    torch.cuda.synchronize()
-    for s in st.sites:
-        wc, s_w = oracle.quantize_weights(st.w_host[s], st.b, 4)
-        _, _, _, y_ref = oracle.linear(st.x[s][0].cpu(), wc, s_w, st.b, 4)
-        yg = st.y[s].float().cpu().numpy().astype(np.float64)
-        tol = 1e-2 * np.abs(y_ref).max(axis=1, keepdims=True)
-        if not np.all(np.abs(yg - y_ref) <= tol):
-            raise SystemExit(f"bench parity check failed at site {s}: GPU output differs from the oracle")
-
-
-def cpu_baseline(st, oracle, torch, budget_s=15.0):
-    """The oracle on the host cores: whole denoising steps (4 site prologues + the 7
-    consumers' contractions and rescales) until about budget_s seconds are spent."""
-    wq = {s: oracle.quantize_weights(st.w_host[s], st.b, 4) for s in st.sites}
-    xs = {s: [a.cpu() for a in st.x[s]] for s in st.sites}
-    steps, t0 = 0, time.perf_counter()
-    while True:
-        t = steps % st.n_steps
-        for s in st.sites:
-            codes, delta = oracle.fwht_quant(xs[s][t], st.b, 4)
-            wc, s_w = wq[s]
-            oracle.dequant(oracle.gemm(codes, wc), delta, s_w)
-        steps += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or steps >= 1000:
-            break
-    ops = st.wl.ops_per_step() * steps
-    model = "unknown"
+def rocprof_points():
+    """name -> committed rocprof summary record of a point (kernel time per call, kernels
+    by grid), or {} when the summary does not match these sources."""
     try:
-        with open("/proc/cpuinfo") as f:
-            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), model)
-    except OSError:
-        pass
-    return {"value": ops / el / 1e12, "unit": "TOPS", "cores": oracle.max_threads(), "kind": "oracle",
-            "sample": f"{steps} denoising steps of the action-expert layer (M=50, 7 projections), "
-                      f"{el:.1f} s", "cpu_model": model, "nproc": os.cpu_count()}
+        with open(POINTS_TRACE_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return {}
+    if t.get("sources_sha256") != sources_digest():
+        return {}
+    return t.get("points", {})
 
+
+# --------------------------------------------------------------------------- timing
 
 def graph_of(torch, fn, reps):
     """Capture `reps` back-to-back calls of fn(i) into one HIP graph."""
@@ -264,8 +193,7 @@ def time_graph(torch, g, replays):
 
 
 def replay_spread(torch, g, replays):
-    """Seconds of each of `replays` replays of g, timed one by one with HIP events (for the
-    p10 / median / p90 of the per-call time)."""
+    """Seconds of each of `replays` replays of g, timed one by one with HIP events."""
     g.replay()
     torch.cuda.synchronize()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(replays + 1)]
@@ -275,6 +203,18 @@ def replay_spread(torch, g, replays):
         ev[r + 1].record()
     torch.cuda.synchronize()
     return [ev[r].elapsed_time(ev[r + 1]) / 1e3 for r in range(replays)]
+
+
+def time_calls(torch, call, calls):
+    """Per-call microseconds of call(i): a graph of `calls` back-to-back calls, warmed up
+    with >= 20 calls, then >= 21 replays timed one by one; (median, p10, p90, mean)."""
+    g = graph_of(torch, call, calls)
+    for _ in range(max(1, -(-20 // calls))):
+        g.replay()
+    reps = max(21, -(-100 // calls) | 1)
+    spread = sorted(t / calls * 1e6 for t in replay_spread(torch, g, reps))
+    del g
+    return spread[reps // 2], spread[reps // 10], spread[reps - 1 - reps // 10], sum(spread) / reps
 
 
 def time_graph_steps(torch, graphs, K, W, loop=None):
@@ -303,105 +243,299 @@ def time_graph_steps(torch, graphs, K, W, loop=None):
     return e0.elapsed_time(e1) / 1e3  # seconds
 
 
-def gemm_counter_run(torch, fq, synth, dev):
-    """The tiled GEMM on the down-projection K 16384 -> N 2048 at M = 816 and 4096 (W4A4),
-    10 eager calls each, for counter collection."""
-    for M in (816, 4096):
-        K, N, b, bits = 16384, 2048, 128, 4
-        lin = fq.QuantLinear(torch.from_numpy(synth.weights(N, K, seed=K + N + bits)).to(dev), b, bits)
-        x = synth.activations(M, K, seed=M + K, outlier_frac=0.005, outlier_scale=50.0).to(dev)
-        codes, delta = fq.fwht_quant(x, b, bits)
-        ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
-        y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
-        for _ in range(10):
-            fq.gemm(codes, delta, lin.w_packed, lin.w_scale, N, K, bits, ws=ws, out=y)
-        torch.cuda.synchronize()
-        print(json.dumps({"gemm_counters": {"M": M, "K": K, "N": N, "calls": 10}}), flush=True)
+# --------------------------------------------------------------------------- the denoising step
+
+class ExpertStep:
+    """Device state of the action-expert layer.  Consumers of one activation site share
+    that site's transform and quantization (Alg. 1 runtime; Sec. III-B shared sites), so
+    their folded weights are packed as one matrix (q|k|v, gate|up): per-output-channel
+    scales make this exactly the same as separate consumers.  One fused projection
+    (fq_linear) runs per site.  copies > 1 keeps that many copies of the packed weights,
+    call c using copy c % copies (cold weights)."""
+
+    def __init__(self, torch, fq, synth, dev, n_steps=10, copies=1):
+        self.torch, self.fq = torch, fq
+        self.wl = synth.action_expert_layer()
+        wl = self.wl
+        self.b = wl.b
+        self.sites = wl.sites()
+        self.site_projs = {s: [p for p in wl.projections if p.site == s] for s in self.sites}
+        self.site_N = {s: sum(p.N for p in ps) for s, ps in self.site_projs.items()}
+        self.w_host = {s: np.concatenate([wl.projection_weight(p) for p in ps], axis=0)
+                       for s, ps in self.site_projs.items()}
+        self.lin = {}
+        for s in self.sites:
+            w = torch.from_numpy(self.w_host[s]).to(dev)
+            self.lin[s] = fq.QuantLinear(w, wl.b, 4)
+            del w
+        self.copies = copies
+        self.wp = {s: [self.lin[s].w_packed] + [self.lin[s].w_packed.clone() for _ in range(copies - 1)]
+                   for s in self.sites}
+        self.x = {s: [wl.site_activation(s, t).to(dev) for t in range(n_steps)] for s in self.sites}
+        M = wl.M
+        self.y = {s: torch.empty((M, N), dtype=torch.bfloat16, device=dev) for s, N in self.site_N.items()}
+        self.ws = {s: fq.workspace(fq.linear_workspace_bytes(M, self.site_N[s], K, 4), dev)
+                   for s, K in self.sites.items()}
+        self.n_steps = n_steps
+
+    def run_site(self, s, t, c=0):
+        lin = self.lin[s]
+        self.fq.linear(self.x[s][t % self.n_steps], self.wp[s][c % self.copies], lin.w_scale, self.site_N[s], self.b,
+                       4, ws=self.ws[s], out=self.y[s])
+
+    def run(self, t, c=0):
+        """Enqueue one denoising step: the 4 sites in order."""
+        for s in self.sites:
+            self.run_site(s, t, c)
+
+    def weight_bytes(self):
+        return sum(w.numel() for w in (self.lin[s].w_packed for s in self.sites))
 
 
-def measure_points(torch, fq, synth, dev, log_fn):
-    """Graded single-projection points, cold: weights rotate through >= 1 GiB of copies so
-    they come from HBM; each point is a graph of back-to-back calls, warmed up with >= 20
-    calls, then replayed >= 21 times with HIP events around every replay; `us` is the
-    median per-call time (p10 / p90 and the mean beside it)."""
-    out = []
+def check_step(st, oracle, torch):
+    """Every site of step 0 against the oracle (bf16 within 1e-2 of the row absmax)."""
+    st.run(0)
+    torch.cuda.synchronize()
+    for s in st.sites:
+        wc, s_w = oracle.quantize_weights(st.w_host[s], st.b, 4)
+        _, _, _, y_ref = oracle.linear(st.x[s][0].cpu(), wc, s_w, st.b, 4)
+        yg = st.y[s].float().cpu().numpy().astype(np.float64)
+        tol = 1e-2 * np.abs(y_ref).max(axis=1, keepdims=True)
+        if not np.all(np.abs(yg - y_ref) <= tol):
+            raise SystemExit(f"bench parity check failed at site {s}: GPU output differs from the oracle")
 
-    def run_point(name, M, K, N, b, bits, kind, warm=False):
-        wl = synth.down_proj_sweep_point(M, b, bits) if K == 16384 else None
-        w = torch.from_numpy(synth.weights(N, K, seed=K + N + bits)).to(dev)
-        lin = fq.QuantLinear(w, b, bits)
-        del w
-        wbytes = lin.w_packed.numel()
-        # cold: weights rotate through >= 1 GiB of copies; warm: one copy, resident in the caches
-        copies = 1 if warm else max(2, min(64, (1 << 30) // wbytes + 1))
-        wp = [lin.w_packed.clone() for _ in range(copies)]
-        x = (wl.site_activation("D", 0) if wl is not None else
-             synth.activations(M, K, seed=M + K, outlier_frac=0.005, outlier_scale=50.0)).to(dev)
-        y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
-        codes, delta = fq.fwht_quant(x, b, bits)
-        if kind == "linear":
-            ws = fq.workspace(fq.linear_workspace_bytes(M, N, K, bits), dev)
-            call = lambda i: fq.linear(x, wp[i % copies], lin.w_scale, N, b, bits, ws=ws, out=y)
-            nbytes = linear_bytes(M, N, K, bits)
+
+# --------------------------------------------------------------------------- single-projection points
+
+def cold_copies(nbytes):
+    return max(2, min(64, COLD_BYTES // max(1, nbytes) + 1))
+
+
+def point_specs(groups=None):
+    """Every timed single-projection point: (group, name, M, K, N, b, bits, kind, weights).
+    kind: linear (fq_linear, the fused projection), gemm (the GEMM alone, on the prologue's
+    codes), w4a16 (weight-only INT4); weights: cold or warm."""
+    specs = []
+
+    def add(g, n, M, K, N, b, bits, kind, w="cold"):
+        specs.append((g, n, M, K, N, b, bits, kind, w))
+
+    # graded: the down-projection K 16384 -> N 2048 (down-projection sweep data, b = 128) and the
+    # backbone's gate and down projections at M = 816
+    for M in (50, 816, 4096):
+        for bits in (4, 8):
+            for kind in ("linear", "gemm"):
+                add("graded", f"down_m{M}_w{bits}a{bits}_{kind}", M, 16384, 2048, 128, bits, kind)
+    for kind in ("linear", "gemm"):
+        add("graded", f"backbone_gate_m816_w4a4_{kind}", 816, 2048, 16384, 128, 4, kind)
+        add("graded", f"backbone_down_m816_w4a4_{kind}", 816, 16384, 2048, 128, 4, kind)
+    # the single linear (M = 64, K = N = 1024, b = 64)
+    for w in ("cold", "warm"):
+        add("single", f"single_m64_k1024_n1024_{w}", 64, 1024, 1024, 64, 4, "linear", w)
+    # action-expert sites, cold and warm (q|k|v, o, gate|up, down), and site D's GEMM alone
+    for site, K, N in (("A", 1024, 1536), ("O", 1024, 1024), ("B", 1024, 8192), ("D", 4096, 1024)):
+        for w in ("cold", "warm"):
+            add("expert_sites", f"expert_site{site}_m50_{w}", 50, K, N, 128, 4, "linear", w)
+    add("expert_sites", "expert_siteD_m50_gemm_cold", 50, 4096, 1024, 128, 4, "gemm")
+    # every projection of the backbone layer at M = 816, and its grouped sites
+    for name, K, N in (("q", 2048, 2048), ("k", 2048, 256), ("v", 2048, 256), ("o", 2048, 2048),
+                       ("gate", 2048, 16384), ("up", 2048, 16384), ("down", 16384, 2048),
+                       ("siteA_qkv", 2048, 2560), ("siteB_gateup", 2048, 32768)):
+        add("backbone_projections", f"backbone_{name}_m816", 816, K, N, 128, 4, "linear")
+    # the whole down-projection sweep, fused projection
+    for bits in (4, 8):
+        for M in (1, 16, 50, 256, 816, 4096):
+            for b in (32, 64, 128, 256):
+                add("sweep", f"sweep_m{M}_b{b}_w{bits}a{bits}", M, 16384, 2048, b, bits, "linear")
+    # weight-only INT4 (the adaptive layer-norm modulation path), b = 1
+    add("w4a16", "adaln_w4a16_m1_k1024_n6144", 1, 1024, 6144, 1, 4, "w4a16")
+    add("w4a16", "down_w4a16_m1", 1, 16384, 2048, 1, 4, "w4a16")
+    add("w4a16", "down_w4a16_m16", 16, 16384, 2048, 1, 4, "w4a16")
+    if groups:
+        specs = [s for s in specs if s[0] in groups]
+    return specs
+
+
+def point_data(synth, name, M, K, N, b, bits):
+    """The point's seeded tokens (bf16 [M, K], CPU) and fp32 weights [N, K]: the workload's
+    own generators (down-projection sweep, backbone layer, action-expert layer, single
+    linear)."""
+    if name.startswith("down_m") or name.startswith("sweep_"):
+        wl = synth.down_proj_sweep_point(M, b, bits)
+        return wl.site_activation("D", 0), wl.projection_weight(wl.projections[0])
+    if name.startswith("backbone_"):
+        wl = synth.backbone_layer()
+        part = name[len("backbone_"):].split("_m816")[0].replace("_w4a4", "")
+        groups = {"siteA_qkv": ("q", "k", "v"), "siteB_gateup": ("gate", "up")}
+        names = groups.get(part, (part,))
+        projs = [p for p in wl.projections if p.name in names]
+        return wl.site_activation(projs[0].site, 0), np.concatenate([wl.projection_weight(p) for p in projs], axis=0)
+    if name.startswith("expert_site"):
+        wl = synth.action_expert_layer()
+        site = name[len("expert_site")]
+        projs = [p for p in wl.projections if p.site == site]
+        return wl.site_activation(site, 0), np.concatenate([wl.projection_weight(p) for p in projs], axis=0)
+    if name.startswith("single_"):
+        wl = synth.single_linear()
+        p = wl.projections[0]
+        return (synth.activations(M, K, seed=0, outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale),
+                wl.projection_weight(p))
+    return (synth.activations(M, K, seed=M + K, outlier_frac=0.005, outlier_scale=50.0),
+            synth.weights(N, K, seed=K + N + bits))
+
+
+class Point:
+    """Device state of one point: weights (with copies for cold rotation), tokens, codes,
+    workspace, output, and the call."""
+
+    def __init__(self, torch, fq, synth, dev, spec):
+        self.spec = spec
+        _, name, M, K, N, b, bits, kind, weights = spec
+        x, w = point_data(synth, name, M, K, N, b, bits)
+        wd = torch.from_numpy(w).to(dev)
+        lin = fq.QuantLinear(wd, b, bits)
+        del wd
+        self.copies = 1 if weights == "warm" else cold_copies(lin.w_packed.numel())
+        self.wp = [lin.w_packed] + [lin.w_packed.clone() for _ in range(self.copies - 1)]
+        self.w_scale = lin.w_scale
+        self.x = x.to(dev)
+        self.y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        if kind == "gemm":
+            self.codes, self.delta = fq.fwht_quant(self.x, b, bits)
+            self.ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
+            self.nbytes, self.peak = gemm_bytes(M, N, K, bits), INT8_PEAK_TOPS
         elif kind == "w4a16":
-            ws = fq.workspace(fq.w4a16_workspace_bytes(M, N, K), dev)
-            call = lambda i: fq.gemm_w4a16(x, wp[i % copies], lin.w_scale, N, ws=ws, out=y)
-            nbytes = linear_bytes(M, N, K, 4)
+            self.ws = fq.workspace(fq.w4a16_workspace_bytes(M, N, K), dev)
+            self.nbytes, self.peak = linear_bytes(M, N, K, 4), BF16_PEAK_TFLOPS
         else:
-            ws = fq.workspace(fq.gemm_workspace_bytes(M, N, K, bits), dev)
-            call = lambda i: fq.gemm(codes, delta, wp[i % copies], lin.w_scale, N, K, bits, ws=ws, out=y)
-            nbytes = gemm_bytes(M, N, K, bits)
-        # a graph of back-to-back calls; >= 20 warm-up calls, then 21 replays timed one by one
-        # (>= 100 calls in all): the median per-call time is the point's figure, p10 / p90 and
-        # the mean beside it
-        calls = 50 if warm else copies
-        g = graph_of(torch, call, calls)
-        for _ in range(max(1, -(-20 // calls))):
-            g.replay()
-        reps = max(21, -(-100 // calls) | 1)
-        spread = sorted(t / calls * 1e6 for t in replay_spread(torch, g, reps))
-        us = spread[reps // 2]
-        us_mean = sum(spread) / reps
-        ops = 2.0 * M * N * K
-        t_hbm = nbytes / HBM_PEAK_GBS / 1e3
-        t_mfma = ops / (BF16_PEAK_TFLOPS if kind == "w4a16" else INT8_PEAK_TOPS) / 1e6
-        rec = {"name": name, "kind": kind, "M": M, "K": K, "N": N, "b": b, "bits": bits, "weights": "warm" if warm else "cold",
-               "us": round(us, 3), "us_p10_p90": [round(spread[reps // 10], 3), round(spread[reps - 1 - reps // 10], 3)],
-               "us_mean": round(us_mean, 3),
-               "TOPS": round(ops / us / 1e6, 2), "GBps": round(nbytes / us / 1e3, 1),
-               "bound": "hbm" if t_hbm >= t_mfma else "mfma",
-               "roofline_frac": round(max(t_hbm, t_mfma) / us, 4)}
-        log_fn(json.dumps(rec))
-        out.append(rec)
-        del wp, lin, ws, g
+            self.ws = fq.workspace(fq.linear_workspace_bytes(M, N, K, bits), dev)
+            self.nbytes, self.peak = linear_bytes(M, N, K, bits), INT8_PEAK_TOPS
+        self.ops = 2.0 * M * N * K
+        c, f = self.copies, fq
+        if kind == "gemm":
+            self.call = lambda i: f.gemm(self.codes, self.delta, self.wp[i % c], self.w_scale, N, K, bits, ws=self.ws,
+                                         out=self.y)
+        elif kind == "w4a16":
+            self.call = lambda i: f.gemm_w4a16(self.x, self.wp[i % c], self.w_scale, N, ws=self.ws, out=self.y)
+        else:
+            self.call = lambda i: f.linear(self.x, self.wp[i % c], self.w_scale, N, b, bits, ws=self.ws, out=self.y)
+
+    def calls(self):
+        return 50 if self.copies == 1 else self.copies
+
+
+def measure_point(torch, fq, synth, dev, spec, traced):
+    pt = Point(torch, fq, synth, dev, spec)
+    group, name, M, K, N, b, bits, kind, weights = spec
+    us, p10, p90, mean = time_calls(torch, pt.call, pt.calls())
+    rec = {"name": name, "group": group, "kind": kind, "M": M, "K": K, "N": N, "b": b, "bits": bits,
+           "weights": weights, "us": round(us, 3), "us_p10_p90": [round(p10, 3), round(p90, 3)],
+           "us_mean": round(mean, 3), "TOPS": round(pt.ops / us / 1e6, 2), "algorithmic_bytes": pt.nbytes,
+           "roofline": roofline(pt.nbytes, pt.ops, us, pt.peak)}
+    tr = traced.get(name)
+    if tr:
+        rec["rocprof_us"] = tr["us_per_call"]
+        rec["rocprof_frac"] = roofline(pt.nbytes, pt.ops, tr["us_per_call"], pt.peak)["frac"]
+    del pt
+    torch.cuda.empty_cache()
+    return rec
+
+
+def rocprof_points_run(torch, fq, synth, dev, groups):
+    """Every point's calls eagerly, as idle-separated segments of a kernel trace: for point i,
+    its set-up (weights and copies: at least one kernel), a pause, its calls (one per weight
+    copy; cold points rotate through >= 1 GiB of copies), a pause.  The manifest printed at
+    the end lists the points in order."""
+    manifest = []
+    for spec in point_specs(groups):
+        pt = Point(torch, fq, synth, dev, spec)
+        torch.cuda.synchronize()
+        time.sleep(0.03)
+        n = max(pt.calls(), 20)
+        for i in range(n):
+            pt.call(i)
+        torch.cuda.synchronize()
+        time.sleep(0.03)
+        manifest.append({"name": spec[1], "calls": n})
+        print(json.dumps({"rocprof_point": spec[1], "calls": n}), flush=True)
+        del pt
         torch.cuda.empty_cache()
+    print(json.dumps({"rocprof_manifest": manifest}), flush=True)
 
-    run_point("down_w4a4_m50_linear", 50, 16384, 2048, 128, 4, "linear")
-    run_point("down_w4a4_m50_gemm", 50, 16384, 2048, 128, 4, "gemm")
-    run_point("down_w8a8_m50_linear", 50, 16384, 2048, 128, 8, "linear")
-    run_point("gate_w4a4_m816_linear", 816, 2048, 16384, 128, 4, "linear")
-    run_point("down_w4a4_m816_linear", 816, 16384, 2048, 128, 4, "linear")
-    run_point("down_w4a4_m816_gemm", 816, 16384, 2048, 128, 4, "gemm")
-    run_point("down_w8a8_m816_linear", 816, 16384, 2048, 128, 8, "linear")
-    run_point("down_w4a4_m4096_gemm", 4096, 16384, 2048, 128, 4, "gemm")
-    # the rest of the down-projection sweep's token counts (K 16384 -> N 2048, b = 128)
-    for bits_ in (4, 8):
-        for M_ in (1, 16, 256, 4096):
-            run_point(f"down_w{bits_}a{bits_}_m{M_}_linear", M_, 16384, 2048, 128, bits_, "linear")
-    # warm: the same weights every call (resident in the 256 MB MALL), as shared weights are
-    # across denoising steps
-    run_point("down_w4a4_m50_linear_warm", 50, 16384, 2048, 128, 4, "linear", warm=True)
-    run_point("down_w4a4_m816_linear_warm", 816, 16384, 2048, 128, 4, "linear", warm=True)
-    # weight-only INT4 (adaptive layer-norm modulation path): b = 1, no rotation
-    run_point("adaln_w4a16_m1", 1, 1024, 6144, 1, 4, "w4a16")
-    run_point("down_w4a16_m1", 1, 16384, 2048, 1, 4, "w4a16")
-    run_point("down_w4a16_m16", 16, 16384, 2048, 1, 4, "w4a16")
-    out += measure_bf16_context(torch, synth, dev, log_fn, out)
-    out += measure_prologue_points(torch, fq, synth, dev, log_fn)
-    out += measure_mixed_chain(torch, fq, synth, dev, log_fn)
-    out += measure_gptq_points(torch, fq, synth, dev, log_fn)
-    return out
 
+def summarize_trace(path, manifest_path):
+    """Per-point, per-grid kernel summary of a `--rocprof-points` kernel trace (rocprofv3
+    CSV): the trace is split at idle gaps of >= 10 ms into segments; the last 2 P of them are
+    the P points' set-up and measured segments, alternating, matched in order to the run's
+    manifest (its last JSON line).  Writes profiles/points_kernels_by_grid.{json,md}."""
+    import csv
+    manifest = None
+    with open(manifest_path) as f:
+        for line in f:
+            if line.startswith("{") and "rocprof_manifest" in line:
+                manifest = json.loads(line)["rocprof_manifest"]
+    if manifest is None:
+        raise SystemExit(f"no manifest line in {manifest_path}")
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            grid = tuple(int(r.get(f"Grid_Size_{a}") or 0) for a in "XYZ")
+            wg = tuple(int(r.get(f"Workgroup_Size_{a}") or 0) for a in "XYZ")
+            rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"], grid, wg))
+    rows.sort()
+    segs, cur, last_end = [], [], -1
+    for r in rows:  # sorted by start; a gap is measured from the latest end so far
+        if cur and r[0] - last_end >= 10_000_000:
+            segs.append(cur)
+            cur = []
+        cur.append(r)
+        last_end = max(last_end, r[1])
+    segs.append(cur)
+    need = 2 * len(manifest)
+    if len(segs) < need:
+        raise SystemExit(f"{len(segs)} trace segments for {len(manifest)} points")
+    segs = segs[len(segs) - need:]
+    points = {}
+    for i, m in enumerate(manifest):
+        by = {}
+        for start, end, name, grid, wg in segs[2 * i + 1]:
+            by.setdefault((name, grid, wg), []).append((end - start) / 1e3)
+        kern = []
+        for (name, grid, wg), d in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+            kern.append({"kernel": name, "grid": list(grid), "workgroup": list(wg), "launches": len(d),
+                         "avg_us": round(sum(d) / len(d), 3), "min_us": round(min(d), 3), "max_us": round(max(d), 3)})
+        total = sum(sum(d) for d in by.values())
+        points[m["name"]] = {"calls": m["calls"], "us_per_call": round(total / m["calls"], 3), "kernels": kern}
+    out = {"sources_sha256": sources_digest(), "points": points,
+           "note": "kernel execution time per call (the sum of the call's kernels, no launch gaps) from a "
+                   "rocprofv3 kernel trace of `python bench.py --rocprof-points`"}
+    with open(POINTS_TRACE_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+    lines = ["# Kernel time per point, by kernel and grid (rocprofv3 kernel trace)", "",
+             "Commands (from the repository root on an MI355X, `cd /tmp && export TMPDIR=/tmp` first):", "",
+             "```",
+             "rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o points -- "
+             "python /root/repo/bench.py --rocprof-points --quiet > <out>/manifest.txt",
+             "python /root/repo/bench.py --summarize-trace <out>/<host>/points_kernel_trace.csv "
+             "--manifest <out>/manifest.txt", "```", "",
+             "Each point ran its calls eagerly between idle gaps (one call per weight copy; cold points rotate "
+             "through >= 1 GiB of copies). `us/call` is the sum of the point's kernel durations divided by its "
+             "calls (no launch gaps); bench.py reports it beside its own graph-replay figure as `rocprof_us`. "
+             f"Sources SHA-256 {out['sources_sha256'][:16]}.", "",
+             "| point | calls | us/call | kernel | grid | workgroup | launches | avg us | min | max |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for name, p in points.items():
+        for j, k in enumerate(p["kernels"]):
+            head = f"| {name} | {p['calls']} | {p['us_per_call']}" if j == 0 else "| | |"
+            lines.append(f"{head} | `{k['kernel'][:100]}` | {'x'.join(map(str, k['grid']))} | "
+                         f"{'x'.join(map(str, k['workgroup']))} | {k['launches']} | {k['avg_us']} | {k['min_us']} | "
+                         f"{k['max_us']} |")
+    with open(POINTS_TRACE_FILE.replace(".json", ".md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(f"{len(points)} points summarized into {POINTS_TRACE_FILE}")
+
+
+# --------------------------------------------------------------------------- other points
 
 def measure_bf16_context(torch, synth, dev, log_fn, pts):
     """Context only (the analog of the paper's floating-point engine control): the same
@@ -410,18 +544,18 @@ def measure_bf16_context(torch, synth, dev, log_fn, pts):
     carries the fused W4A4 projection's speed-up over it."""
     out = []
     lin_us = {(p["M"], p["K"], p["N"]): p["us"] for p in pts
-              if p["kind"] == "linear" and p["bits"] == 4 and p.get("weights") == "cold"}
+              if p.get("kind") == "linear" and p.get("bits") == 4 and p.get("weights") == "cold" and p.get("b") == 128}
     for (M, K, N) in ((50, 16384, 2048), (816, 16384, 2048), (816, 2048, 16384)):
         wt = torch.from_numpy(synth.weights(N, K, seed=K + N).T.copy()).to(dev).to(torch.bfloat16)  # [K, N]
-        copies = max(2, min(64, (1 << 30) // (wt.numel() * 2) + 1))
+        copies = cold_copies(wt.numel() * 2)
         ws = [wt.clone() for _ in range(copies)]
         del wt
         x = synth.activations(M, K, seed=M + K, outlier_frac=0.005, outlier_scale=50.0).to(dev)
         y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
         g = graph_of(torch, lambda i: torch.matmul(x, ws[i % copies], out=y), copies)
         us = time_graph(torch, g, max(1, 200 // copies)) / copies * 1e6
-        rec = {"name": f"context_bf16_matmul_m{M}_k{K}_n{N}", "kind": "bf16_matmul", "M": M, "K": K, "N": N,
-               "us": round(us, 3), "TFLOPS": round(2.0 * M * N * K / us / 1e6, 2),
+        rec = {"name": f"context_bf16_matmul_m{M}_k{K}_n{N}", "group": "context", "kind": "bf16_matmul", "M": M,
+               "K": K, "N": N, "us": round(us, 3), "TFLOPS": round(2.0 * M * N * K / us / 1e6, 2),
                "w4a4_linear_speedup": round(us / lin_us[(M, K, N)], 2) if (M, K, N) in lin_us else None}
         log_fn(json.dumps(rec))
         out.append(rec)
@@ -446,7 +580,7 @@ def measure_gptq_points(torch, fq, synth, dev, log_fn):
         stages = (("hessian", lambda: fq.gptq_hessian(z, G), T * K * (K + 1)),
                   ("factor", lambda: fq.gptq_factor(G), 2 * K ** 3 / 3),
                   ("sweep", lambda: fq.gptq_sweep(w_t, U, b, 4), N * K ** 2))
-        rec = {"name": name, "kind": "gptq", "N": N, "K": K, "T": T, "b": b, "bits": 4}
+        rec = {"name": name, "group": "gptq", "kind": "gptq", "N": N, "K": K, "T": T, "b": b, "bits": 4}
         total = 0.0
         for sname, fn, flops in stages:
             fn()
@@ -470,9 +604,10 @@ def measure_gptq_points(torch, fq, synth, dev, log_fn):
 
 def measure_prologue_points(torch, fq, synth, dev, log_fn):
     """The activation prologue alone, block Hadamard butterfly against the stored composite
-    rotation (permutation + dense per-block matrices) on the same tokens.  Algorithmic bytes:
-    x, codes and scales, plus the permutation and the blocks for the composite one; its
-    2 M K b flops (fp32 fma chains) give the ALU side of its roofline."""
+    rotation (permutation + dense per-block matrices) on the same tokens, and the butterfly
+    at every block size of the down-projection sweep.  Algorithmic bytes: x, codes and
+    scales, plus the permutation and the blocks for the composite one; its 2 M K b flops
+    (fp32 fma chains) give the ALU side of its roofline."""
     out = []
     for (name, M, K, b) in (("ae_prologue_m50_k1024", 50, 1024, 128), ("ae_prologue_m50_k4096", 50, 4096, 128),
                             ("lang_prologue_m816_k2048", 816, 2048, 128)):
@@ -483,7 +618,7 @@ def measure_prologue_points(torch, fq, synth, dev, log_fn):
         delta = torch.empty((M,), dtype=torch.float32, device=dev)
         ws = fq.workspace(int(fq.LIB.fq_rotate_quant_workspace_bytes(M, K)), dev)
         reps = 50
-        base = M * (2 * K + K // 2 + 4)
+        base = quant_bytes(M, K, 4)
         for kind in ("fwht", "rotate"):
             if kind == "fwht":
                 call = lambda i: fq._check(fq.LIB.fq_fwht_quant(fq._p(x), K, None, None, M, K, b, 4, 1.0, fq._p(codes),
@@ -498,16 +633,14 @@ def measure_prologue_points(torch, fq, synth, dev, log_fn):
             us = time_graph(torch, g, 4) / reps * 1e6
             t_hbm = nbytes / HBM_PEAK_GBS / 1e3
             t_alu = flops / FP32_VALU_PEAK_TFLOPS / 1e6
-            rec = {"name": f"{name}_{kind}", "kind": f"prologue_{kind}", "M": M, "K": K, "b": b, "bits": 4,
-                   "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1),
+            rec = {"name": f"{name}_{kind}", "group": "prologue", "kind": f"prologue_{kind}", "M": M, "K": K, "b": b,
+                   "bits": 4, "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1),
                    "bound": "hbm" if t_hbm >= t_alu else "alu", "roofline_frac": round(max(t_hbm, t_alu) / us, 4)}
             log_fn(json.dumps(rec))
             out.append(rec)
             del g
         del x, perm, blocks, codes, delta, ws
         torch.cuda.empty_cache()
-    # the butterfly prologue at every block size of the down-projection sweep (M = 816,
-    # K = 16384, Student-t rows): log2 b stages, the last log2(b / 16) across lanes
     M, K = 816, 16384
     for b in (32, 64, 128, 256):
         x = synth.down_proj_sweep_point(M, b, 4).site_activation("D", 0).to(dev)
@@ -518,9 +651,9 @@ def measure_prologue_points(torch, fq, synth, dev, log_fn):
         reps = 20
         g = graph_of(torch, call, reps)
         us = time_graph(torch, g, 4) / reps * 1e6
-        nbytes = M * (2 * K + K // 2 + 4)
-        rec = {"name": f"sweep_prologue_m816_b{b}_fwht", "kind": "prologue_fwht", "M": M, "K": K, "b": b, "bits": 4,
-               "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1), "bound": "hbm",
+        nbytes = quant_bytes(M, K, 4)
+        rec = {"name": f"sweep_prologue_m816_b{b}_fwht", "group": "prologue", "kind": "prologue_fwht", "M": M,
+               "K": K, "b": b, "bits": 4, "us": round(us, 3), "GBps": round(nbytes / us / 1e3, 1), "bound": "hbm",
                "roofline_frac": round(nbytes / HBM_PEAK_GBS / 1e3 / us, 4)}
         log_fn(json.dumps(rec))
         out.append(rec)
@@ -529,99 +662,250 @@ def measure_prologue_points(torch, fq, synth, dev, log_fn):
     return out
 
 
-def measure_mixed_chain(torch, fq, synth, dev, log_fn, layers=18):
-    """Selective-INT8 language backbone: `layers` layers of the width-2048 shapes at
-    M = 816 (q|k|v 2048 -> 2560 and gate|up 2048 -> 32768 W4A4; o 2048 -> 2048 and down
-    16384 -> 2048 W8A8; b = 128).  Per layer: a = RMSNorm(h) (eps 1e-6), q|k|v = Lin_A(a)
-    with the norm's gain folded into the weights; o = Lin_O(q), q standing in for the
-    attention output; h1 = h + o; g|u = Lin_B(RMSNorm(h1)), gain folded; d =
-    Lin_D(silu(g) * u); h = h1 + d.  Norms, SwiGLU and residuals run in fp32 torch (outside
-    the projection).  Weights N(0, 0.02) drawn on the device (torch generator seeded
-    4000 + layer), gains U(0.5, 1.5); h0 = the backbone's seeded activations.  Times the
-    whole quantized chain and its 4 fused projections per layer (HIP graphs) and reports
-    the cosine of the final hidden state against the same chain in fp32 with the
-    unquantized weights and explicit gains."""
-    M, D, KV, F, b = 816, 2048, 256, 16384, 128
-    shapes = {"A": (D + 2 * KV, D, 4), "O": (D, D, 8), "B": (2 * F, D, 4), "D": (D, F, 8)}
+# --------------------------------------------------------------------------- the 18-layer chain
 
-    def layer_weights(l):
-        g = torch.Generator(device=dev)
-        g.manual_seed(4000 + l)
-        w = {s_: torch.randn((n, k), generator=g, device=dev, dtype=torch.float32) * 0.02
-             for s_, (n, k, _) in shapes.items()}
-        gain = {s_: torch.rand((D,), generator=g, device=dev, dtype=torch.float32) + 0.5 for s_ in ("A", "B")}
+class MixedChain:
+    """Selective-INT8 language backbone: layers of the width-2048 shapes at M = 816
+    (q|k|v 2048 -> 2560 and gate|up 2048 -> 32768 W4A4; o 2048 -> 2048 and down
+    16384 -> 2048 W8A8).  Per layer: a = RMSNorm(h) (eps 1e-6; its gain gamma_A ~ U(0.5,
+    1.5) folded into W_q,k,v by eq. (4)); q|k|v = Lin_A(a); o = Lin_O(q), q standing in for
+    the attention output; h1 = h + o; g|u = Lin_B(RMSNorm(h1)) (gain gamma_B folded);
+    d = Lin_D(silu(g) * u); h = h1 + d.  Norms, SwiGLU and residuals run in fp32 torch
+    (outside the projection); each projection's input is rounded to bf16.  Weights are the
+    seeded backbone-layer weights of layer l (synth.backbone_layer_mixed(l)), gains
+    synth.channel_vector(seed 7000 + 2 l for A, 7001 + 2 l for B); h0 = layer 0's seeded
+    site-A activations.  Layers are added one at a time (add_layer), so that a caller can
+    share one layer's host weights between chains and checks; layer(l, record) runs layer l
+    on the current hidden state and can keep every projection's bf16 input and output."""
+
+    M, D, KV, F = 816, 2048, 256, 16384
+    SHAPES = {"A": (2048 + 2 * 256, 2048, 4), "O": (2048, 2048, 8), "B": (2 * 16384, 2048, 4), "D": (2048, 16384, 8)}
+    SITE_PROJ = {"A": ("q", "k", "v"), "O": ("o",), "B": ("gate", "up"), "D": ("down",)}
+
+    def __init__(self, torch, fq, synth, dev, b=128, keep_fp32=False):
+        self.torch, self.fq, self.synth, self.dev, self.b, self.keep_fp32 = torch, fq, synth, dev, b, keep_fp32
+        self.lins, self.w32, self.gains = [], [], []
+        M, D, F = self.M, self.D, self.F
+        self.ws = fq.workspace(max(fq.linear_workspace_bytes(M, n, k, bits) for n, k, bits in self.SHAPES.values()), dev)
+        self.h0 = synth.backbone_layer_mixed(0).site_activation("A", 0).to(dev).float()
+        self.h = self.h0.clone()
+        bf = dict(dtype=torch.bfloat16, device=dev)
+        self.a_in = torch.empty((M, D), **bf)
+        self.qkv = torch.empty((M, D + 2 * self.KV), **bf)
+        self.o = torch.empty((M, D), **bf)
+        self.b_in = torch.empty((M, D), **bf)
+        self.gu = torch.empty((M, 2 * F), **bf)
+        self.m_in = torch.empty((M, F), **bf)
+        self.dn = torch.empty((M, D), **bf)
+
+    @classmethod
+    def layer_weights(cls, synth, l):
+        """Host fp32 weights of layer l per site (consumers of a site stacked) and its gains."""
+        wl = synth.backbone_layer_mixed(l)
+        w = {s: np.concatenate([wl.projection_weight(p) for p in wl.projections if p.name in names], axis=0)
+             for s, names in cls.SITE_PROJ.items()}
+        gain = {"A": synth.channel_vector(cls.D, seed=7000 + 2 * l, low=0.5, high=1.5),
+                "B": synth.channel_vector(cls.D, seed=7001 + 2 * l, low=0.5, high=1.5)}
         return w, gain
 
-    def rms(h):
-        return h * torch.rsqrt(torch.mean(h * h, dim=1, keepdim=True) + 1e-6)
+    def add_layer(self, w, gain):
+        torch, fq, dev = self.torch, self.fq, self.dev
+        self.gains.append(gain)
+        self.lins.append({s: fq.QuantLinear(torch.from_numpy(w[s]).to(dev), self.b, bits,
+                                            col_scale=torch.from_numpy(gain[s]).to(dev) if s in gain else None)
+                          for s, (_, _, bits) in self.SHAPES.items()})
+        if self.keep_fp32:
+            self.w32.append({s: torch.from_numpy(w[s]).to(dev) for s in self.SHAPES})
 
-    lins, ws_bytes = [], 0
+    def rms(self, h):
+        return h * self.torch.rsqrt(self.torch.mean(h * h, dim=1, keepdim=True) + 1e-6)
+
+    def layer(self, l, record=False):
+        torch, D, F, ws, L = self.torch, self.D, self.F, self.ws, self.lins[l]
+        self.a_in.copy_(self.rms(self.h))
+        L["A"](self.a_in, ws=ws, out=self.qkv)
+        L["O"](self.qkv[:, :D], ws=ws, out=self.o)
+        self.h.add_(self.o.float())
+        rec = {"A": (self.a_in.clone(), self.qkv.clone()), "O": (self.qkv[:, :D].contiguous(), self.o.clone())} \
+            if record else None
+        self.b_in.copy_(self.rms(self.h))
+        L["B"](self.b_in, ws=ws, out=self.gu)
+        self.m_in.copy_(torch.nn.functional.silu(self.gu[:, :F].float()) * self.gu[:, F:].float())
+        L["D"](self.m_in, ws=ws, out=self.dn)
+        self.h.add_(self.dn.float())
+        if record:
+            rec.update({"B": (self.b_in.clone(), self.gu.clone()), "D": (self.m_in.clone(), self.dn.clone())})
+        return rec
+
+    def forward(self, layers=None):
+        self.h.copy_(self.h0)
+        for l in range(len(self.lins) if layers is None else layers):
+            self.layer(l)
+
+    def projections(self):
+        ws, D = self.ws, self.D
+        for L in self.lins:
+            L["A"](self.a_in, ws=ws, out=self.qkv)
+            L["O"](self.qkv[:, :D], ws=ws, out=self.o)
+            L["B"](self.b_in, ws=ws, out=self.gu)
+            L["D"](self.m_in, ws=ws, out=self.dn)
+
+    def reference(self):
+        """The same chain in fp32 with the unquantized weights and explicit gains; the hidden
+        state after every layer."""
+        torch, D, F = self.torch, self.D, self.F
+        hr, hs = self.h0.clone(), []
+        for l, w in enumerate(self.w32):
+            gA = torch.from_numpy(self.gains[l]["A"]).to(self.dev)
+            gB = torch.from_numpy(self.gains[l]["B"]).to(self.dev)
+            qkv = (gA * self.rms(hr)) @ w["A"].t()
+            hr = hr + qkv[:, :D] @ w["O"].t()
+            gu = (gB * self.rms(hr)) @ w["B"].t()
+            hr = hr + (torch.nn.functional.silu(gu[:, :F]) * gu[:, F:]) @ w["D"].t()
+            hs.append(hr)
+        return hs
+
+
+def measure_mixed_chain(torch, fq, synth, dev, log_fn, layers=18):
+    """The 18-layer selective-INT8 chain (MixedChain) on the seeded weights the parity tests
+    check: at b = 128 the whole chain and its projections alone timed as HIP graphs; at
+    b = 128 and at b = 1 (no rotation: plain per-token and per-channel round-to-nearest) the
+    cosine of the hidden state against the fp32 chain after every layer, which shows the
+    rotation's effect."""
+    chains = {128: MixedChain(torch, fq, synth, dev, b=128, keep_fp32=True), 1: MixedChain(torch, fq, synth, dev, b=1)}
     for l in range(layers):
-        w, gain = layer_weights(l)
-        lins.append({s_: fq.QuantLinear(w[s_], b, bits, col_scale=gain.get(s_))
-                     for s_, (_, _, bits) in shapes.items()})
-        ws_bytes = max([ws_bytes] + [fq.linear_workspace_bytes(M, n, k, bits) for n, k, bits in shapes.values()])
-        del w, gain
-    ws = fq.workspace(ws_bytes, dev)
-    h0 = synth.backbone_layer_mixed(0).site_activation("A", 0).to(dev).float()
-    h = torch.empty_like(h0)
-    a_in = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
-    qkv = torch.empty((M, D + 2 * KV), dtype=torch.bfloat16, device=dev)
-    o = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
-    b_in = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
-    gu = torch.empty((M, 2 * F), dtype=torch.bfloat16, device=dev)
-    m_in = torch.empty((M, F), dtype=torch.bfloat16, device=dev)
-    dn = torch.empty((M, D), dtype=torch.bfloat16, device=dev)
-
-    def forward(i):
-        h.copy_(h0)
-        for L in lins:
-            a_in.copy_(rms(h))
-            L["A"](a_in, ws=ws, out=qkv)
-            L["O"](qkv[:, :D], ws=ws, out=o)
-            h.add_(o.float())
-            b_in.copy_(rms(h))
-            L["B"](b_in, ws=ws, out=gu)
-            m_in.copy_(torch.nn.functional.silu(gu[:, :F].float()) * gu[:, F:].float())
-            L["D"](m_in, ws=ws, out=dn)
-            h.add_(dn.float())
-
-    def projections(i):
-        for L in lins:
-            L["A"](a_in, ws=ws, out=qkv)
-            L["O"](qkv[:, :D], ws=ws, out=o)
-            L["B"](b_in, ws=ws, out=gu)
-            L["D"](m_in, ws=ws, out=dn)
-
-    g_chain = graph_of(torch, forward, 1)
-    us_chain = time_graph(torch, g_chain, 5) * 1e6
-    g_chain.replay()
-    torch.cuda.synchronize()
-    h_q = h.clone()
-    g_proj = graph_of(torch, projections, 1)
-    us_proj = time_graph(torch, g_proj, 5) * 1e6
-    del g_chain, g_proj
-
-    # fp32 reference chain (unquantized weights, gains applied to the activations)
-    hr = h0.clone()
-    for l in range(layers):
-        w, gain = layer_weights(l)
-        qkv_r = (gain["A"] * rms(hr)) @ w["A"].t()
-        hr = hr + qkv_r[:, :D] @ w["O"].t()
-        gu_r = (gain["B"] * rms(hr)) @ w["B"].t()
-        hr = hr + (torch.nn.functional.silu(gu_r[:, :F]) * gu_r[:, F:]) @ w["D"].t()
-        del w, gain
-    cos = torch.nn.functional.cosine_similarity(h_q.flatten(), hr.flatten(), dim=0).item()
-    ops = layers * 2.0 * M * sum(n * k for n, k, _ in shapes.values())
-    rec = {"name": f"mixed_chain_{layers}l_m{M}", "kind": "chain", "layers": layers, "M": M, "b": b,
-           "us_total": round(us_chain, 1), "us_per_layer": round(us_chain / layers, 2),
-           "projections_us_per_layer": round(us_proj / layers, 2),
-           "projection_TOPS": round(ops / us_proj / 1e6, 1), "cosine_vs_fp32": round(cos, 6)}
-    log_fn(json.dumps(rec))
-    del lins, ws
+        w, gain = MixedChain.layer_weights(synth, l)
+        for ch in chains.values():
+            ch.add_layer(w, gain)
+        del w
+    chains[1].w32 = chains[128].w32
+    hr = chains[128].reference()
+    recs = []
+    for b, ch in chains.items():
+        rec = {"name": f"mixed_chain_{layers}l_m{ch.M}_b{b}", "group": "chain", "kind": "chain", "layers": layers,
+               "M": ch.M, "b": b}
+        if b == 128:
+            g_chain = graph_of(torch, lambda i: ch.forward(), 1)
+            us_chain = time_graph(torch, g_chain, 5) * 1e6
+            del g_chain
+            g_proj = graph_of(torch, lambda i: ch.projections(), 1)
+            us_proj = time_graph(torch, g_proj, 5) * 1e6
+            del g_proj
+            ops = layers * 2.0 * ch.M * sum(n * k for n, k, _ in MixedChain.SHAPES.values())
+            rec.update({"us_total": round(us_chain, 1), "us_per_layer": round(us_chain / layers, 2),
+                        "projections_us_per_layer": round(us_proj / layers, 2),
+                        "projection_TOPS": round(ops / us_proj / 1e6, 1)})
+        cos = []
+        ch.h.copy_(ch.h0)
+        for l in range(layers):
+            ch.layer(l)
+            cos.append(round(torch.nn.functional.cosine_similarity(ch.h.flatten(), hr[l].flatten(), dim=0).item(), 6))
+        rec["cosine_vs_fp32"] = cos[-1]
+        rec["cosine_vs_fp32_per_layer"] = cos
+        log_fn(json.dumps(rec))
+        recs.append(rec)
+    del chains, hr
     torch.cuda.empty_cache()
-    return [rec]
+    return recs
 
+
+# --------------------------------------------------------------------------- CPU baseline
+
+def host_cpu_info():
+    info = {"nproc": os.cpu_count(), "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
+    try:
+        import subprocess
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=20).stdout
+        for line in out.splitlines():
+            k, _, v = line.partition(":")
+            k, v = k.strip(), v.strip()
+            if k in ("Model name", "Socket(s)", "Core(s) per socket", "Thread(s) per core", "CPU(s)"):
+                info[k] = v
+    except (OSError, ValueError):  # lscpu is optional
+        pass
+    return info
+
+
+def cpu_baseline(st, oracle, synth, budget_s=12.0):
+    """The oracle on the host cores: whole denoising steps of the action-expert layer (4 site
+    prologues + the 7 consumers' contractions and rescales) with all threads for about
+    budget_s seconds; then one denoising step and the single linear (M 64, 1024 -> 1024)
+    with one thread and with all threads."""
+    wq = {s: oracle.quantize_weights(st.w_host[s], st.b, 4) for s in st.sites}
+    xs = {s: [a.cpu() for a in st.x[s]] for s in st.sites}
+
+    def step(t):
+        for s in st.sites:
+            codes, delta = oracle.fwht_quant(xs[s][t], st.b, 4)
+            wc, s_w = wq[s]
+            oracle.dequant(oracle.gemm(codes, wc), delta, s_w)
+
+    wl = synth.single_linear()
+    p = wl.projections[0]
+    x1 = synth.activations(wl.M, p.K, seed=0, outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale)
+    wc1, s_w1 = oracle.quantize_weights(wl.projection_weight(p), wl.b, 4)
+
+    def single():
+        t0 = time.perf_counter()
+        oracle.linear(x1, wc1, s_w1, wl.b, 4)
+        return (time.perf_counter() - t0) * 1e6
+
+    threads = oracle.max_threads()
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        step(steps % st.n_steps)
+        steps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or steps >= 1000:
+            break
+    ops = st.wl.ops_per_step() * steps
+    rec = {"value": ops / el / 1e12, "unit": "TOPS", "cores": threads, "kind": "oracle",
+           "sample": f"{steps} denoising steps of the action-expert layer (M=50, 7 projections) in {el:.1f} s "
+                     f"on {threads} threads; then one step and the single linear on 1 thread",
+           "us_per_step": round(el / steps * 1e6, 1), "us_single_linear": round(single(), 1)}
+    oracle.set_threads(1)
+    try:
+        t0 = time.perf_counter()
+        step(0)
+        rec["single_thread_us_per_step"] = round((time.perf_counter() - t0) * 1e6, 1)
+        rec["single_thread_us_single_linear"] = round(single(), 1)
+    finally:
+        oracle.set_threads(threads)
+    rec["host"] = host_cpu_info()
+    return rec
+
+
+# --------------------------------------------------------------------------- counter helpers
+
+def traffic_run(torch, fq, synth, dev, site):
+    st = ExpertStep(torch, fq, synth, dev)
+    for i in range(100):
+        st.run_site(site, i % st.n_steps)
+    torch.cuda.synchronize()
+    print(json.dumps({"traffic_site": site, "calls": 100}), flush=True)
+
+
+def counter_point_run(torch, fq, synth, dev, name):
+    spec = next(s for s in point_specs() if s[1] == name)
+    pt = Point(torch, fq, synth, dev, spec)
+    n = max(pt.calls(), 20)
+    for i in range(n):
+        pt.call(i)
+    torch.cuda.synchronize()
+    print(json.dumps({"counter_point": name, "calls": n}), flush=True)
+
+
+def copy_calibration(torch, dev):
+    n = 64 << 20  # float32 elements: 256 MiB read and 256 MiB written per launch
+    a = torch.ones(n, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(20):
+        torch.add(a, 0.0, out=b)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "launches": 20}), flush=True)
+
+
+# --------------------------------------------------------------------------- main
 
 def main():
     args = parse()
@@ -630,32 +914,37 @@ def main():
               "(the projection's multi-GPU sharding is a design note, not a measured path).",
               file=sys.stderr)
         sys.exit(2)
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.manifest)
+        return
     import torch
 
     from paper_2609_24433_amd import fq, synth
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     K_steps, W = args.steps, args.warmup
+    groups = args.points.split(",") if args.points else None
 
     if args.copy_calibration:
         copy_calibration(torch, dev)
         return
-    if args.gemm_counters:
-        gemm_counter_run(torch, fq, synth, dev)
-        return
     if args.traffic_site:
         traffic_run(torch, fq, synth, dev, args.traffic_site)
         return
-    if args.only_points:
-        print(json.dumps({"points": measure_points(torch, fq, synth, dev, lambda m: log(args, m))}), flush=True)
+    if args.counter_point:
+        counter_point_run(torch, fq, synth, dev, args.counter_point)
         return
+    if args.rocprof_points:
+        rocprof_points_run(torch, fq, synth, dev, groups)
+        return
+
     st = ExpertStep(torch, fq, synth, dev)
     import oracle  # the parity check and the CPU baseline only
     check_step(st, oracle, torch)
     log(args, "parity check ok")
 
-    # the denoising loop (10 steps) captured as one graph, as a serving loop runs it;
-    # one graph per step covers a remainder of K, and is also timed on its own
+    # the denoising loop (10 steps) captured as one graph, as a serving loop runs it (the
+    # weights shared across steps stay resident); one graph per step covers a remainder of K
     graphs = [graph_of(torch, lambda i, t=t: st.run(t), 1) for t in range(st.n_steps)]
     loop = graph_of(torch, lambda i: st.run(i), st.n_steps)
     elapsed = time_graph_steps(torch, graphs, K_steps, W, loop=loop)
@@ -663,29 +952,62 @@ def main():
     value = ops_step * K_steps / elapsed / 1e12
     ms_step = elapsed * 1e3 / K_steps
     per_step_graphs = time_graph_steps(torch, graphs, K_steps, W) * 1e6 / K_steps
+    del graphs, loop
     log(args, f"loop graph replay: {ms_step * 1e3:.2f} us/step, {value:.3f} TOPS; "
               f"one graph per step: {per_step_graphs:.2f} us/step")
 
-    # per-site fused projection duration: a graph of 50 back-to-back calls per site
-    # (weights resident, as across the denoising steps), HIP events around the replays
+    # the step with cold weights: every step on its own copy of the packed weights (>= 1 GiB
+    # in rotation)
+    cold = ExpertStep(torch, fq, synth, dev, copies=int(max(2, min(160, COLD_BYTES // st.weight_bytes() + 1))))
+    us_cold, p10c, p90c, _ = time_calls(torch, lambda i: cold.run(i % cold.n_steps, i), cold.copies)
+    del cold
+    torch.cuda.empty_cache()
+    log(args, f"cold step: {us_cold:.2f} us")
+
+    # each site's fused projection, resident and cold weights; a site on the two-kernel path
+    # (K too long for the one-kernel projection) also has its GEMM timed alone, cold
     M = st.wl.M
+    traced = rocprof_points()
     per_site = {}
     for s_, K in st.sites.items():
-        g = graph_of(torch, lambda i, s_=s_: st.run_site(s_, i % st.n_steps), 50)
-        per_site[s_] = time_graph(torch, g, 4) / 50 * 1e6
-    log(args, "per-site fused projection us: " + ", ".join(f"{k}={v:.2f}" for k, v in per_site.items()))
-    # the dominant kernel: the longest single launch of the step, a site's GEMM (each
-    # site's GEMM timed alone as a graph of 50 back-to-back launches, weights resident)
-    gemm_site = {}
-    for s_ in st.sites:
-        g = graph_of(torch, st.gemm_call(s_), 50)
-        gemm_site[s_] = time_graph(torch, g, 4) / 50 * 1e6
-    dom = max(gemm_site, key=lambda k: gemm_site[k])
-    Kd, Nd = st.sites[dom], st.site_N[dom]
-    dom_bytes = gemm_bytes(M, Nd, Kd, 4)
-    ach = dom_bytes / gemm_site[dom] / 1e3  # GB/s
-    lin_bytes = linear_bytes(M, Nd, Kd, 4)
-    log(args, "per-site GEMM kernel us: " + ", ".join(f"{k}={v:.2f}" for k, v in gemm_site.items()))
+        N = st.site_N[s_]
+        r = {"K": K, "N": N, "one_kernel": fq.linear_workspace_bytes(M, N, K, 4) == 0}
+        r["warm_us"] = round(time_calls(torch, lambda i, s_=s_: st.run_site(s_, i), 50)[0], 3)
+        kinds = ("linear",) if r["one_kernel"] else ("linear", "gemm")
+        for kind in kinds:
+            name = f"expert_site{s_}_m50_cold" if kind == "linear" else f"expert_site{s_}_m50_gemm_cold"
+            pt = Point(torch, fq, synth, dev, ("expert_sites", name, M, K, N, st.b, 4, kind, "cold"))
+            r["cold_us" if kind == "linear" else "gemm_cold_us"] = round(time_calls(torch, pt.call, pt.calls())[0], 3)
+            del pt
+        per_site[s_] = r
+        torch.cuda.empty_cache()
+    log(args, "per-site: " + json.dumps(per_site))
+
+    # the dominant kernel: the step's longest single launch, cold weights
+    def launch(s_):
+        r = per_site[s_]
+        return (r["cold_us"], "linear") if r["one_kernel"] else (r["gemm_cold_us"], "gemm")
+
+    dom = max(per_site, key=lambda k: launch(k)[0])
+    r = per_site[dom]
+    Kd, Nd = r["K"], r["N"]
+    dom_us, dom_kind = launch(dom)
+    if dom_kind == "linear":
+        dom_kernel, dom_bytes, tname = "linear_small_kernel (the one-kernel projection)", linear_bytes(M, Nd, Kd, 4), \
+            f"expert_site{dom}_m50_cold"
+    else:
+        dom_kernel, dom_bytes, tname = "the site's GEMM", gemm_bytes(M, Nd, Kd, 4), f"expert_site{dom}_m50_gemm_cold"
+    ach = dom_bytes / dom_us / 1e3
+    roof = {"bound": "hbm", "kernel": f"{dom_kernel}, site {dom}, M={M} K={Kd} N={Nd}, the step's longest launch",
+            "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic(dom, dom_kind), "kernel_us": round(dom_us, 3),
+            "weights": "cold: rotating copies of >= 1 GiB, graph of back-to-back calls, HIP events",
+            "algorithmic_bytes": dom_bytes,
+            "resident_weights_us": r["warm_us"] if dom_kind == "linear" else None}
+    tr = traced.get(tname)
+    if tr:
+        roof["rocprof_us"] = tr["us_per_call"]
+        roof["rocprof_frac"] = round(dom_bytes / tr["us_per_call"] / 1e3 / HBM_PEAK_GBS, 4)
 
     rec = {
         "metric": "W4A4 fused-linear TOPS and us/projection at M=50 and M=816; % of roofline",
@@ -697,27 +1019,32 @@ def main():
                                "q/k/v/o/gate/up/down W4A4, block 128, 10 steps of fresh activations; "
                                "one fused projection per activation site (q|k|v and gate|up grouped)",
                    "M": M, "b": st.wl.b, "projections": 7, "sites": 4,
-                   "graph": f"the {st.n_steps}-step denoising loop as one HIP graph",
+                   "graph": f"the {st.n_steps}-step denoising loop as one HIP graph, weights shared across steps",
                    "us_per_step_one_graph_per_step": round(per_step_graphs, 3),
+                   "us_per_step_cold_weights": round(us_cold, 3),
+                   "us_per_step_cold_p10_p90": [round(p10c, 3), round(p90c, 3)],
                    "us_per_projection": round(ms_step * 1e3 / 7, 3),
-                   "us_per_site": {k: round(v, 3) for k, v in per_site.items()},
-                   "gemm_us_per_site": {k: round(v, 3) for k, v in gemm_site.items()}},
-        "roofline": {"bound": "hbm", "kernel": f"gemm_stream_kernel, site {dom} GEMM, M={M} K={Kd} N={Nd} "
-                                               f"(the step's longest launch)",
-                     "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(dom, "gemm"),
-                     "kernel_us": round(gemm_site[dom], 3), "algorithmic_bytes": dom_bytes,
-                     "fused_projection": {"site": dom, "us": round(per_site[dom], 3),
-                                          "algorithmic_bytes": lin_bytes,
-                                          "achieved": round(lin_bytes / per_site[dom] / 1e3, 1),
-                                          "frac": round(lin_bytes / per_site[dom] / 1e3 / HBM_PEAK_GBS, 4),
-                                          "traffic": measured_traffic(dom, "linear")}},
+                   "site_us": per_site},
+        "roofline": roof,
     }
     if not args.no_points:
-        rec["points"] = measure_points(torch, fq, synth, dev, lambda m: log(args, m))
+        pts, graded = [], []
+        for spec in point_specs(groups):
+            p = measure_point(torch, fq, synth, dev, spec, traced)
+            log(args, json.dumps(p))
+            (graded if spec[0] == "graded" else pts).append(p)
+        if groups is None or "prologue" in groups:
+            pts += measure_prologue_points(torch, fq, synth, dev, lambda m: log(args, m))
+        if groups is None or "gptq" in groups:
+            pts += measure_gptq_points(torch, fq, synth, dev, lambda m: log(args, m))
+        if groups is None or "context" in groups:
+            pts += measure_bf16_context(torch, synth, dev, lambda m: log(args, m), graded + pts)
+        if groups is None or "chain" in groups:
+            pts += measure_mixed_chain(torch, fq, synth, dev, lambda m: log(args, m))
+        rec["graded"] = graded
+        rec["points"] = pts
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(st, oracle, torch)
+        rec["cpu_baseline"] = cpu_baseline(st, oracle, synth)
     print(json.dumps(rec), flush=True)
 
 
