@@ -249,6 +249,8 @@ __global__ __launch_bounds__(kSmallThreads) void linear_small_kernel(SmallParams
   lds_barrier();  // the codes and the scales are in LDS
 
   // ---- GEMM over the whole of K ---------------------------------------------------------------
+  // Steps past this K take zero activation operands (they add nothing), so that the MFMA
+  // loop runs straight through.
   const int rr = cl & (R - 1);  // MFMA row -> a valid row of the block
   const uint8_t *arow = al + rr * K;
   v4i ar[KT][2];
@@ -256,7 +258,8 @@ __global__ __launch_bounds__(kSmallThreads) void linear_small_kernel(SmallParams
   for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
     for (int c = 0; c < 2; ++c)
-      ar[kt][c] = *reinterpret_cast<const v4i *>(arow + code_unit(rr, min(kt, ktot - 1) * 8 + 2 * g + c) * 16);
+      ar[kt][c] = kt < ktot ? *reinterpret_cast<const v4i *>(arow + code_unit(rr, kt * 8 + 2 * g + c) * 16)
+                            : v4i{0, 0, 0, 0};
   v4i acc[2][NCW];
 #pragma unroll
   for (int h = 0; h < 2; ++h)
@@ -264,35 +267,39 @@ __global__ __launch_bounds__(kSmallThreads) void linear_small_kernel(SmallParams
     for (int i = 0; i < NCW; ++i) acc[h][i] = v4i{0, 0, 0, 0};
 #pragma unroll
   for (int kt = 0; kt < KT; ++kt) {
-    if (kt < ktot) {
 #pragma unroll
-      for (int i = 0; i < NCW; ++i) {
-        v4i b0, b1;
-        if constexpr (BITS == 4) {
-          b0 = widen8(v2i{(int)wr[i][kt][0].x, (int)wr[i][kt][0].y});
-          b1 = widen8(v2i{(int)wr[i][kt][0].z, (int)wr[i][kt][0].w});
-        } else {
-          b0 = __builtin_bit_cast(v4i, wr[i][kt][0]);
-          b1 = __builtin_bit_cast(v4i, wr[i][kt][1]);
-        }
-        acc[kt & 1][i] = mfma16x16x64(ar[kt][0], b0, acc[kt & 1][i]);
-        acc[kt & 1][i] = mfma16x16x64(ar[kt][1], b1, acc[kt & 1][i]);
+    for (int i = 0; i < NCW; ++i) {
+      v4i b0, b1;
+      if constexpr (BITS == 4) {
+        b0 = widen8(v2i{(int)wr[i][kt][0].x, (int)wr[i][kt][0].y});
+        b1 = widen8(v2i{(int)wr[i][kt][0].z, (int)wr[i][kt][0].w});
+      } else {
+        b0 = __builtin_bit_cast(v4i, wr[i][kt][0]);
+        b1 = __builtin_bit_cast(v4i, wr[i][kt][1]);
       }
+      acc[kt & 1][i] = mfma16x16x64(ar[kt][0], b0, acc[kt & 1][i]);
+      acc[kt & 1][i] = mfma16x16x64(ar[kt][1], b1, acc[kt & 1][i]);
     }
   }
 
   // ---- rescale and store straight from the MFMA layout ----------------------------------------
+  // lane (g, cl) holds rows 4 g + e of column cl; the deltas of rows 4 g .. 4 g + 3 in one
+  // read (rows past R read the spare words after the deltas and are never stored)
+  const float4 d4 = *reinterpret_cast<const float4 *>(dl + 4 * g);
+  const float dr[4] = {d4.x, d4.y, d4.z, d4.w};
+  const int rows_here = min(R, p.M - m0) - 4 * g;  // valid rows from 4 g on
+  uint16_t *yrow = p.y + (int64_t)(m0 + 4 * g) * p.ldy;
 #pragma unroll
   for (int i = 0; i < NCW; ++i) {
     const v4i tsum = acc[0][i] + acc[1][i];
     const int n = (nt0 + wave + S::NW * i) * 16 + cl;
+    if (n < p.N) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int row = 4 * g + e, mm = m0 + row;
-      if (row < R && mm < p.M && n < p.N) {
-        const float val = (float)(tsum[e] >> S::SHIFT) * (sw[i] * dl[row]) + bj[i];
-        p.y[(int64_t)mm * p.ldy + n] = (uint16_t)f32_to_bf16(val);
-      }
+      for (int e = 0; e < 4; ++e)
+        if (e < rows_here) {
+          const float val = (float)(tsum[e] >> S::SHIFT) * (sw[i] * dr[e]) + bj[i];
+          yrow[(int64_t)e * p.ldy + n] = (uint16_t)f32_to_bf16(val);
+        }
     }
   }
 }
