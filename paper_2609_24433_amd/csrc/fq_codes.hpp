@@ -132,15 +132,69 @@ __device__ __forceinline__ void chunk_stage(float (&v)[CW]) {
 }
 
 // Butterfly stage h = CW M across lanes: chunk j pairs with chunk j ^ M, held by lane ^ M.
-// The lower chunk keeps a + c, the upper one a - c, as fma(+-1, own, partner): one
-// rounding of the exact sum or difference, the same as the add or subtract.
+// Each lane computes own + s * partner with s = -1 on the upper lane, as one fma (the exact
+// sum or difference, rounded once): the lower lane gets a + c, the upper one c - a, the
+// negation of a - c (round to nearest even is symmetric, so bit for bit -(a - c)).  Both
+// partners carry the same sign (it depends only on the chunk index bits below M), so every
+// later stage stays the same pair update up to that sign; row_sign() gives the sign a lane
+// carries after the whole transform.  In this form the partner is a multiplicand, which lets
+// the compiler fold a DPP lane move into the multiply-add.
+// own + s * partner for every value of a chunk, the partner read through a DPP lane move
+// folded into v_fmac_f32 (one instruction per value).  The leading s_nop covers the DPP
+// read-after-write wait states for values written just before the block; inside the block
+// every instruction reads and writes its own register.
+#define FQ_FMAC(i, CTL) "v_fmac_f32_dpp %" #i ", %" #i ", %[s] " CTL "\n\t"
+#define FQ_FMAC8(CTL)                                                                             \
+  FQ_FMAC(0, CTL) FQ_FMAC(1, CTL) FQ_FMAC(2, CTL) FQ_FMAC(3, CTL) FQ_FMAC(4, CTL) FQ_FMAC(5, CTL) \
+  FQ_FMAC(6, CTL) FQ_FMAC(7, CTL)
+#define FQ_FMAC16(CTL)                                                                              \
+  FQ_FMAC8(CTL) FQ_FMAC(8, CTL) FQ_FMAC(9, CTL) FQ_FMAC(10, CTL) FQ_FMAC(11, CTL) FQ_FMAC(12, CTL) \
+  FQ_FMAC(13, CTL) FQ_FMAC(14, CTL) FQ_FMAC(15, CTL)
+#define FQ_DPP_FMAC_CHUNK(NAME, CTL)                                                               \
+  __device__ __forceinline__ void NAME(float (&v)[16], float s) {                                 \
+    asm("s_nop 4\n\t" FQ_FMAC16(CTL)                                                             \
+        : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),      \
+          "+v"(v[7]), "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]), "+v"(v[12]), "+v"(v[13]),   \
+          "+v"(v[14]), "+v"(v[15])                                                                \
+        : [s] "v"(s));                                                                            \
+  }                                                                                               \
+  __device__ __forceinline__ void NAME(float (&v)[8], float s) {                                  \
+    asm("s_nop 4\n\t" FQ_FMAC8(CTL)                                                              \
+        : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),      \
+          "+v"(v[7])                                                                              \
+        : [s] "v"(s));                                                                            \
+  }
+FQ_DPP_FMAC_CHUNK(fmac_xor1, "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf")
+FQ_DPP_FMAC_CHUNK(fmac_xor2, "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf")
+FQ_DPP_FMAC_CHUNK(fmac_xor8, "row_ror:8 row_mask:0xf bank_mask:0xf")
+#undef FQ_DPP_FMAC_CHUNK
+#undef FQ_FMAC16
+#undef FQ_FMAC8
+#undef FQ_FMAC
+
 template <int M, int CPT, int CW = 16>
 __device__ __forceinline__ void lane_stage(float (&v)[CPT][CW], int tau) {
-  const float sgn = (tau & M) ? -1.0f : 1.0f;
+  const float s = (tau & M) ? -1.0f : 1.0f;
 #pragma unroll
-  for (int c = 0; c < CPT; ++c)
+  for (int c = 0; c < CPT; ++c) {
+    if constexpr (M == 1) fmac_xor1(v[c], s);
+    else if constexpr (M == 2) fmac_xor2(v[c], s);
+    else if constexpr (M == 8) fmac_xor8(v[c], s);
+    else {
 #pragma unroll
-    for (int i = 0; i < CW; ++i) v[c][i] = __builtin_fmaf(sgn, v[c][i], lane_xor<M>(v[c][i]));
+      for (int i = 0; i < CW; ++i) v[c][i] = __builtin_fmaf(lane_xor<M>(v[c][i]), s, v[c][i]);
+    }
+  }
+}
+
+// Sign of the values lane tau holds after row_transform(log2b): -1 when an odd number of
+// its lane stages left it on the upper side.  |value| and value * (sign * inv) are those of
+// the true transform exactly.
+template <int CW = 16>
+__device__ __forceinline__ float row_sign(int log2b, int tau) {
+  constexpr int L = CW == 16 ? 4 : 3;  // stages inside a chunk
+  const int lanes = log2b > L ? (1 << (log2b - L)) - 1 : 0;
+  return (__builtin_popcount(tau & lanes) & 1) ? -1.0f : 1.0f;
 }
 
 // The blockwise unnormalized Sylvester transform of a row held as CW-channel chunks

@@ -9,7 +9,8 @@
 //   stages h = 1..8: the optional per-channel multiplier, then the butterfly inside each
 //           chunk, in registers;
 //   stages h = 16..b/2: lane exchanges (a b-block spans b/16 <= 16 lanes of one wave),
-//           no LDS;
+//           no LDS; an upper lane keeps the negated difference (lane_stage), undone by the
+//           sign it multiplies into 1 / (r A);
 //   the row absmax is reduced over the row's lanes (DPP / swizzle) and waves (LDS), and
 //   each thread quantizes, packs and stores its chunks in natural channel order.
 // Every stage is the pair update (a, c) -> (a + c, a - c) in fp32 in ascending h, so the
@@ -165,6 +166,10 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   const float rA = p.clip_ratio * amax;
   const float inv = zero ? 0.0f : qf / rA;
   if (row_ok && tau == 0) p.delta[row] = zero ? 0.0f : (rA * p.cb) / qf;
+  // the lane stages leave this lane's values multiplied by sgn (lane_stage); sgn * inv
+  // gives the same products as inv on the true values
+  const float sgn = B >= 32 ? ((__builtin_popcount(tau & (B / 16 - 1)) & 1) ? -1.0f : 1.0f) : 1.0f;
+  const float inv_l = inv * sgn;
 
   // ---- quantize and pack in natural channel order ------------------------------------
   if (row_ok) {
@@ -176,7 +181,7 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
       if (j < nchunks) {
         int cc[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) cc[i] = quantize_bits(v1[c][i], inv, lim);
+        for (int i = 0; i < 16; ++i) cc[i] = quantize_bits(v1[c][i], inv_l, lim);
         store_chunk_bits(row_out, j, cc, p.out_fmt);
       }
     }

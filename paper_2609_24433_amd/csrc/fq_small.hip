@@ -203,7 +203,7 @@ __global__ __launch_bounds__(kSmallThreads) void linear_small_kernel(SmallParams
     const float qf = (float)q;
     const bool zero = !(amax > 0.0f);
     const float rA = p.clip_ratio * amax;
-    const float inv = zero ? 0.0f : qf / rA;
+    const float inv = (zero ? 0.0f : qf / rA) * row_sign<CW>(p.log2b, t);  // see lane_stage
     if (t == 0) dl[r] = zero ? 0.0f : (rA * p.cb) / qf;
     const float lim = qf + 0.49f;
     uint8_t *row_l = al + r * K;
