@@ -879,20 +879,29 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       pl.mt = 1;
       pl.rb = (int)((M + 15) / 16);
     }
-    // Long K with 33-64 rows (nibble codes): one 16-row tile per workgroup and 128 k steps
-    // per slice (the whole of K = 16384), 32 output channels per workgroup.  Each
-    // workgroup streams four times the weights of the 64-row plan (its sibling row blocks
-    // share them through the XCD's L2), but K needs no split: the split-K epilogue goes
-    // away.  Measured at M = 50, K 16384 -> N 2048: 11.1 against 11.7 us.
-    if (bits == 4 && M > 32 && ktot >= 128) {
-      pl.mt = 1;
-      pl.rb = (int)((M + 15) / 16);
-      pl.wk = 4;
-      pl.kt = 32;
-      pl.ksteps = 128;
-      pl.splits = (ktot + 127) / 128;
-      pl.wc = 2;
-      pl.tiles = (N + 31) / 32;
+    // Long K (nibble codes): one 16-row tile per workgroup and 128 k steps per slice (the
+    // whole of K = 16384), 16 output channels per workgroup for up to 32 rows, 32 for
+    // 33-64 rows.  Each row block streams the weights again (sibling row blocks share them
+    // through the XCD's L2), but K needs no split, so the split-K epilogue launch goes
+    // away.  Measured at M = 50, K 16384 -> N 2048: 11.1 against 11.7 us.  Up to 32 rows
+    // this needs a grid of >= 128 workgroups to keep the weight stream wide enough.
+    if (bits == 4 && ktot >= 128) {
+      const int rb = (int)((M + 15) / 16);
+      const int wc = rb <= 2 ? 1 : 2;
+      const int64_t tiles = (N + 16 * wc - 1) / (16 * wc);
+      const int splits = (ktot + 127) / 128;
+      if (M > 32 || tiles * rb * splits >= 128) {
+        // 8 wave groups of 16 steps with one wave column (as many waves as with two
+        // columns, and at most 32 loads in flight per wave)
+        pl.mt = 1;
+        pl.rb = rb;
+        pl.wk = wc == 1 ? 8 : 4;
+        pl.kt = wc == 1 ? 16 : 32;
+        pl.ksteps = 128;
+        pl.splits = splits;
+        pl.wc = wc;
+        pl.tiles = tiles;
+      }
     }
   } else {
     pl.kind = 1;
@@ -964,6 +973,12 @@ static hipError_t launch_stream_wc(const GemmParams &p, int kt, int wk, dim3 gri
         return hipErrorInvalidValue;
       default: return hipErrorInvalidValue;
     }
+  }
+  if (wk == 8) {
+    // one 16-row tile and one wave column over 128 k steps (nibble codes)
+    if constexpr (AFMT == kANibble && MT == 1 && WC == 1)
+      if (kt == 16) return launch_stream<BITS, AFMT, MT, 16, 8, WC>(p, grid, s, go);
+    return hipErrorInvalidValue;
   }
   if (wk == 1) {
     switch (kt) {
