@@ -442,32 +442,48 @@ def measure_point(torch, fq, synth, dev, spec, traced):
 
 
 def rocprof_points_run(torch, fq, synth, dev, groups):
-    """Every point's calls eagerly, as idle-separated segments of a kernel trace: for point i,
-    its set-up (weights and copies: at least one kernel), a pause, its calls (one per weight
-    copy; cold points rotate through >= 1 GiB of copies), a pause.  The manifest printed at
-    the end lists the points in order."""
+    """Every point as bench.py times it, for a kernel trace: for point i, its set-up (weights
+    and copies), the graph of its back-to-back calls (one per weight copy; cold points
+    rotate through >= 1 GiB of copies) replayed until >= 20 calls have run, then a sentinel
+    kernel (a uint8 bitwise_not that nothing else launches), replays of the graph until
+    >= 100 calls have run, a second sentinel.  The manifest printed at the end lists the
+    points in order with their calls between the sentinels."""
     manifest = []
+    s_in = torch.zeros(64, dtype=torch.uint8, device=dev)
+    s_out = torch.empty_like(s_in)
     for spec in point_specs(groups):
         pt = Point(torch, fq, synth, dev, spec)
+        calls = pt.calls()
+        g = graph_of(torch, pt.call, calls)
+        for _ in range(max(1, -(-20 // calls))):
+            g.replay()
+        reps = max(1, -(-100 // calls))
+        torch.bitwise_not(s_in, out=s_out)
+        for _ in range(reps):
+            g.replay()
+        torch.bitwise_not(s_in, out=s_out)
         torch.cuda.synchronize()
-        time.sleep(0.03)
-        n = max(pt.calls(), 20)
-        for i in range(n):
-            pt.call(i)
-        torch.cuda.synchronize()
-        time.sleep(0.03)
-        manifest.append({"name": spec[1], "calls": n})
-        print(json.dumps({"rocprof_point": spec[1], "calls": n}), flush=True)
-        del pt
+        manifest.append({"name": spec[1], "calls": calls * reps})
+        print(json.dumps({"rocprof_point": spec[1], "calls": calls * reps}), flush=True)
+        del g, pt
         torch.cuda.empty_cache()
     print(json.dumps({"rocprof_manifest": manifest}), flush=True)
 
 
-def summarize_trace(path, manifest_path):
+def trace_segments(rows, n_points):
+    """The kernels of each point in a `--rocprof-points` trace: rows (start, end, name, grid,
+    workgroup) sorted by start; the kernels strictly between sentinel 2 i and 2 i + 1 are
+    point i's calls."""
+    marks = [j for j, r in enumerate(rows) if "bitwise_not" in r[2]]
+    if len(marks) != 2 * n_points:
+        raise SystemExit(f"{len(marks)} sentinel kernels in the trace for {n_points} points")
+    return [rows[marks[2 * i] + 1:marks[2 * i + 1]] for i in range(n_points)]
+
+
+def summarize_trace(path, manifest_path, out_path=POINTS_TRACE_FILE):
     """Per-point, per-grid kernel summary of a `--rocprof-points` kernel trace (rocprofv3
-    CSV): the trace is split at idle gaps of >= 10 ms into segments; the last 2 P of them are
-    the P points' set-up and measured segments, alternating, matched in order to the run's
-    manifest (its last JSON line).  Writes profiles/points_kernels_by_grid.{json,md}."""
+    CSV), each point's calls found between its two sentinel kernels and matched in order to
+    the run's manifest (its last JSON line).  Writes profiles/points_kernels_by_grid.{json,md}."""
     import csv
     manifest = None
     with open(manifest_path) as f:
@@ -483,22 +499,11 @@ def summarize_trace(path, manifest_path):
             wg = tuple(int(r.get(f"Workgroup_Size_{a}") or 0) for a in "XYZ")
             rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]), r["Kernel_Name"], grid, wg))
     rows.sort()
-    segs, cur, last_end = [], [], -1
-    for r in rows:  # sorted by start; a gap is measured from the latest end so far
-        if cur and r[0] - last_end >= 10_000_000:
-            segs.append(cur)
-            cur = []
-        cur.append(r)
-        last_end = max(last_end, r[1])
-    segs.append(cur)
-    need = 2 * len(manifest)
-    if len(segs) < need:
-        raise SystemExit(f"{len(segs)} trace segments for {len(manifest)} points")
-    segs = segs[len(segs) - need:]
+    segs = trace_segments(rows, len(manifest))
     points = {}
     for i, m in enumerate(manifest):
         by = {}
-        for start, end, name, grid, wg in segs[2 * i + 1]:
+        for start, end, name, grid, wg in segs[i]:
             by.setdefault((name, grid, wg), []).append((end - start) / 1e3)
         kern = []
         for (name, grid, wg), d in sorted(by.items(), key=lambda kv: -sum(kv[1])):
@@ -509,7 +514,7 @@ def summarize_trace(path, manifest_path):
     out = {"sources_sha256": sources_digest(), "points": points,
            "note": "kernel execution time per call (the sum of the call's kernels, no launch gaps) from a "
                    "rocprofv3 kernel trace of `python bench.py --rocprof-points`"}
-    with open(POINTS_TRACE_FILE, "w") as f:
+    with open(out_path, "w") as f:
         json.dump(out, f, indent=1)
     lines = ["# Kernel time per point, by kernel and grid (rocprofv3 kernel trace)", "",
              "Commands (from the repository root on an MI355X, `cd /tmp && export TMPDIR=/tmp` first):", "",
@@ -518,8 +523,9 @@ def summarize_trace(path, manifest_path):
              "python /root/repo/bench.py --rocprof-points --quiet > <out>/manifest.txt",
              "python /root/repo/bench.py --summarize-trace <out>/<host>/points_kernel_trace.csv "
              "--manifest <out>/manifest.txt", "```", "",
-             "Each point ran its calls eagerly between idle gaps (one call per weight copy; cold points rotate "
-             "through >= 1 GiB of copies). `us/call` is the sum of the point's kernel durations divided by its "
+             "Each point replayed the graph of back-to-back calls that bench.py times (one call per weight copy; "
+             "cold points rotate through >= 1 GiB of copies), warmed up, then >= 100 calls between two sentinel "
+             "kernels. `us/call` is the sum of the point's kernel durations divided by its "
              "calls (no launch gaps); bench.py reports it beside its own graph-replay figure as `rocprof_us`. "
              f"Sources SHA-256 {out['sources_sha256'][:16]}.", "",
              "| point | calls | us/call | kernel | grid | workgroup | launches | avg us | min | max |",
@@ -530,9 +536,9 @@ def summarize_trace(path, manifest_path):
             lines.append(f"{head} | `{k['kernel'][:100]}` | {'x'.join(map(str, k['grid']))} | "
                          f"{'x'.join(map(str, k['workgroup']))} | {k['launches']} | {k['avg_us']} | {k['min_us']} | "
                          f"{k['max_us']} |")
-    with open(POINTS_TRACE_FILE.replace(".json", ".md"), "w") as f:
+    with open(out_path.replace(".json", ".md"), "w") as f:
         f.write("\n".join(lines) + "\n")
-    print(f"{len(points)} points summarized into {POINTS_TRACE_FILE}")
+    print(f"{len(points)} points summarized into {out_path}")
 
 
 # --------------------------------------------------------------------------- other points
