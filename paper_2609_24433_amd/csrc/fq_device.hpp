@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 namespace fq {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -59,6 +61,16 @@ __device__ __forceinline__ v4i mfma16x16x64(v4i a, v4i b, v4i c) {
 
 __device__ __forceinline__ void lds_fence() { asm volatile("" ::: "memory"); }
 
+// f(std::integral_constant<int, i>) for i = 0 .. N-1 in order, each i a compile-time constant.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // Instruction-scheduling wall: the compiler moves nothing across it.
 __device__ __forceinline__ void sched_wall() { __builtin_amdgcn_sched_barrier(0); }
 
@@ -101,6 +113,31 @@ __device__ __forceinline__ float lds_read4_untracked(const void *p) {
   return v;
 }
 __device__ __forceinline__ void lgkm_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// 16-byte global load the compiler does not track: it places no wait of its own for the
+// result, which a kernel that streams many loads into registers needs when the compiler's
+// bookkeeping would otherwise make the first use wait for every load in flight.  The
+// caller waits with vm_wait_on before using the value.
+__device__ __forceinline__ v4i global_load16_untracked(const void *p) {
+  v4i v;
+  asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+// s_waitcnt vmcnt(N) tied to a and b, results of untracked loads: no use of them moves
+// above the wait.
+template <int N>
+__device__ __forceinline__ void vm_wait_on(v4i &a, v4i &b) {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%2)" : "+v"(a), "+v"(b) : "i"(N) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void vm_wait_on(v4i &a) {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%1)" : "+v"(a) : "i"(N) : "memory");
+}
+// lgkmcnt(0) tied to v, the result of an untracked read: no use of v moves above the wait.
+__device__ __forceinline__ void lgkm_wait_on(v4i &v) {
+  asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v)::"memory");
+}
 // LDS writes the compiler does not track (same reason); an lds_barrier() orders them.
 __device__ __forceinline__ void lds_write4_untracked(void *p, float v) {
   const uint32_t a = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(p));

@@ -569,6 +569,155 @@ static size_t stream_lds_bytes() {
   return slice > out ? slice : out;
 }
 
+// ---------------- streaming kernel, one K range per wave (M <= 64, long K, INT4) ----------------
+//
+// Workgroup = WK waves, NCW 16-channel tiles (16 NCW output channels), one 16-row block
+// (blockIdx.z) and a K slice of WK * KT steps (blockIdx.y).  Wave kg owns the steps
+// [kg KT, (kg + 1) KT) of the slice for every tile of the workgroup: it stages its own part
+// of the activation slice (16 rows x KT steps of nibble codes) in its own LDS region with
+// direct-to-LDS loads (16-byte chunks XOR-swizzled by row, as in the kernel above), then
+// loads its NCW x KT weight tiles into registers, and multiplies as soon as its own part
+// has landed: no wave waits for another before the final sum, and each widened activation
+// operand serves all NCW tiles.  Steps past K take zero activation operands.  At the end
+// the waves' sums add up through LDS (exact integers) and wave i rescales tile i.
+template <int KT, int WK, int NCW>
+__global__ __launch_bounds__(64 * WK) void gemm_stream_kw_kernel(GemmParams p) {
+  using F = Fmt<4, kANibble>;
+  constexpr int AROW = KT * F::arow;  // bytes of one row in a wave's part
+  constexpr int PART = 16 * AROW;     // a wave's part: 16 rows
+  constexpr int KPR = AROW / 1024;    // direct-to-LDS loads (1 KB each) per row
+  constexpr int NCOL = 16 * NCW;
+  static_assert(AROW % 1024 == 0 && NCW <= WK, "whole-KB rows; one finishing wave per tile");
+  extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
+
+  const int lane = threadIdx.x & 63;
+  const int kg = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nblk = blockIdx.x, split = blockIdx.y, nsplit = gridDim.y;
+  const int ktot = p.K / kTileK;
+  const int ks_begin = split * WK * KT + kg * KT;
+  const int nk = max(0, min(KT, ktot - ks_begin));
+  const int m0 = blockIdx.z * 16;
+  const int mz = min(16, p.M - m0);  // rows of the block (>= 1)
+  uint8_t *part = lds + kg * PART;
+
+  // rescale factors first (every wave loads them; wave i < NCW uses those of tile i), so
+  // that only the weight tiles are issued after the slice
+  float dt[1][4];
+  EpiParams ep[1];
+  const int ntile_own = nblk * NCW + (kg < NCW ? kg : 0);
+  load_epi<1, 1>(p, m0, ntile_own * 16, lane, dt, ep);
+
+  // 1. this wave's part of the slice: row r < mz, KT * 4 chunks, chunk c at unit c ^ (r & 15);
+  // chunks past K read chunk 0 (their operands are zeroed below); a wave whose steps all
+  // lie past K loads nothing
+  sched_wall();
+  if (nk > 0) {
+    const uint8_t *abase = p.a + (int64_t)m0 * p.lda + (int64_t)ks_begin * F::arow;
+    const int valid = nk * (F::arow / 16);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if (r >= mz) break;
+#pragma unroll
+      for (int h = 0; h < KPR; ++h) {
+        int c = (h * 64 + lane) ^ r;
+        if (c >= valid) c = 0;
+        load_to_lds16(abase + (int64_t)r * p.lda + (uint32_t)(c * 16), part + r * AROW + h * 1024);
+      }
+    }
+  }
+
+  // 2. the weight tiles of every tile of the workgroup, in k order (steps past K re-read
+  // the last step, never used with a nonzero operand), as untracked loads: step kt waits
+  // for exactly its own tiles below
+  sched_wall();
+  v4i wreg[NCW][KT];
+  const uint8_t *wt[NCW];
+#pragma unroll
+  for (int i = 0; i < NCW; ++i)
+    wt[i] = p.w + (int64_t)min(nblk * NCW + i, p.N / 16 - 1) * ktot * F::tb + lane * F::lb;
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+    for (int i = 0; i < NCW; ++i)
+      wreg[i][kt] = global_load16_untracked(wt[i] + (int64_t)min(ks_begin + kt, ktot - 1) * F::tb);
+  sched_wall();
+
+  // 3. MFMA over the wave's steps once this wave's slice loads have landed (they were
+  // issued before the weights, and loads complete in issue order).  The slice is read with
+  // untracked LDS reads: the compiler cannot tell this wave's region from the ones other
+  // waves' direct-to-LDS loads are filling.  Each read is waited for (lgkmcnt) before its
+  // value is used, one step ahead of the MFMAs; step kt waits (vmcnt) until only the
+  // tiles of later steps are in flight.
+  wait_vmcnt<NCW * KT>();
+  const int r16 = lane & 15, g = lane >> 4;
+  const uint8_t *rp = part + r16 * AROW;
+  auto load_a = [&](int kt) -> v4i {
+    return __builtin_bit_cast(v4i, lds_read16_untracked(rp + (((kt * 4 + g) ^ r16) * 16)));
+  };
+  v4i acc[2][NCW];
+#pragma unroll
+  for (int h = 0; h < 2; ++h)
+#pragma unroll
+    for (int i = 0; i < NCW; ++i) acc[h][i] = v4i{0, 0, 0, 0};
+  v4i araw = load_a(0);
+  auto step = [&](auto kt_c) {
+    constexpr int kt = decltype(kt_c)::value;
+    sched_wall();
+    if constexpr (NCW == 2)
+      vm_wait_on<(KT - 1 - kt) * NCW>(wreg[0][kt], wreg[1][kt]);
+    else
+      vm_wait_on<(KT - 1 - kt) * NCW>(wreg[0][kt]);
+    lgkm_wait_on(araw);
+    const v4i cur = araw;
+    if constexpr (kt + 1 < KT) araw = load_a(kt + 1);
+    v4i a0 = widen8(v2i{cur.x, cur.y});
+    v4i a1 = widen8(v2i{cur.z, cur.w});
+    if (kt >= nk) {
+      a0 = v4i{0, 0, 0, 0};
+      a1 = v4i{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int i = 0; i < NCW; ++i) {
+      const v4i w = wreg[i][kt];
+      acc[0][i] = mfma16x16x64(a0, widen8(v2i{w.x, w.y}), acc[0][i]);
+      acc[1][i] = mfma16x16x64(a1, widen8(v2i{w.z, w.w}), acc[1][i]);
+    }
+  };
+  static_for<KT>(step);
+
+  // 4. the waves' sums add up through LDS (the slice is no longer read); wave i < NCW
+  // finishes tile i
+  __syncthreads();
+  v4i *red = reinterpret_cast<v4i *>(lds);
+#pragma unroll
+  for (int i = 0; i < NCW; ++i) red[(kg * NCW + i) * 64 + lane] = acc[0][i] + acc[1][i];
+  __syncthreads();
+  uint8_t *stage = lds + (size_t)WK * NCW * 64 * 16;
+  if (kg < NCW) {
+    v4i t = red[kg * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < WK; ++w) t += red[(w * NCW + kg) * 64 + lane];
+    const v4i tt[1][1] = {{t}};
+    if (p.acc_out && nsplit == 1) store_acc_out<1, 1, F::shift>(p, tt, m0, ntile_own * 16, lane);
+    if (nsplit == 1)
+      stage_tiles<1, 1, F::shift, true>(stage, NCOL, tt, 0, kg * 16, lane, dt, ep);
+    else
+      stage_tiles<1, 1, F::shift, false>(stage, NCOL, tt, 0, kg * 16, lane, dt, ep);
+  }
+  __syncthreads();
+  if (nsplit == 1)
+    store_staged<true>(stage, 16, NCOL, m0, nblk * NCOL, p, 0, 64 * WK);
+  else
+    store_staged<false>(stage, 16, NCOL, m0, nblk * NCOL, p, split, 64 * WK);
+}
+
+template <int KT, int WK, int NCW>
+static constexpr size_t stream_kw_lds_bytes() {
+  constexpr size_t slice = (size_t)WK * 16 * KT * 64;
+  constexpr size_t fin = (size_t)WK * NCW * 64 * 16 + 16 * (16 * NCW * 4 + 16);
+  return slice > fin ? slice : fin;
+}
+
 // ---------------- tiled kernel (M > 64) ----------------
 //
 // BM x BN output tile per workgroup (2 x 2 waves), k steps of 128 channels.  Operands
@@ -879,27 +1028,26 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       pl.mt = 1;
       pl.rb = (int)((M + 15) / 16);
     }
-    // Long K (nibble codes): one 16-row tile per workgroup and 128 k steps per slice (the
-    // whole of K = 16384), 16 output channels per workgroup for up to 32 rows, 32 for
-    // 33-64 rows.  Each row block streams the weights again (sibling row blocks share them
-    // through the XCD's L2), but K needs no split, so the split-K epilogue launch goes
-    // away.  Measured at M = 50, K 16384 -> N 2048: 11.1 against 11.7 us.  Up to 32 rows
-    // this needs a grid of >= 128 workgroups to keep the weight stream wide enough.
+    // Long K (nibble codes): one K range per wave (gemm_stream_kw_kernel): 16-row blocks,
+    // 8 waves of 16 steps each (the whole of K = 16384 in one slice, 128 KB of LDS, no
+    // split-K epilogue), 32 output channels per workgroup for 33-64 rows, 16 for up to 32
+    // rows when that grid holds >= 128 workgroups.  Each row block streams the weights
+    // again (its siblings share them through the XCD's L2); each wave waits only for its
+    // own slice part.
     if (bits == 4 && ktot >= 128) {
       const int rb = (int)((M + 15) / 16);
-      const int wc = rb <= 2 ? 1 : 2;
-      const int64_t tiles = (N + 16 * wc - 1) / (16 * wc);
+      const int ncw = rb <= 2 ? 1 : 2;
+      const int64_t tiles = (N + 16 * ncw - 1) / (16 * ncw);
       const int splits = (ktot + 127) / 128;
       if (M > 32 || tiles * rb * splits >= 128) {
-        // 8 wave groups of 16 steps with one wave column (as many waves as with two
-        // columns, and at most 32 loads in flight per wave)
+        pl.kind = 2;
         pl.mt = 1;
         pl.rb = rb;
-        pl.wk = wc == 1 ? 8 : 4;
-        pl.kt = wc == 1 ? 16 : 32;
+        pl.wk = 8;
+        pl.kt = 16;
         pl.ksteps = 128;
         pl.splits = splits;
-        pl.wc = wc;
+        pl.wc = ncw;
         pl.tiles = tiles;
       }
     }
@@ -957,6 +1105,17 @@ static hipError_t launch_stream(const GemmParams &p, dim3 grid, hipStream_t s, b
   return hipGetLastError();
 }
 
+template <int KT, int WK, int NCW>
+static hipError_t launch_stream_kw(const GemmParams &p, dim3 grid, hipStream_t s, bool go) {
+  constexpr size_t lds = stream_kw_lds_bytes<KT, WK, NCW>();
+  static_assert(lds <= 160 * 1024, "LDS budget");
+  static std::atomic<uint64_t> attr{0};
+  hipError_t e = allow_dynamic_lds(&gemm_stream_kw_kernel<KT, WK, NCW>, lds, attr);
+  if (e != hipSuccess || !go) return e;
+  hipLaunchKernelGGL((gemm_stream_kw_kernel<KT, WK, NCW>), grid, dim3(64 * WK), lds, s, p);
+  return hipGetLastError();
+}
+
 template <int BITS, int AFMT, int MT, int WC>
 static hipError_t launch_stream_wc(const GemmParams &p, int kt, int wk, dim3 grid, hipStream_t s, bool go) {
   if (wk == 4) {
@@ -967,18 +1126,8 @@ static hipError_t launch_stream_wc(const GemmParams &p, int kt, int wk, dim3 gri
       case 8:
         if constexpr (AFMT == kANibble) return launch_stream<BITS, AFMT, MT, 8, 4, WC>(p, grid, s, go);
         return hipErrorInvalidValue;  // a 32-step int8 slice does not fit in LDS
-      case 32:
-        // one 16-row tile over 128 k steps (nibble codes): the whole of K = 16384 in one slice
-        if constexpr (AFMT == kANibble && MT == 1 && WC == 2) return launch_stream<BITS, AFMT, MT, 32, 4, WC>(p, grid, s, go);
-        return hipErrorInvalidValue;
       default: return hipErrorInvalidValue;
     }
-  }
-  if (wk == 8) {
-    // one 16-row tile and one wave column over 128 k steps (nibble codes)
-    if constexpr (AFMT == kANibble && MT == 1 && WC == 1)
-      if (kt == 16) return launch_stream<BITS, AFMT, MT, 16, 8, WC>(p, grid, s, go);
-    return hipErrorInvalidValue;
   }
   if (wk == 1) {
     switch (kt) {
@@ -1029,7 +1178,14 @@ static hipError_t launch_tile_shape(const GemmParams &p, const GemmPlan &pl, dim
 template <int BITS, int AFMT>
 static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStream_t s, bool go) {
   hipError_t e;
-  if (pl.kind == 0) {
+  if (pl.kind == 2) {
+    dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits, (unsigned)pl.rb);
+    e = hipErrorInvalidValue;
+    if constexpr (BITS == 4 && AFMT == kANibble) {
+      if (pl.kt == 16 && pl.wk == 8 && pl.wc == 1) e = launch_stream_kw<16, 8, 1>(p, grid, s, go);
+      if (pl.kt == 16 && pl.wk == 8 && pl.wc == 2) e = launch_stream_kw<16, 8, 2>(p, grid, s, go);
+    }
+  } else if (pl.kind == 0) {
     dim3 grid((unsigned)pl.tiles, (unsigned)pl.splits, (unsigned)pl.rb);
     switch (pl.mt) {
       case 1: e = launch_stream_mt<BITS, AFMT, 1>(p, pl.kt, pl.wk, pl.wc, grid, s, go); break;

@@ -55,7 +55,7 @@ hipError_t launch_unpack_weights(const uint8_t *packed, int64_t N, int K, int bi
 
 // GEMM plan: which kernel, its tiling and its split of K.
 struct GemmPlan {
-  int kind;     // 0 = streaming (M <= 64), 1 = tiled
+  int kind;     // 0 = streaming (M <= 64), 1 = tiled, 2 = streaming with one K range per wave (long K)
   int mt;       // streaming: 16-row tiles covering M
   int kt, wk;   // streaming: k steps per wave, wave groups along K per workgroup
   int wc;       // streaming: 16-channel wave columns per workgroup

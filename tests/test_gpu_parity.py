@@ -159,9 +159,11 @@ GEMM_CASES = [
     # these small grids; 128 x 128 in the full-size tests), split-K where the plan asks
     (1, 16, 128), (16, 48, 1024), (17, 256, 1024), (50, 2048, 4096), (64, 272, 2048),
     (65, 256, 1024), (130, 400, 1024), (300, 272, 2048), (50, 1024, 16384), (200, 128, 8192),
-    # long K: 16-row blocks over 128-step slices (one or two K slices), 16 output channels
-    # per workgroup up to 32 rows, 32 from 33 rows on
+    # long K: 16-row blocks over 128-step slices (one or two K slices), one K range per
+    # wave, 16 output channels per workgroup up to 32 rows, 32 from 33 rows on
     (33, 64, 32768), (64, 96, 16384), (1, 2048, 16384), (16, 1040, 16384), (20, 2048, 32768),
+    # a second K slice with one step, and one whose later waves hold no step at all
+    (40, 272, 16512), (1, 2048, 18432),
 ]
 
 
