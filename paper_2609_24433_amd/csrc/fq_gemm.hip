@@ -583,9 +583,9 @@ static size_t stream_lds_bytes() {
 template <int KT, int WK, int NCW>
 __global__ __launch_bounds__(64 * WK) void gemm_stream_kw_kernel(GemmParams p) {
   using F = Fmt<4, kANibble>;
-  constexpr int AROW = KT * F::arow;  // bytes of one row in a wave's part
-  constexpr int PART = 16 * AROW;     // a wave's part: 16 rows
-  constexpr int KPR = AROW / 1024;    // direct-to-LDS loads (1 KB each) per row
+  constexpr int AROW = KT * F::arow;            // bytes of one row in a wave's part
+  constexpr int PART = 16 * AROW;               // a wave's part: 16 rows
+  constexpr int KPR = AROW / 1024;              // direct-to-LDS loads (1 KB each) per row
   constexpr int NCOL = 16 * NCW;
   static_assert(AROW % 1024 == 0 && NCW <= WK, "whole-KB rows; one finishing wave per tile");
   extern __shared__ __attribute__((aligned(1024))) uint8_t lds[];
@@ -1028,17 +1028,21 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       pl.mt = 1;
       pl.rb = (int)((M + 15) / 16);
     }
-    // Long K (nibble codes): one K range per wave (gemm_stream_kw_kernel): 16-row blocks,
-    // 8 waves of 16 steps each (the whole of K = 16384 in one slice, 128 KB of LDS, no
-    // split-K epilogue), 32 output channels per workgroup for 33-64 rows, 16 for up to 32
-    // rows when that grid holds >= 128 workgroups.  Each row block streams the weights
+    // Long K (nibble codes, K >= 16384): one K range per wave (gemm_stream_kw_kernel),
+    // 16-row blocks, 8 waves of 16 steps each (the whole of K = 16384 in one slice, 128 KB
+    // of LDS, no split-K epilogue).  32 output channels per workgroup when that grid still
+    // holds >= 256 workgroups, else 16; up to 32 rows the plan needs a grid of >= 128
+    // workgroups to keep the weight stream wide enough.  Each row block streams the weights
     // again (its siblings share them through the XCD's L2); each wave waits only for its
-    // own slice part.
+    // own slice part.  Measured at M = 50, K 16384 -> N 2048: 11.1 us with four wave groups
+    // sharing one slice, 9.5 us this way.  Shorter K stays on the kernel above (site D of
+    // the action expert, K 4096: 3.3 against 3.5 us this way).
     if (bits == 4 && ktot >= 128) {
       const int rb = (int)((M + 15) / 16);
-      const int ncw = rb <= 2 ? 1 : 2;
-      const int64_t tiles = (N + 16 * ncw - 1) / (16 * ncw);
       const int splits = (ktot + 127) / 128;
+      int ncw = 2;
+      if (((N + 31) / 32) * rb * splits < 256) ncw = 1;
+      const int64_t tiles = (N + 16 * ncw - 1) / (16 * ncw);
       if (M > 32 || tiles * rb * splits >= 128) {
         pl.kind = 2;
         pl.mt = 1;

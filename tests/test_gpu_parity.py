@@ -164,6 +164,8 @@ GEMM_CASES = [
     (33, 64, 32768), (64, 96, 16384), (1, 2048, 16384), (16, 1040, 16384), (20, 2048, 32768),
     # a second K slice with one step, and one whose later waves hold no step at all
     (40, 272, 16512), (1, 2048, 18432),
+    # 4096 <= K < 16384 (four wave groups sharing one slice; K split in two)
+    (50, 1024, 4096), (33, 512, 8192), (1, 4096, 4224), (17, 1024, 12288),
 ]
 
 
