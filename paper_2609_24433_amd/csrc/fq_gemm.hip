@@ -578,8 +578,8 @@ static size_t stream_lds_bytes() {
 // direct-to-LDS loads (16-byte chunks XOR-swizzled by row, as in the kernel above), then
 // loads its NCW x KT weight tiles into registers, and multiplies as soon as its own part
 // has landed: no wave waits for another before the final sum, and each widened activation
-// operand serves all NCW tiles.  Steps past K take zero activation operands.  At the end
-// the waves' sums add up through LDS (exact integers) and wave i rescales tile i.
+// operand serves all NCW tiles.  Steps past K find zero activation codes in LDS.  At the
+// end the waves' sums add up through LDS (exact integers) and wave i rescales tile i.
 template <int KT, int WK, int NCW>
 __global__ __launch_bounds__(64 * WK) void gemm_stream_kw_kernel(GemmParams p) {
   using F = Fmt<4, kANibble>;
@@ -607,28 +607,39 @@ __global__ __launch_bounds__(64 * WK) void gemm_stream_kw_kernel(GemmParams p) {
   const int ntile_own = nblk * NCW + (kg < NCW ? kg : 0);
   load_epi<1, 1>(p, m0, ntile_own * 16, lane, dt, ep);
 
-  // 1. this wave's part of the slice: row r < mz, KT * 4 chunks, chunk c at unit c ^ (r & 15);
-  // chunks past K read chunk 0 (their operands are zeroed below); a wave whose steps all
-  // lie past K loads nothing
+  // 1. this wave's part of the slice: row r < mz, KT * 4 chunks, chunk c at unit c ^ r.
+  // Units of chunks past K are written with zeros instead (a partial last slice), so their
+  // MFMAs add nothing and the loop below needs no masking
   sched_wall();
-  if (nk > 0) {
+  {
     const uint8_t *abase = p.a + (int64_t)m0 * p.lda + (int64_t)ks_begin * F::arow;
     const int valid = nk * (F::arow / 16);
+    if (valid == KT * 4) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      if (r >= mz) break;
+      for (int r = 0; r < 16; ++r) {
+        if (r >= mz) break;
 #pragma unroll
-      for (int h = 0; h < KPR; ++h) {
-        int c = (h * 64 + lane) ^ r;
-        if (c >= valid) c = 0;
-        load_to_lds16(abase + (int64_t)r * p.lda + (uint32_t)(c * 16), part + r * AROW + h * 1024);
+        for (int h = 0; h < KPR; ++h)
+          load_to_lds16(abase + (int64_t)r * p.lda + (uint32_t)((((h * 64 + lane) ^ r)) * 16),
+                        part + r * AROW + h * 1024);
       }
+    } else {
+      for (int r = 0; r < mz; ++r)
+        for (int h = 0; h < KPR; ++h) {
+          const int c = (h * 64 + lane) ^ r;
+          if (c < valid)
+            load_to_lds16(abase + (int64_t)r * p.lda + (uint32_t)(c * 16), part + r * AROW + h * 1024);
+          else
+            lds_write16_untracked(part + r * AROW + (h * 64 + lane) * 16, make_uint4(0u, 0u, 0u, 0u));
+        }
     }
   }
 
   // 2. the weight tiles of every tile of the workgroup, in k order (steps past K re-read
   // the last step, never used with a nonzero operand), as untracked loads: step kt waits
-  // for exactly its own tiles below
+  // for exactly its own tiles below.  The compiler takes an untracked load's register as
+  // written at once, so no control flow may separate the loads from their waits: at a
+  // join the register allocator may copy a register whose data has not landed.
   sched_wall();
   v4i wreg[NCW][KT];
   const uint8_t *wt[NCW];
@@ -670,12 +681,8 @@ __global__ __launch_bounds__(64 * WK) void gemm_stream_kw_kernel(GemmParams p) {
     lgkm_wait_on(araw);
     const v4i cur = araw;
     if constexpr (kt + 1 < KT) araw = load_a(kt + 1);
-    v4i a0 = widen8(v2i{cur.x, cur.y});
-    v4i a1 = widen8(v2i{cur.z, cur.w});
-    if (kt >= nk) {
-      a0 = v4i{0, 0, 0, 0};
-      a1 = v4i{0, 0, 0, 0};
-    }
+    const v4i a0 = widen8(v2i{cur.x, cur.y});
+    const v4i a1 = widen8(v2i{cur.z, cur.w});
 #pragma unroll
     for (int i = 0; i < NCW; ++i) {
       const v4i w = wreg[i][kt];
