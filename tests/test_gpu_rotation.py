@@ -33,6 +33,9 @@ CASES = [
     (16, 1024, 16, 4, True, False, False, 0), (50, 2048, 32, 8, True, True, True, 16), (50, 1024, 64, 4, True, False, False, 0),
     (130, 2048, 128, 4, True, True, True, 0), (3, 2048, 128, 8, False, False, False, 8), (2, 32768, 64, 4, True, True, False, 0),
     (257, 512, 4, 4, True, False, False, 0),
+    # the language prologue's shape (M = 816, K 2048) and larger grids at b = 16 and 32
+    (816, 2048, 128, 4, True, True, True, 0), (300, 8192, 32, 8, True, False, False, 0),
+    (100, 4096, 16, 4, False, True, False, 8),
 ]
 
 
