@@ -78,23 +78,15 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   const float qf = (float)q;
 
   // ---- all loads first (branch-free: out-of-range chunks read chunk 0) ----------------
+  // (the optional multipliers are read where they are applied: kept in registers from
+  // here, they would cost 32 VGPRs per chunk whether used or not, and with them the kernel
+  // holds half the waves per SIMD)
   Chunk<Tin> raw[CPT];
-  float4 cm[CPT][4], pm[CPT][4];
 #pragma unroll
   for (int c = 0; c < CPT; ++c) {
     const int j = c * TPR + tau;
     const int jc = j < nchunks ? j : 0;
     load_chunk<Tin>(p.x, row_c * p.ldx + (int64_t)jc * 16, raw[c]);
-    if (p.chan_mult) {
-      const float4 *m4 = reinterpret_cast<const float4 *>(p.chan_mult + jc * 16);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) cm[c][i] = m4[i];
-    }
-    if (p.post_mult) {
-      const float4 *m4 = reinterpret_cast<const float4 *>(p.post_mult + jc * 16);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) pm[c][i] = m4[i];
-    }
   }
 
   // ---- pass 1: optional multiplier, stages h < 16 in registers -------------------------
@@ -103,13 +95,12 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   for (int c = 0; c < CPT; ++c) {
     unpack_chunk<Tin>(raw[c], v1[c]);
     if (p.chan_mult) {
+      const int j = c * TPR + tau;
+      const float4 *m4 = reinterpret_cast<const float4 *>(p.chan_mult + (j < nchunks ? j : 0) * 16);
+      float4 cm[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        v1[c][4 * i] = v1[c][4 * i] * cm[c][i].x;
-        v1[c][4 * i + 1] = v1[c][4 * i + 1] * cm[c][i].y;
-        v1[c][4 * i + 2] = v1[c][4 * i + 2] * cm[c][i].z;
-        v1[c][4 * i + 3] = v1[c][4 * i + 3] * cm[c][i].w;
-      }
+      for (int i = 0; i < 4; ++i) cm[i] = m4[i];
+      mul_chunk(v1[c], cm);
     }
     butterfly<16, B1>(v1[c]);
   }
@@ -125,14 +116,14 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
   // ---- optional fold-after multiplier (Sec. III-C), one fp32 rounding per element -------
   if (p.post_mult) {
 #pragma unroll
-    for (int c = 0; c < CPT; ++c)
+    for (int c = 0; c < CPT; ++c) {
+      const int j = c * TPR + tau;
+      const float4 *m4 = reinterpret_cast<const float4 *>(p.post_mult + (j < nchunks ? j : 0) * 16);
+      float4 pm[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        v1[c][4 * i] = v1[c][4 * i] * pm[c][i].x;
-        v1[c][4 * i + 1] = v1[c][4 * i + 1] * pm[c][i].y;
-        v1[c][4 * i + 2] = v1[c][4 * i + 2] * pm[c][i].z;
-        v1[c][4 * i + 3] = v1[c][4 * i + 3] * pm[c][i].w;
-      }
+      for (int i = 0; i < 4; ++i) pm[i] = m4[i];
+      mul_chunk(v1[c], pm);
+    }
   }
 
   // ---- row absmax: own chunks, then the row's lanes, then the row's waves ---------------
