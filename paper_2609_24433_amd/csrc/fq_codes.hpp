@@ -18,6 +18,45 @@ __device__ __forceinline__ int quantize_bits(float u, float inv, float lim) {
   return __float_as_int(t + 12582912.0f);
 }
 
+// Nibble codes in biased form, for the prologue kernel: clamp (when the clip ratio can push
+// |u * inv| past q + 1/2) and add 1.5 * 2^23 + 8, which rounds exactly as quantize_bits does
+// (the added integer is even, so ties still go to even) and leaves the bit pattern
+// 0x4B400000 + code + 8: the low nibble holds code + 8 in [1, 15] and bits 4..15 are zero.
+// With r = 1 no clamp is needed: |u| <= A, inv = fl(q / A), so |fl(u * inv)| <= q (1 + 2^-24)^2
+// < q + 1/2 and the rounded value never passes q.
+template <bool CLAMP>
+__device__ __forceinline__ uint32_t quantize_bits_biased(float u, float inv, float lim) {
+  const float t = CLAMP ? __builtin_amdgcn_fmed3f(u * inv, -lim, lim) : u * inv;
+  return __float_as_uint(t + 12582920.0f);
+}
+
+// (a << S) | b as one instruction; written out so that the compiler keeps the two-level
+// combination below instead of re-associating it into separate shifts.
+template <int S>
+__device__ __forceinline__ uint32_t lshl_or(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "i"(S), "v"(b));
+  return r;
+}
+
+// 16 biased bit patterns (natural channel order) -> canonical nibbles, 8 bytes.  Byte 0 of
+// (odd << 4) | even is (c_odd + 8) << 4 | (c_even + 8) and its byte 1 is zero, so two such
+// words combine with one more shift-or, two halves with a byte permute, and one xor with 0x8
+// per nibble turns code + 8 into the two's-complement nibble.
+__device__ __forceinline__ uint2 pack_chunk_nibbles_biased(const uint32_t (&c)[16]) {
+  uint32_t w[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t pb[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pb[i] = lshl_or<4>(c[8 * h + 2 * i + 1], c[8 * h + 2 * i]);
+    const uint32_t lo = lshl_or<8>(pb[1], pb[0]);
+    const uint32_t hi = lshl_or<8>(pb[3], pb[2]);
+    w[h] = __builtin_amdgcn_perm(hi, lo, 0x05040100u) ^ 0x88888888u;
+  }
+  return make_uint2(w[0], w[1]);
+}
+
 // Pack 16 quantized bit patterns (natural channel order; low byte = code) into canonical
 // nibbles (8 bytes: channel 2i in the low nibble of byte i) or int8 (16 bytes).
 __device__ __forceinline__ uint2 pack_chunk_nibbles(const int (&c)[16]) {

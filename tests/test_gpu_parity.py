@@ -28,6 +28,8 @@ QUANT_CASES = [
     (37, 1024, 256, 4, 1.0), (70, 384, 128, 4, 0.85), (3, 4096, 128, 4, 1.0), (5, 16384, 256, 8, 1.0),
     (5, 16384, 32, 4, 1.0), (9, 2048, 64, 8, 0.7), (1, 128, 128, 4, 1.0), (300, 1152, 128, 4, 1.0),
     (2, 32768, 128, 4, 1.0), (2, 32768, 8, 8, 1.0), (4, 8192, 256, 4, 1.0), (130, 640, 128, 8, 1.0),
+    # rows of 2 chunks per thread with the last chunks of the row past K
+    (3, 12288, 128, 4, 1.0), (17, 6144, 256, 4, 0.9), (6, 24576, 64, 8, 0.8), (5, 24576, 128, 4, 1.0),
 ]
 
 
