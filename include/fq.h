@@ -144,10 +144,11 @@ size_t fq_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
  *   y_bf16    [M, ldy] bf16 output: y = bf16_rne(fp32(acc) * (w_scale[j] * delta[t]) + bias[j]).
  *   acc_out   int32 [M, N] raw accumulators, or NULL (for verification).
  *   ws        scratch of at least fq_gemm_workspace_bytes(M, N, K, bits) bytes (0 when
- *             the shape needs no split of K; ws may then be NULL).  It needs no
- *             initialization; it holds the INT32 partial sums of a split K between the
- *             GEMM kernel and its epilogue.  Calls that share a workspace race unless
- *             they are ordered, e.g. on one stream.
+ *             the shape needs none; ws may then be NULL).  It needs no initialization;
+ *             it holds the INT32 partial sums of a split K between the GEMM kernel and
+ *             its epilogue, or (W4A4, a few hundred rows at long K) a k-step-major copy
+ *             of a_codes that the GEMM reads with coalesced loads.  Calls that share a
+ *             workspace race unless they are ordered, e.g. on one stream.
  * Accumulation is exact: |acc| <= K q^2 < 2^31 for K <= 32768 at INT4 and
  * K <= 32768 at INT8 (127^2 * 32768 < 2^31 holds up to K = 133152). */
 fq_status fq_gemm_w4a4(const void *a_codes, const float *delta, const void *w_packed,
@@ -178,14 +179,15 @@ fq_status fq_gemm_w4a16(const void *x_bf16, int64_t ldx, const void *w_packed, c
                         int64_t N, int64_t K, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes fq_linear needs: the intermediate activation codes and scales, and the
- * split-K partial sums.  Scratch with no initialization requirement. */
+ * split-K partial sums.  Scratch with no initialization requirement.  (The intermediate
+ * codes are the canonical nibbles or int8, or for the shapes the k-group GEMM serves the
+ * same nibbles stored k-step major: the same bytes in another order.) */
 size_t fq_linear_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits);
 
 /* The whole runtime projection for one consumer (Alg. 1 runtime; eqs. (5), (8)):
  * prologue on x, integer GEMM against w_packed, rescale + bias, bf16 out.
  * Same arguments and contracts as fq_fwht_quant followed by fq_gemm_w{4a4,8a8}, and the
- * same output bit for bit; the intermediate codes (canonical layout) and scales live
- * in `ws`. */
+ * same output bit for bit; the intermediate codes and scales live in `ws`. */
 fq_status fq_linear(const void *x_bf16, int64_t ldx, const float *smooth_inv, const float *post_inv,
                     int64_t M, int64_t K, int64_t N, int b, int bits, float clip_ratio,
                     const void *w_packed, const float *w_scale, const float *bias, void *y_bf16,

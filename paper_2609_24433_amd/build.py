@@ -4,9 +4,11 @@
 
 Every HIP source is compiled with -ffp-contract=off (the prologue's codes must be
 reproducible bit for bit: no multiply-add may be fused) and with packed-fp32
-instructions disabled.  The GEMM source keeps MFMA accumulators in ordinary VGPRs
+instructions disabled.  The GEMM sources keep MFMA accumulators in ordinary VGPRs
 (``-amdgpu-mfma-vgpr-form``): with them in AGPRs the register allocator splits the budget
-in half and spills the GEMM's double-buffered operands into AGPRs.
+in half and spills the GEMM's double-buffered operands into AGPRs.  The k-group GEMM
+(``fq_gemm_kg.hip``) is the exception: its 128 accumulators and two register sets of
+operands need the AGPRs.
 """
 from __future__ import annotations
 
@@ -20,7 +22,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libfq.so")
-SOURCES = ["fq_api.cpp", "fq_quant.hip", "fq_rotate.hip", "fq_gemm.hip", "fq_gptq.hip", "fq_small.hip"]
+SOURCES = ["fq_api.cpp", "fq_quant.hip", "fq_rotate.hip", "fq_gemm.hip", "fq_gemm_kg.hip", "fq_gptq.hip",
+           "fq_small.hip"]
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

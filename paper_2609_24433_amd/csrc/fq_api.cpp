@@ -158,7 +158,7 @@ fq_status gemm_common(const void *a_codes, int a_fmt, int64_t lda, const float *
                       int64_t ldy, int32_t *acc_out, int64_t M, int64_t N, int64_t K, int bits,
                       void *ws, size_t ws_bytes, hipStream_t stream, bool go = true) {
   const fq::GemmPlan pl = fq::plan_gemm(M, N, K, bits);
-  const size_t need = fq::gemm_plan_workspace(pl);
+  const size_t need = fq::gemm_plan_workspace(pl) + (a_fmt == fq::kANibble ? fq::gemm_plan_relayout_bytes(pl, M, K) : 0);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
   if (need > 0 && !aligned16(ws)) return fail(FQ_ERR_ALIGN, "workspace must be 16-byte aligned");
@@ -270,11 +270,13 @@ fq_status linear_common(const void *x_bf16, int64_t ldx, const float *smooth_inv
   float *delta = reinterpret_cast<float *>(codes + codes_bytes);
   void *gws = codes + codes_bytes + delta_bytes;
   const size_t gws_bytes = ws_bytes - codes_bytes - delta_bytes;
-  // W4A4 codes between the two kernels are canonical nibbles (half the bytes of int8, the
-  // same per-step cost in the GEMMs, which widen them in registers); W8A8 codes are int8.
+  // W4A4 codes between the two kernels are nibbles (half the bytes of int8, the same
+  // per-step cost in the GEMMs, which widen them in registers), canonical or, for the
+  // k-group GEMM, k-step major; W8A8 codes are int8.
   const bool nibble = bits == 4;
-  const int fmt = nibble ? fq::kOutNibble : fq::kOutInt8;
-  const int afmt = nibble ? fq::kANibble : fq::kAInt8;
+  const bool kmajor = nibble && fq::plan_gemm(M, N, K, bits).kind == 3;
+  const int fmt = nibble ? (kmajor ? fq::kOutNibbleKM : fq::kOutNibble) : fq::kOutInt8;
+  const int afmt = nibble ? (kmajor ? fq::kANibbleKM : fq::kANibble) : fq::kAInt8;
   const int64_t lda = nibble ? K / 2 : K;
   s = gemm_common(codes, afmt, lda, delta, w_packed, w_scale, bias, y_bf16, ldy, nullptr, M, N, K, bits, gws,
                   gws_bytes, st, /*go=*/false);
@@ -455,7 +457,8 @@ fq_status fq_unpack_weights(const void *w_packed, int64_t N, int64_t K, int bits
 
 size_t fq_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int bits) {
   if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
-  return fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
+  const fq::GemmPlan pl = fq::plan_gemm(M, N, K, bits);
+  return fq::gemm_plan_workspace(pl) + fq::gemm_plan_relayout_bytes(pl, M, K);
 }
 
 fq_status fq_gemm_w4a4(const void *a_codes, const float *delta, const void *w_packed,

@@ -1063,6 +1063,24 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
       }
     }
   } else {
+    // INT4 at long K where 128 x 128 tiles would not fill the chip without splitting K (a
+    // few hundred to ~1000 rows, N ~ 2048): 128 x 64 tiles with the K range split across
+    // the workgroup's four waves instead (gemm_kgroup_kernel, no partial buffer, no second
+    // kernel).  Measured at M = 816, K 16384 -> N 2048 against the split 128 x 128 plan:
+    // 31 against 43 us on one GPU (fed k-step-major codes).  Short K (fewer than 64 steps
+    // per tile) and grids of fewer than 160 tiles stay on the LDS-ring kernel below.
+    if (bits == 4 && ktot >= 64) {
+      const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
+      const int64_t tkg = ((M + 127) / 128) * ((N + 63) / 64);
+      if (t128 < 200 && tkg >= 160) {
+        pl.kind = 3;
+        pl.tiles = tkg;
+        pl.splits = 1;
+        pl.ksteps = ktot;
+        pl.partial_bytes = 0;
+        return pl;
+      }
+    }
     pl.kind = 1;
     // K slices: split a grid of fewer than 200 tiles while each slice keeps >= 32 steps
     auto slices = [&](int64_t tiles) {
@@ -1102,6 +1120,10 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
 }
 
 size_t gemm_plan_workspace(const GemmPlan &pl) { return pl.partial_bytes; }
+
+size_t gemm_plan_relayout_bytes(const GemmPlan &pl, int64_t M, int64_t K) {
+  return pl.kind == 3 ? align256((size_t)M * (size_t)K / 2) : 0;
+}
 
 // Every launcher below takes `go`: false resolves the kernel the plan selects and raises
 // its dynamic-LDS limit without launching anything, so that a caller can find out whether
@@ -1223,6 +1245,28 @@ static hipError_t launch_gemm_t(const GemmParams &p, const GemmPlan &pl, hipStre
 
 hipError_t launch_gemm(const GemmArgs &g, const GemmPlan &pl, void *ws, hipStream_t s, bool go) {
   if (g.M <= 0 || g.N <= 0) return hipSuccess;
+  if (pl.kind == 3) {
+    // k groups: k-step-major codes as given, or canonical ones converted into ws first
+    if (g.bits != 4) return hipErrorInvalidValue;
+    KgParams kp;
+    kp.delta = g.delta;
+    kp.w = g.w;
+    kp.w_scale = g.w_scale;
+    kp.bias = g.bias;
+    kp.y = g.y;
+    kp.ldy = g.ldy;
+    kp.acc_out = g.acc_out;
+    kp.M = (int)g.M;
+    kp.N = (int)g.N;
+    kp.K = (int)g.K;
+    if (g.a_fmt == kANibbleKM) {
+      kp.a = g.a;
+      return launch_gemm_kgroup(kp, nullptr, nullptr, s, go);
+    }
+    if (g.a_fmt != kANibble || g.lda != g.K / 2) return hipErrorInvalidValue;
+    kp.a = static_cast<const uint8_t *>(ws);
+    return launch_gemm_kgroup(kp, g.a, static_cast<uint8_t *>(ws), s, go);
+  }
   GemmParams p;
   p.a = g.a;
   p.lda = g.lda;

@@ -29,12 +29,14 @@ inline hipError_t allow_dynamic_lds(Kern kern, size_t lds, std::atomic<uint64_t>
 }
 
 // Output layouts of the prologue.
-constexpr int kOutNibble = 0;  // canonical signed-INT4: channel 2i low nibble of byte i
-constexpr int kOutInt8 = 1;    // canonical int8, one byte per channel
+constexpr int kOutNibble = 0;    // canonical signed-INT4: channel 2i low nibble of byte i
+constexpr int kOutInt8 = 1;      // canonical int8, one byte per channel
+constexpr int kOutNibbleKM = 2;  // the same nibbles k-step major: [K/128][M][64 B]
 
 // Activation operand formats of the GEMM.
-constexpr int kANibble = 0;  // canonical nibbles (widened in the kernel)
-constexpr int kAInt8 = 1;    // canonical int8 (W8A8)
+constexpr int kANibble = 0;    // canonical nibbles (widened in the kernel)
+constexpr int kAInt8 = 1;      // canonical int8 (W8A8)
+constexpr int kANibbleKM = 2;  // nibbles k-step major: [K/128][M][64 B] (plan kind 3)
 
 hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const float *chan_mult,
                              const float *post_mult, int64_t M, int K, int b, int bits, float clip_ratio, float cb,
@@ -55,7 +57,8 @@ hipError_t launch_unpack_weights(const uint8_t *packed, int64_t N, int K, int bi
 
 // GEMM plan: which kernel, its tiling and its split of K.
 struct GemmPlan {
-  int kind;     // 0 = streaming (M <= 64), 1 = tiled, 2 = streaming with one K range per wave (long K)
+  int kind;     // 0 = streaming (M <= 64), 1 = tiled, 2 = streaming with one K range per wave (long K),
+                // 3 = k groups (INT4, a few hundred rows, long K; k-step-major codes)
   int mt;       // streaming: 16-row tiles covering M
   int kt, wk;   // streaming: k steps per wave, wave groups along K per workgroup
   int wc;       // streaming: 16-channel wave columns per workgroup
@@ -71,7 +74,28 @@ struct GemmPlan {
 };
 
 GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits);
+// scratch of the GEMM itself (split-K partials); a kind-3 plan fed canonical codes also
+// needs gemm_plan_relayout_bytes for their k-step-major copy
 size_t gemm_plan_workspace(const GemmPlan &pl);
+size_t gemm_plan_relayout_bytes(const GemmPlan &pl, int64_t M, int64_t K);
+
+// k-group GEMM (fq_gemm_kg.hip), plan kind 3: INT4 codes k-step major (a_fmt kANibbleKM).
+struct KgParams {
+  const uint8_t *a;  // [K/128][M][64 B]
+  const float *delta;
+  const uint8_t *w;
+  const float *w_scale;
+  const float *bias;
+  uint16_t *y;
+  int64_t ldy;
+  int32_t *acc_out;
+  int M, N, K;
+};
+size_t kgroup_lds_bytes();
+// a_canonical != NULL: first convert those canonical codes into a_kmajor (M K/2 bytes),
+// which p.a must point to.  go = false only resolves the kernel and raises its LDS limit.
+hipError_t launch_gemm_kgroup(const KgParams &p, const uint8_t *a_canonical, uint8_t *a_kmajor, hipStream_t s,
+                              bool go);
 
 struct GemmArgs {
   const uint8_t *a;

@@ -34,7 +34,8 @@ struct QuantParams {
   float clip_ratio;
   float cb;  // float nearest 1/sqrt(b)
   uint8_t *codes;
-  int64_t ld_codes;  // bytes per output row
+  int64_t ld_codes;  // bytes per output row (64 for k-step-major nibbles)
+  int64_t kstride;   // nibbles: bytes between the 128-channel k steps of a row (64 canonical)
   float *delta;
   int out_fmt;
   int tpr_log2;
@@ -197,7 +198,8 @@ __global__ __launch_bounds__(NT) void fwht_quant_kernel(QuantParams p) {
 #pragma unroll
             for (int i = 0; i < 16; ++i) cc[i] = quantize_bits_biased<false>(v1[c][i], inv_l, lim);
           }
-          *reinterpret_cast<uint2 *>(row_out + (int64_t)j * 8) = pack_chunk_nibbles_biased(cc);
+          *reinterpret_cast<uint2 *>(row_out + (int64_t)(j >> 3) * p.kstride + (j & 7) * 8) =
+              pack_chunk_nibbles_biased(cc);
         } else {
           int cc[16];
           if (clamp) {
@@ -320,8 +322,14 @@ hipError_t launch_fwht_quant(const void *x, bool x_is_f32, int64_t ldx, const fl
   p.cb = cb;
   p.codes = codes;
   p.ld_codes = ld_codes;
+  p.kstride = 64;
   p.delta = delta;
   p.out_fmt = out_fmt;
+  if (out_fmt == kOutNibbleKM) {  // row r, k step ks at ks * 64 M + 64 r
+    p.out_fmt = kOutNibble;
+    p.ld_codes = 64;
+    p.kstride = 64 * M;
+  }
   p.tpr_log2 = q.tpr_log2;
   return x_is_f32 ? launch_t<float>(p, log2b, q, (int)grid64, s)
                   : launch_t<uint16_t>(p, log2b, q, (int)grid64, s);

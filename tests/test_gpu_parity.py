@@ -168,6 +168,9 @@ GEMM_CASES = [
     (40, 272, 16512), (1, 2048, 18432),
     # 4096 <= K < 16384 (four wave groups sharing one slice; K split in two)
     (50, 1024, 4096), (33, 512, 8192), (1, 4096, 4224), (17, 1024, 12288),
+    # k-group GEMM (INT4; 128 x 64 tiles, K over the workgroup's four waves): ragged rows
+    # and a ragged last column tile; 65 k steps, so one wave takes a step more than the rest
+    (700, 2000, 8192), (816, 2048, 8320),
 ]
 
 
@@ -224,6 +227,7 @@ LINEAR_CASES = [
     (16, 16384, 2048, 32, 8), (1, 16384, 2048, 256, 4), (77, 2048, 256, 128, 8),
     (130, 2048, 2048, 128, 4), (33, 512, 48, 16, 4), (0, 1024, 256, 64, 4),
     (200, 16384, 256, 128, 4),   # tiled GEMM with K split in 4 (split-K epilogue)
+    (700, 8192, 2000, 128, 4),   # k-group GEMM fed k-step-major codes by the prologue
 ]
 
 
