@@ -80,6 +80,11 @@ def parse():
     ap.add_argument("--summarize-trace", default=None, metavar="CSV",
                     help="summarize a --rocprof-points kernel trace into profiles/ and exit")
     ap.add_argument("--manifest", default=None, help="stdout of the --rocprof-points run (its point list)")
+    ap.add_argument("--summarize-traffic", default=None, metavar="DIR",
+                    help="summarize --traffic-site / --copy-calibration counter runs under DIR into profiles/ and exit")
+    ap.add_argument("--summarize-counters", default=None, metavar="DIR",
+                    help="summarize --counter-point counter runs under DIR into profiles/ and exit")
+    ap.add_argument("--counter-points", default=None, help="comma-separated points for --summarize-counters")
     ap.add_argument("--points", default=None, help="comma-separated point groups to run (default: all)")
     return ap.parse_args()
 
@@ -541,6 +546,203 @@ def summarize_trace(path, manifest_path, out_path=POINTS_TRACE_FILE):
     print(f"{len(points)} points summarized into {out_path}")
 
 
+# --------------------------------------------------------------------------- counter summaries
+
+def counter_rows(run_dir):
+    """(dispatch id, kernel, grid threads, counter, value) rows of one rocprofv3 --pmc run
+    (csv output under run_dir)."""
+    import csv
+    import glob
+    rows = []
+    for path in glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], int(r["Grid_Size"]), r["Counter_Name"],
+                             float(r["Counter_Value"])))
+    if not rows:
+        raise SystemExit(f"no counter rows under {run_dir}")
+    return rows
+
+
+def counter_means(run_dir, min_dispatches):
+    """(kernel, grid) -> {"dispatches": n, counter: mean per dispatch} over the kernels
+    dispatched at least min_dispatches times (the measured calls; set-up kernels such as
+    the weight rounding and packing run once)."""
+    per = {}
+    for disp, name, grid, ctr, val in counter_rows(run_dir):
+        d = per.setdefault((name, grid), {})
+        d.setdefault(ctr, {})[disp] = d.get(ctr, {}).get(disp, 0.0) + val
+    out = {}
+    for key, ctrs in per.items():
+        n = max(len(v) for v in ctrs.values())
+        if n >= min_dispatches:
+            out[key] = {"dispatches": n, **{c: sum(v.values()) / len(v) for c, v in ctrs.items()}}
+    return out
+
+
+def short_kernel(name):
+    return name.replace("void ", "").replace("(anonymous namespace)::", "").split("(")[0].replace("fq::", "")
+
+
+def copy_factors(d):
+    """KiB per launch that FETCH_SIZE and WRITE_SIZE read for the copy-like calibration
+    kernel (256 MiB each way), and the true bytes."""
+    f = counter_means(os.path.join(d, "copy_fetch"), 20)
+    w = counter_means(os.path.join(d, "copy_write"), 20)
+    fk = max(v["FETCH_SIZE"] for v in f.values())
+    wk = max(v["WRITE_SIZE"] for v in w.values())
+    return fk, wk, 256 << 20, 256 << 20
+
+
+SITE_SHAPES = {"A": (1024, 1536, "q|k|v"), "O": (1024, 1024, "o"), "B": (1024, 8192, "gate|up"),
+               "D": (4096, 1024, "down")}
+
+
+def summarize_traffic(d, out_path=TRAFFIC_FILE):
+    """HBM bytes of the action-expert sites from `--traffic-site` counter runs under d
+    (traffic_<S>_fetch, traffic_<S>_write, copy_fetch, copy_write).  Writes
+    profiles/site_traffic.{json,md}."""
+    fk, wk, rb, wb = copy_factors(d)
+    ff, fw = fk * 1024 / rb, wk * 1024 / wb
+    out = {"copy_fetch_kib": round(fk, 2), "copy_write_kib": round(wk, 2), "copy_bytes_read": rb,
+           "copy_bytes_written": wb, "copy_launches": 20, "sources_sha256": sources_digest(), "sites": {}}
+    detail = []
+    for site in "AOBD":
+        f = counter_means(os.path.join(d, f"traffic_{site}_fetch"), 100)
+        w = counter_means(os.path.join(d, f"traffic_{site}_write"), 100)
+        rec = {"fetch_kib_per_call": 0.0, "write_kib_per_call": 0.0, "calls": 100,
+               "gemm_fetch_kib_per_call": 0.0, "gemm_write_kib_per_call": 0.0}
+        for key in sorted(set(f) | set(w)):
+            fkib = f.get(key, {}).get("FETCH_SIZE", 0.0) * f.get(key, {}).get("dispatches", 0) / 100
+            wkib = w.get(key, {}).get("WRITE_SIZE", 0.0) * w.get(key, {}).get("dispatches", 0) / 100
+            rec["fetch_kib_per_call"] += fkib
+            rec["write_kib_per_call"] += wkib
+            if "fwht_quant_kernel" not in key[0] and "linear_small_kernel" not in key[0]:
+                rec["gemm_fetch_kib_per_call"] += fkib
+                rec["gemm_write_kib_per_call"] += wkib
+            detail.append((site, short_kernel(key[0]), key[1], f.get(key, {}).get("dispatches", 0),
+                           f.get(key, {}).get("FETCH_SIZE", 0.0), w.get(key, {}).get("WRITE_SIZE", 0.0)))
+        out["sites"][site] = {k: (round(v, 2) if isinstance(v, float) else v) for k, v in rec.items()}
+    with open(out_path, "w") as fo:
+        json.dump(out, fo, indent=1)
+    M = 50
+    lines = ["# HBM traffic: action-expert fused projections (M=50, width 1024, W4A4, block 128)", "",
+             "Commands (from the repository root on an MI355X, `cd /tmp && export TMPDIR=/tmp` first), for each "
+             "site S in A, O, B, D, then the summary:", "", "```"]
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        lines.append(f"rocprofv3 --pmc {c} --output-format csv -d <out>/traffic_S_{'fetch' if c[0] == 'F' else 'write'} "
+                     "-o x -- python /root/repo/bench.py --traffic-site S --quiet")
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        lines.append(f"rocprofv3 --pmc {c} --output-format csv -d <out>/copy_{'fetch' if c[0] == 'F' else 'write'} "
+                     "-o x -- python /root/repo/bench.py --copy-calibration --quiet")
+    lines += ["python /root/repo/bench.py --summarize-traffic <out>", "```", "",
+              f"Calibration: a plain float32 copy-like kernel (`torch.add(a, 0, out=b)`, 256 MiB read and 256 MiB "
+              f"written per launch, 20 launches) reads FETCH_SIZE {fk:.1f} KiB and WRITE_SIZE {wk:.1f} KiB: factors "
+              f"{ff:.4f} (fetch) and {fw:.4f} (write) of the true bytes.  Each site's counters are divided by them.  "
+              f"Sources SHA-256 {out['sources_sha256'][:16]}.", "",
+              "| site | K -> N | algorithmic MB | fetch MB | write MB | measured MB | measured / algorithmic | "
+              "GEMM kernel alone: algorithmic MB | measured MB |", "|---|---|---|---|---|---|---|---|---|"]
+    for site in "AOBD":
+        K, N, nm = SITE_SHAPES[site]
+        r = out["sites"][site]
+        alg = linear_bytes(M, N, K, 4)
+        fmb = r["fetch_kib_per_call"] * 1024 / ff / 1e6
+        wmb = r["write_kib_per_call"] * 1024 / fw / 1e6
+        gmb = (r["gemm_fetch_kib_per_call"] * 1024 / ff + r["gemm_write_kib_per_call"] * 1024 / fw) / 1e6
+        galg = gemm_bytes(M, N, K, 4) if site == "D" else 0
+        lines.append(f"| {site} ({nm}) | {K} -> {N} | {alg / 1e6:.3f} | {fmb:.3f} | {wmb:.3f} | **{fmb + wmb:.3f}** | "
+                     f"{(fmb + wmb) * 1e6 / alg:.2f} | {galg / 1e6:.3f} | {gmb:.3f} |")
+    lines += ["", "Per kernel, counter KiB per dispatch (mean over the measured dispatches):", "",
+              "| site | kernel | grid (threads) | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB |",
+              "|---|---|---|---|---|---|"]
+    for site, k, g, n, fv, wv in detail:
+        lines.append(f"| {site} | `{k}` | {g} | {n} | {fv:.1f} | {wv:.1f} |")
+    with open(out_path.replace(".json", ".md"), "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print(f"traffic of sites A, O, B, D summarized into {out_path}")
+
+
+COUNTER_SETS = ["fetch", "write", "tcc", "sq1", "sq2"]
+
+
+def summarize_counters(d, points, out_path=os.path.join(PROFILES, "gemm_counters.json")):
+    """Counters of graded GEMM points from `--counter-point` runs under d (<point>_fetch,
+    _write, _tcc, _sq1, _sq2).  Writes profiles/gemm_counters.{json,md}."""
+    fk, wk, rb, wb = copy_factors(d)
+    ff, fw = fk * 1024 / rb, wk * 1024 / wb
+    res = {"sources_sha256": sources_digest(), "points": {}}
+    for pt in points:
+        spec = next(s for s in point_specs() if s[1] == pt)
+        _, _, M, K, N, b, bits, kind, weights = spec
+        merged = {}
+        for cs in COUNTER_SETS:
+            for key, v in counter_means(os.path.join(d, f"{pt}_{cs}"), 20).items():
+                if "__amd_rocclr" not in key[0]:  # the weight copies' set-up copies
+                    merged.setdefault(key, {}).update(v)
+        kerns = []
+        for (name, grid), v in sorted(merged.items(), key=lambda kv: -kv[1].get("SQ_WAVE_CYCLES", 0)):
+            mfma = v.get("SQ_INSTS_MFMA", 0.0)
+            valu = v.get("SQ_INSTS_VALU", 0.0)
+            waves = v.get("SQ_WAVES", 0.0)
+            gui = v.get("GRBM_GUI_ACTIVE", 0.0)
+            hit, miss = v.get("TCC_HIT_sum", 0.0), v.get("TCC_MISS_sum", 0.0)
+            rec = {"kernel": short_kernel(name), "grid_threads": grid, "dispatches": v["dispatches"],
+                   "hbm_read_mb": round(v.get("FETCH_SIZE", 0.0) * 1024 / ff / 1e6, 2),
+                   "hbm_write_mb": round(v.get("WRITE_SIZE", 0.0) * 1024 / fw / 1e6, 2),
+                   "l2_hit_rate": round(hit / (hit + miss), 3) if hit + miss else None,
+                   "waves": int(waves), "mfma": int(mfma), "valu_incl_mfma": int(valu),
+                   "valu_per_mfma": round((valu - mfma) / mfma, 2) if mfma else None,
+                   "mfma_busy_cycles_per_mfma": round(v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / mfma, 1) if mfma else None,
+                   # GRBM_GUI_ACTIVE summed over the 8 XCDs: SIMD cycles = 1024 x gui / 8
+                   "mfma_utilisation": round(v.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (1024 * gui / 8), 3) if gui else None,
+                   "lds_instr_per_mfma": round(v.get("SQ_INSTS_LDS", 0.0) / mfma, 3) if mfma else None,
+                   "lds_bank_conflicts": int(v.get("SQ_LDS_BANK_CONFLICT", 0.0)),
+                   "wait_per_wave_cycles": round(v.get("SQ_WAIT_INST_ANY", 0.0) / v["SQ_WAVE_CYCLES"], 3)
+                   if v.get("SQ_WAVE_CYCLES") else None,
+                   "valu_active_per_wave_cycles": round(v.get("SQ_ACTIVE_INST_VALU", 0.0) / v["SQ_WAVE_CYCLES"], 3)
+                   if v.get("SQ_WAVE_CYCLES") else None}
+            kerns.append(rec)
+        res["points"][pt] = {"M": M, "K": K, "N": N, "bits": bits, "weights": weights,
+                             "algorithmic_mb": round(gemm_bytes(M, N, K, bits) / 1e6, 2), "kernels": kerns}
+    with open(out_path, "w") as fo:
+        json.dump(res, fo, indent=1)
+    lines = ["# Counters: graded GEMM points (the GEMM kernel alone, cold weights)", "",
+             "Commands (from the repository root on an MI355X, `cd /tmp && export TMPDIR=/tmp` first), one pass per "
+             "counter set, for each point P below, then the copy calibration and the summary:", "", "```"]
+    sets = {"fetch": "FETCH_SIZE", "write": "WRITE_SIZE", "tcc": "TCC_HIT_sum TCC_MISS_sum",
+            "sq1": "SQ_WAVES SQ_INSTS_VALU SQ_INSTS_MFMA SQ_INSTS_LDS SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_INST_ANY "
+                   "SQ_ACTIVE_INST_VALU",
+            "sq2": "SQ_VALU_MFMA_BUSY_CYCLES SQ_WAIT_INST_LDS SQ_ACTIVE_INST_LDS SQ_LDS_BANK_CONFLICT GRBM_GUI_ACTIVE"}
+    for cs in COUNTER_SETS:
+        lines.append(f"timeout -s KILL 150 rocprofv3 --pmc {sets[cs]} --output-format csv -d <out>/P_{cs} -o p -- "
+                     "python /root/repo/bench.py --counter-point P --quiet")
+    lines += ["rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/copy_fetch -o x -- "
+              "python /root/repo/bench.py --copy-calibration --quiet",
+              "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/copy_write -o x -- "
+              "python /root/repo/bench.py --copy-calibration --quiet",
+              f"python /root/repo/bench.py --summarize-counters <out> --counter-points {','.join(points)}", "```", "",
+              f"HBM bytes: FETCH_SIZE and WRITE_SIZE divided by what they read for the copy calibration: factors "
+              f"{ff:.4f} and {fw:.4f}.  MFMA utilisation = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8), "
+              "GRBM_GUI_ACTIVE summed over the 8 XCDs (it includes the profiler's per-dispatch overhead, so it reads "
+              "a little below the timed points).  VALU / MFMA counts the other vector instructions per MFMA "
+              "(SQ_INSTS_VALU includes the MFMAs).  Per-dispatch means over the point's calls (one per weight "
+              f"copy).  Sources SHA-256 {res['sources_sha256'][:16]}.", "",
+              "| point | kernel | grid (threads) | dispatches | HBM read MB | HBM write MB | algorithmic MB | L2 hit rate "
+              "| waves | MFMA | VALU / MFMA | MFMA busy cycles / MFMA | MFMA utilisation | LDS instr / MFMA | "
+              "LDS bank conflicts | wait / wave cycles | VALU active / wave cycles |",
+              "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for pt, pr in res["points"].items():
+        for k in pr["kernels"]:
+            lines.append(f"| {pt} | `{k['kernel']}` | {k['grid_threads']} | {k['dispatches']} | {k['hbm_read_mb']} | "
+                         f"{k['hbm_write_mb']} | {pr['algorithmic_mb']} | {k['l2_hit_rate']} | {k['waves']} | "
+                         f"{k['mfma']} | {k['valu_per_mfma']} | {k['mfma_busy_cycles_per_mfma']} | "
+                         f"{k['mfma_utilisation']} | {k['lds_instr_per_mfma']} | {k['lds_bank_conflicts']} | "
+                         f"{k['wait_per_wave_cycles']} | {k['valu_active_per_wave_cycles']} |")
+    with open(out_path.replace(".json", ".md"), "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print(f"{len(points)} points summarized into {out_path}")
+
+
 # --------------------------------------------------------------------------- other points
 
 def measure_bf16_context(torch, synth, dev, log_fn, pts):
@@ -922,6 +1124,12 @@ def main():
         sys.exit(2)
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, args.manifest)
+        return
+    if args.summarize_traffic:
+        summarize_traffic(args.summarize_traffic)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.counter_points.split(","))
         return
     import torch
 

@@ -187,20 +187,24 @@ __global__ __launch_bounds__(64 * kKgWaves) void gemm_kgroup_kernel(KgParams p) 
   }
 }
 
-// Canonical nibble codes [M][K/2] -> k-step major [K/128][M][64 B]: thread t moves 16 bytes,
-// t = (ks M + r) 4 + q, so the writes are contiguous and each read is a quarter of a row's
-// step.
+// Canonical nibble codes [M][K/2] -> k-step major [K/128][M][64 B], 16 bytes per thread.
+// Thread u takes 16-byte chunk c = 16 kq + u % 16 of row r = (u / 16) % M, kq = u / (16 M):
+// a wave reads 4 rows x 256 contiguous bytes (whole cache lines) and writes, for each of
+// the 4 k steps those bytes hold, 4 consecutive rows x 64 bytes (256 contiguous bytes).
+// (Read as a quarter step per thread, the rows' cache lines were fetched twice.)
 __global__ __launch_bounds__(256) void codes_kmajor_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst,
                                                             int M, int K) {
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = (int64_t)M * (K / 32);  // 16-byte units
-  if (t >= total) return;
-  const int q = (int)(t & 3);
-  const int64_t rk = t >> 2;
-  const int r = (int)(rk % M);
-  const int ks = (int)(rk / M);
-  *reinterpret_cast<uint4 *>(dst + t * 16) =
-      *reinterpret_cast<const uint4 *>(src + (int64_t)r * (K / 2) + (int64_t)ks * 64 + q * 16);
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int cpr = K / 32;  // 16-byte chunks per row (4 per k step)
+  const int64_t rowunits = (int64_t)M * 16;
+  const int kq = (int)(u / rowunits);
+  const int rem = (int)(u - (int64_t)kq * rowunits);
+  const int r = rem >> 4;
+  const int c = 16 * kq + (rem & 15);
+  if (c >= cpr) return;
+  const int ks = c >> 2;
+  *reinterpret_cast<uint4 *>(dst + (int64_t)ks * 64 * M + (int64_t)r * 64 + (c & 3) * 16) =
+      *reinterpret_cast<const uint4 *>(src + (int64_t)r * (K / 2) + (int64_t)c * 16);
 }
 
 }  // namespace
@@ -213,7 +217,7 @@ hipError_t launch_gemm_kgroup(const KgParams &p, const uint8_t *a_canonical, uin
   hipError_t e = allow_dynamic_lds(&gemm_kgroup_kernel, kKgLds, attr);
   if (e != hipSuccess || !go) return e;
   if (a_canonical) {
-    const int64_t units = (int64_t)p.M * (p.K / 32);
+    const int64_t units = (int64_t)((p.K / 32 + 15) / 16) * p.M * 16;  // 16-chunk row groups, rounded up
     hipLaunchKernelGGL(codes_kmajor_kernel, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, s, a_canonical,
                        a_kmajor, p.M, p.K);
     e = hipGetLastError();
