@@ -33,6 +33,9 @@ point in the committed rocprofv3 summary (profiles/points_kernels_by_grid.json, 
   python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-points] [--points GROUPS]
   python bench.py --rocprof-points           (under rocprofv3 --kernel-trace --stats)
   python bench.py --summarize-trace CSV --manifest STDOUT_OF_THAT_RUN
+  python bench.py --traffic-site S | --counter-point P | --copy-calibration   (under rocprofv3 --pmc)
+  python bench.py --summarize-traffic DIR | --summarize-counters DIR --counter-points P,...
+  python bench.py --summarize-stats CSV --bench-json STDOUT_OF_A_TRACED_DEFAULT_RUN
 """
 from __future__ import annotations
 
@@ -85,6 +88,9 @@ def parse():
     ap.add_argument("--summarize-counters", default=None, metavar="DIR",
                     help="summarize --counter-point counter runs under DIR into profiles/ and exit")
     ap.add_argument("--counter-points", default=None, help="comma-separated points for --summarize-counters")
+    ap.add_argument("--summarize-stats", default=None, metavar="CSV",
+                    help="write profiles/bench_kernel_stats.md from a --stats kernel summary of the default run and exit")
+    ap.add_argument("--bench-json", default=None, help="stdout of the traced run, for --summarize-stats")
     ap.add_argument("--points", default=None, help="comma-separated point groups to run (default: all)")
     return ap.parse_args()
 
@@ -662,6 +668,40 @@ def summarize_traffic(d, out_path=TRAFFIC_FILE):
     print(f"traffic of sites A, O, B, D summarized into {out_path}")
 
 
+def summarize_stats(stats_csv, bench_json, out_path=os.path.join(PROFILES, "bench_kernel_stats.md")):
+    """profiles/bench_kernel_stats.md from the --stats kernel summary of the default bench run
+    under a kernel trace (and that run's JSON line, for its step time)."""
+    import csv
+    with open(stats_csv) as f:
+        rows = list(csv.DictReader(f))
+    step_us = None
+    with open(bench_json) as f:
+        for line in f:
+            if line.startswith('{"metric"'):
+                step_us = json.loads(line)["ms_per_step"] * 1e3
+    lines = ["# Kernel statistics of the benchmark's own run (rocprofv3 --kernel-trace --stats)", "",
+             "Commands (from the repository root on an MI355X, `cd /tmp && export TMPDIR=/tmp` first):", "", "```",
+             "rocprofv3 --kernel-trace --stats --output-format csv -d <out> -o bench -- python /root/repo/bench.py "
+             "> <out>/bench.json",
+             "python /root/repo/bench.py --summarize-stats <out>/<host>/bench_kernel_stats.csv --bench-json <out>/bench.json",
+             "```", "",
+             "The whole default run: the 10-step denoising loop (warm-up, timed steps), the cold step and sites, the "
+             "graded block, every point, the chain, the CPU baseline.  Each kernel's average is over every launch of "
+             "that instantiation in the run, across all the shapes it served (the per-point, per-grid figures are in "
+             "`points_kernels_by_grid.md`).  Under a full kernel trace every graph launch carries its own completion "
+             "signal and timestamps, so this run's own step time"
+             + (f" ({step_us:.1f} us)" if step_us else "") + " is not comparable with an untraced run; its kernel "
+             f"durations are.  Sources SHA-256 {sources_digest()[:16]}.", "",
+             "| kernel | calls | total ms | average us | min us | max us | share |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| `{r['Name'][:110]}` | {r['Calls']} | {int(r['TotalDurationNs']) / 1e6:.2f} | "
+                     f"{float(r['AverageNs']) / 1e3:.3f} | {int(r['MinNs']) / 1e3:.3f} | {int(r['MaxNs']) / 1e3:.3f} | "
+                     f"{float(r['Percentage']):.1f}% |")
+    with open(out_path, "w") as fo:
+        fo.write("\n".join(lines) + "\n")
+    print(f"{len(rows)} kernels summarized into {out_path}")
+
+
 COUNTER_SETS = ["fetch", "write", "tcc", "sq1", "sq2"]
 
 
@@ -1130,6 +1170,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters, args.counter_points.split(","))
+        return
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats, args.bench_json)
         return
     import torch
 
