@@ -57,6 +57,18 @@ __device__ __forceinline__ uint2 pack_chunk_nibbles_biased(const uint32_t (&c)[1
   return make_uint2(w[0], w[1]);
 }
 
+// 8 biased bit patterns (channels 0..7, see quantize_bits_biased) straight to the INT4
+// MFMA operand words, the form widen_nibbles gives from the packed nibbles: lo holds
+// 16 * {c0, c2, c4, c6}, hi 16 * {c1, c3, c5, c7}, one int8 lane each.  Two shift-ors and a
+// byte permute gather four (code + 8) bytes; shifting them up a nibble gives 16 (code + 8),
+// and xor 0x80 per byte subtracts the 128 (mod 256).
+__device__ __forceinline__ void widen_biased8(const uint32_t *b, uint32_t &lo, uint32_t &hi) {
+  const uint32_t le = __builtin_amdgcn_perm(lshl_or<8>(b[6], b[4]), lshl_or<8>(b[2], b[0]), 0x05040100u);
+  const uint32_t ho = __builtin_amdgcn_perm(lshl_or<8>(b[7], b[5]), lshl_or<8>(b[3], b[1]), 0x05040100u);
+  lo = (le << 4) ^ 0x80808080u;
+  hi = (ho << 4) ^ 0x80808080u;
+}
+
 // Pack 16 quantized bit patterns (natural channel order; low byte = code) into canonical
 // nibbles (8 bytes: channel 2i in the low nibble of byte i) or int8 (16 bytes).
 __device__ __forceinline__ uint2 pack_chunk_nibbles(const int (&c)[16]) {

@@ -206,42 +206,50 @@ __global__ __launch_bounds__(kSmallThreads) void linear_small_kernel(SmallParams
     const float inv = (zero ? 0.0f : qf / rA) * row_sign<CW>(p.log2b, t);  // see lane_stage
     if (t == 0) dl[r] = zero ? 0.0f : (rA * p.cb) / qf;
     const float lim = qf + 0.49f;
+    // no clamp at r = 1 (|u * inv| < q + 1/2; see quantize_bits_biased) unless inv is not finite
+    const bool clamp = p.clip_ratio != 1.0f || !__builtin_isfinite(inv);
     uint8_t *row_l = al + r * K;
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       const int j = c * TPR + t;
       if (j < nch) {
-        int cc[CW];
-#pragma unroll
-        for (int i = 0; i < CW; ++i) cc[i] = quantize_bits(v[c][i], inv, lim);
-        // the chunk's part of one MFMA operand (16 channels, stored as the MFMA consumes
+        // the chunk's part of one MFMA operand (CW channels, stored as the MFMA consumes
         // it: INT4 widened to int8 x 16, INT8 as is), at its place in the row's k step
-        if constexpr (CW == 16) {
-          uint4 op;
-          if constexpr (BITS == 4) {
-            const v4i wdn = widen8(__builtin_bit_cast(v2i, pack_chunk_nibbles(cc)));
-            op = make_uint4((uint32_t)wdn.x, (uint32_t)wdn.y, (uint32_t)wdn.z, (uint32_t)wdn.w);
-          } else {
-            op = pack_chunk_int8(cc);
-          }
-          *reinterpret_cast<uint4 *>(row_l + code_unit(r, j) * 16) = op;
-        } else {
-          uint2 op;
-          if constexpr (BITS == 4) {
-            uint32_t b4[4];
+        if constexpr (BITS == 4) {
+          uint32_t cb[CW];
+          if (clamp) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) b4[i] = ((uint32_t)cc[2 * i] & 0xFu) | ((uint32_t)cc[2 * i + 1] << 4);
-            const uint32_t w = __builtin_amdgcn_perm(b4[1], b4[0], 0x0c0c0400u) | __builtin_amdgcn_perm(b4[3], b4[2], 0x04000c0cu);
-            uint32_t lo, hi;
-            widen_nibbles(w, lo, hi);
-            op = make_uint2(lo, hi);
+            for (int i = 0; i < CW; ++i) cb[i] = quantize_bits_biased<true>(v[c][i], inv, lim);
           } else {
+#pragma unroll
+            for (int i = 0; i < CW; ++i) cb[i] = quantize_bits_biased<false>(v[c][i], inv, lim);
+          }
+          uint32_t w[CW / 4];
+#pragma unroll
+          for (int h = 0; h < CW / 8; ++h) widen_biased8(cb + 8 * h, w[2 * h], w[2 * h + 1]);
+          if constexpr (CW == 16)
+            *reinterpret_cast<uint4 *>(row_l + code_unit(r, j) * 16) = make_uint4(w[0], w[1], w[2], w[3]);
+          else
+            *reinterpret_cast<uint2 *>(row_l + code_unit(r, j >> 1) * 16 + (j & 1) * 8) = make_uint2(w[0], w[1]);
+        } else {
+          int cc[CW];
+          if (clamp) {
+#pragma unroll
+            for (int i = 0; i < CW; ++i) cc[i] = quantize_bits(v[c][i], inv, lim);
+          } else {
+#pragma unroll
+            for (int i = 0; i < CW; ++i) cc[i] = __float_as_int(v[c][i] * inv + 12582912.0f);
+          }
+          if constexpr (CW == 16) {
+            *reinterpret_cast<uint4 *>(row_l + code_unit(r, j) * 16) = pack_chunk_int8(cc);
+          } else {
+            uint2 op;
             op.x = __builtin_amdgcn_perm((uint32_t)cc[1], (uint32_t)cc[0], 0x0c0c0400u) |
                    __builtin_amdgcn_perm((uint32_t)cc[3], (uint32_t)cc[2], 0x04000c0cu);
             op.y = __builtin_amdgcn_perm((uint32_t)cc[5], (uint32_t)cc[4], 0x0c0c0400u) |
                    __builtin_amdgcn_perm((uint32_t)cc[7], (uint32_t)cc[6], 0x04000c0cu);
+            *reinterpret_cast<uint2 *>(row_l + code_unit(r, j >> 1) * 16 + (j & 1) * 8) = op;
           }
-          *reinterpret_cast<uint2 *>(row_l + code_unit(r, j >> 1) * 16 + (j & 1) * 8) = op;
         }
       }
     }
