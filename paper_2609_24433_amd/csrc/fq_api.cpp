@@ -157,7 +157,7 @@ fq_status gemm_common(const void *a_codes, int a_fmt, int64_t lda, const float *
                       const void *w_packed, const float *w_scale, const float *bias, void *y,
                       int64_t ldy, int32_t *acc_out, int64_t M, int64_t N, int64_t K, int bits,
                       void *ws, size_t ws_bytes, hipStream_t stream, bool go = true) {
-  const fq::GemmPlan pl = fq::plan_gemm(M, N, K, bits);
+  const fq::GemmPlan pl = fq::plan_gemm(M, N, K, bits, a_fmt == fq::kANibbleKM);
   const size_t need = fq::gemm_plan_workspace(pl) + (a_fmt == fq::kANibble ? fq::gemm_plan_relayout_bytes(pl, M, K) : 0);
   if (need > 0 && (!ws || ws_bytes < need))
     return fail(FQ_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need, ws ? ws_bytes : (size_t)0);
@@ -209,7 +209,7 @@ size_t linear_ws_bytes(int64_t M, int64_t N, int64_t K, int bits) {
   if (M <= 0 || N <= 0 || K < 128 || (bits != 4 && bits != 8)) return 0;
   if (fq::plan_small(M, N, K, bits).ok) return 0;
   return align256((size_t)M * (size_t)K * (size_t)bits / 8) + align256((size_t)M * 4) +
-         fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits));
+         fq::gemm_plan_workspace(fq::plan_gemm(M, N, K, bits, bits == 4));
 }
 
 int log2_pow2(int b) {
@@ -274,7 +274,7 @@ fq_status linear_common(const void *x_bf16, int64_t ldx, const float *smooth_inv
   // per-step cost in the GEMMs, which widen them in registers), canonical or, for the
   // k-group GEMM, k-step major; W8A8 codes are int8.
   const bool nibble = bits == 4;
-  const bool kmajor = nibble && fq::plan_gemm(M, N, K, bits).kind == 3;
+  const bool kmajor = nibble && fq::plan_gemm(M, N, K, bits, true).kind == 3;
   const int fmt = nibble ? (kmajor ? fq::kOutNibbleKM : fq::kOutNibble) : fq::kOutInt8;
   const int afmt = nibble ? (kmajor ? fq::kANibbleKM : fq::kANibble) : fq::kAInt8;
   const int64_t lda = nibble ? K / 2 : K;

@@ -994,7 +994,7 @@ static constexpr size_t tile_lds_bytes() {
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits, bool kmajor_codes) {
   GemmPlan pl{};
   const int ktot = (int)(K / kTileK);
   if (M <= 64) {
@@ -1069,10 +1069,16 @@ GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits) {
     // kernel).  Measured at M = 816, K 16384 -> N 2048 against the split 128 x 128 plan:
     // 31 against 43 us on one GPU (fed k-step-major codes).  Short K (fewer than 64 steps
     // per tile) and grids of fewer than 160 tiles stay on the LDS-ring kernel below.
-    if (bits == 4 && ktot >= 64) {
+    // With k-step-major codes for free (no conversion kernel), grids of up to 1023 such
+    // tiles at K >= 16384 take it too: K 16384 -> N 2048 at M = 1600 / 2048 / 3072 in
+    // 56.5 / 58.3 / 85.4 against 63.3 / 64.1 / 103.8 us on the LDS-ring kernel; at 1024
+    // tiles (M = 4096) the two measured the same and at K = 8192 the ring kernel led.
+    // Byte offsets into the codes and the weights are 32-bit in that kernel.
+    if (bits == 4 && ktot >= 64 && M * K / 2 < (int64_t(1) << 31) && N * K / 2 < (int64_t(1) << 31)) {
       const int64_t t128 = ((M + 127) / 128) * ((N + 127) / 128);
       const int64_t tkg = ((M + 127) / 128) * ((N + 63) / 64);
-      if (t128 < 200 && tkg >= 160) {
+      const bool wide = kmajor_codes && ktot >= 128 && tkg < 1024;
+      if ((t128 < 200 || wide) && tkg >= 160) {
         pl.kind = 3;
         pl.tiles = tkg;
         pl.splits = 1;

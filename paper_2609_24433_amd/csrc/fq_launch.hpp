@@ -73,7 +73,9 @@ struct GemmPlan {
   size_t partial_bytes; // split-K INT32 partials [splits][M][N]
 };
 
-GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits);
+// kmajor_codes: the caller writes the activation codes k-step major at no extra cost (the
+// fused projection's prologue), which widens the k-group plan's range
+GemmPlan plan_gemm(int64_t M, int64_t N, int64_t K, int bits, bool kmajor_codes = false);
 // scratch of the GEMM itself (split-K partials); a kind-3 plan fed canonical codes also
 // needs gemm_plan_relayout_bytes for their k-step-major copy
 size_t gemm_plan_workspace(const GemmPlan &pl);

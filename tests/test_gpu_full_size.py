@@ -159,3 +159,24 @@ def test_down_proj_sweep(M, b, bits):
     flush(f"full size: {wl.name}")
     x = wl.site_activation("D", 0)
     run_and_check(x, wl.projection_weight(p), b, bits, rows=sample_rows(M, seed=M + b))
+
+
+# ------------------------------------------------------------------ k-group plan, fused path
+
+@pytest.mark.parametrize("M,N", [(1700, 2000), (3072, 2048)])
+def test_fused_kgroup_wide_plan_sampled(M, N):
+    """A fused projection whose prologue writes the codes k-step major takes the k-group
+    GEMM on grids of up to 1023 tiles of 128 x 64 at K = 16384, where the GEMM entry point
+    (canonical codes) keeps the LDS-ring kernel: ragged rows and columns against the oracle
+    on sampled rows, and the two outputs identical bit for bit everywhere."""
+    flush(f"full size: fused k-group plan M={M} K=16384 N={N}")
+    f = fq()
+    K, b, bits = 16384, 128, 4
+    x = synth.activations(M, K, seed=M, outlier_frac=0.005, outlier_scale=50.0)
+    w = synth.weights(N, K, seed=N + 7)
+    y = run_and_check(x, w, b, bits, rows=sample_rows(M, seed=M))
+    lin = f.QuantLinear(torch.from_numpy(w).to(DEV), b, bits)
+    codes, delta = f.fwht_quant(x.to(DEV), b, bits)
+    y2 = f.gemm(codes, delta, lin.w_packed, lin.w_scale, N, K, bits)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
