@@ -1,8 +1,6 @@
 // Tiled INT4 GEMM for a few hundred to ~1000 tokens at long K (eq. (8) contraction and
 // rescale), where 128 x 128 output tiles would leave most compute units idle unless K is
-// split across workgroups (and a second kernel adds the slices); in the fused projection,
-// whose prologue writes its codes k-step major, also up to a few thousand tokens at
-// K >= 16384, where its 128 x 64 tiles balance better than the LDS-ring kernel's.
+// split across workgroups (and a second kernel adds the slices).
 //
 // Workgroup: 4 waves, one 128 x 64 output tile (8 x 4 tiles of 16 x 16); wave w owns the
 // k steps w, w + 4, w + 8, ... of the whole of K, so the tile needs no split of K across
