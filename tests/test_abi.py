@@ -52,6 +52,26 @@ def test_sizes():
         assert fq.gemm_workspace_bytes(M, 2048, 16384, 4) % 256 == 0
 
 
+def _a256(n):
+    return (n + 255) // 256 * 256
+
+
+def test_plan_workspaces():
+    """The workspaces pin the launch plans of the long-K W4A4 projection (K 16384 -> N 2048):
+    the k-group GEMM needs no split-K partials; the GEMM entry point feeds it a k-step-major
+    copy of the canonical codes (M = 816), the fused projection's prologue writes that
+    order itself (M = 816 .. 3072); M = 2048 and 4096 through the GEMM entry point take the
+    LDS-ring kernel unsplit."""
+    K, N = 16384, 2048
+    assert fq.gemm_workspace_bytes(816, N, K, 4) == _a256(816 * K // 2)
+    for M in (2048, 4096):
+        assert fq.gemm_workspace_bytes(M, N, K, 4) == 0
+    for M in (816, 1600, 2048, 3072, 4096):
+        assert fq.linear_workspace_bytes(M, N, K, 4) == _a256(M * K // 2) + _a256(M * 4)
+    # W8A8 at M = 816 splits K in two: int32 partials [2][M][N]
+    assert fq.gemm_workspace_bytes(816, N, K, 8) == _a256(2 * 816 * N * 4)
+
+
 def call_quant(x=FAKE, ldx=1024, smooth=NULL, M=4, K=1024, b=64, bits=4, r=1.0, codes=FAKE, delta=FAKE,
                post=NULL):
     return fq.LIB.fq_fwht_quant(x, ldx, smooth, post, M, K, b, bits, r, codes, delta, None)
